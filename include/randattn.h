@@ -1,0 +1,242 @@
+/*
+ * randattn.h -- C ABI of the Random Attention decode hot path on MI355X.
+ *
+ * Random Attention (Section 3 of the paper) keeps, per KV head, the prompt
+ * and the r most recent pairs, and evicts the other cached pairs uniformly
+ * at random down to a budget, with no scoring pass.  This library holds the
+ * compressed per-KV-head cache in caller-owned device memory and exposes the
+ * three operations of the problem statement:
+ *   - append one key/value pair per decode step (Section 2, periodic
+ *     eviction paragraph: each decode step appends one pair);
+ *   - evict per KV head to the budget, reproducibly from a per-request seed
+ *     (Eq. 1; Section 3; Appendix F; Appendix H "Statistics and randomness");
+ *   - grouped-query decode attention over the kept pairs (Section 2,
+ *     "Notation"; Appendix F: query groups share their KV head's keep-set).
+ *
+ * Conventions for every call
+ * --------------------------
+ * - Pointers named dev_* / pools / q / out / workspace are DEVICE pointers
+ *   (hipMalloc or torch CUDA tensors, 16-byte aligned); pointers named
+ *   host_* are host memory.  `stream` is a hipStream_t passed as void*
+ *   (NULL = the null stream).  All calls are asynchronous on `stream` unless
+ *   marked synchronous.
+ * - The library never allocates device memory.  The caller owns the pools,
+ *   the metadata buffer and the workspace and must keep them alive until
+ *   ra_cache_destroy.  One ra_cache must be driven from one stream (calls
+ *   are stream-ordered); it is not thread-safe.
+ * - Every call returns an ra_status.  Shapes, capacities, budgets and the
+ *   step protocol are validated on the host mirror BEFORE any launch, so an
+ *   error leaves device state untouched.  A failed launch returns
+ *   RA_ERR_HIP (ra_last_hip_error gives the hipError_t).  Nothing throws
+ *   across the ABI.
+ * - head_dim must be 128; dtype f32 or bf16 (keys, values, queries and
+ *   outputs all in that dtype); positions are int32.
+ *
+ * Eviction rule (what the kernels compute; the CPU oracle restates it)
+ * -----------------------------------------------------------------
+ * A sequence's prompt positions 0..lp-1 are never evicted.  Decode step t
+ * (1-based) caches position lp+t-1 in every (layer, KV head).  At the end
+ * of step t, if t mod evict_every == 0 and the entries outside prompt and
+ * recent buffer exceed k_keep, eviction event e (0-based count per
+ * sequence) runs in every (layer l, KV head g): the candidates are the
+ * cached positions outside the prompt and the r most recent; each candidate
+ * p gets the 64-bit uniform key = word (p mod 4) of Philox4x64-10 at counter
+ * (p/4, e, l, g) with key (seed, request_id); the m = |C| - k_keep smallest
+ * (key, p) pairs are dropped and the survivors are compacted in place,
+ * chronological order kept.  k_keep = budget_k (RA_BUDGET_EVICTABLE) or
+ * budget_k - lp (RA_BUDGET_TOTAL, the convention of Eq. 1, where the
+ * prompt counts against K).
+ */
+#ifndef RANDATTN_H
+#define RANDATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  RA_OK = 0,
+  RA_ERR_INVALID_ARG = -1,  /* bad pointer, index, shape or config field */
+  RA_ERR_CAPACITY = -2,     /* pool full, or a head region would overflow */
+  RA_ERR_BUDGET = -3,       /* TOTAL mode and the prompt exceeds budget_k */
+  RA_ERR_UNSUPPORTED = -4,  /* valid but not implemented (head_dim, group) */
+  RA_ERR_HIP = -5,          /* a HIP call or kernel launch failed */
+  RA_ERR_STATE = -6         /* call out of protocol order for this state */
+} ra_status;
+
+typedef enum { RA_F32 = 0, RA_BF16 = 1 } ra_dtype;
+
+typedef enum {
+  RA_BUDGET_EVICTABLE = 0,  /* budget_k counts kept non-prompt, non-buffer rows */
+  RA_BUDGET_TOTAL = 1       /* budget_k counts the prompt too (Eq. 1) */
+} ra_budget_mode;
+
+typedef struct {
+  int32_t num_layers;     /* L >= 1 */
+  int32_t num_q_heads;    /* Hq, a multiple of Hkv */
+  int32_t num_kv_heads;   /* Hkv >= 1; group G = Hq / Hkv, G <= 16 */
+  int32_t head_dim;       /* d; must be 128 */
+  int32_t budget_k;       /* K >= 0 (see budget_mode) */
+  int32_t recent_r;       /* r >= 0: the buffer of most recent pairs (64) */
+  int32_t evict_every;    /* R in [1, 1024]: trigger period in steps (64) */
+  int32_t budget_mode;    /* ra_budget_mode */
+  int32_t dtype;          /* ra_dtype */
+  int32_t max_seqs;       /* sequence slots, [1, 65536] */
+  int32_t attn_split;     /* keys per attention work item (multiple of 32),
+                             0 = chosen by the library */
+} ra_config;
+
+typedef struct ra_cache ra_cache;   /* host-side descriptor + host mirror */
+
+typedef struct {
+  int32_t active;       /* 1 if the slot holds a sequence */
+  int32_t prompt_len;   /* lp */
+  int32_t len;          /* cached rows per (layer, KV head) between steps */
+  int32_t step;         /* completed decode steps */
+  int32_t event;        /* eviction events performed */
+  int32_t k_keep;       /* evictable rows kept per head */
+  int32_t cap;          /* row capacity of each (layer, KV head) region */
+  int64_t base;         /* first pool row of the sequence's regions */
+} ra_seq_info;
+
+/* ---- sizing (pure host functions; no device access) --------------------- */
+
+/* RA_OK if the config is usable. */
+ra_status ra_config_check(const ra_config* cfg);
+
+/* Row capacity of one (layer, KV head) region for a prompt of prompt_len:
+ * lp + k_keep + recent_r + evict_every rounded up to a multiple of 32.
+ * Negative ra_status on error (bad config, TOTAL mode with lp > K). */
+int64_t ra_region_rows(const ra_config* cfg, int32_t prompt_len);
+
+/* Pool rows one sequence occupies: L * Hkv * ra_region_rows.  The K and V
+ * pools hold pool_rows * head_dim elements each, the position pool
+ * pool_rows int32.  Negative ra_status on error. */
+int64_t ra_seq_rows(const ra_config* cfg, int32_t prompt_len);
+
+/* Bytes of the persistent device metadata buffer (per-slot state and
+ * attention completion counters).  0 on a bad config. */
+size_t ra_meta_bytes(const ra_config* cfg);
+
+/* Bytes of the attention workspace (split partial results) that
+ * ra_decode_attention needs.  0 on a bad config. */
+size_t ra_workspace_bytes(const ra_config* cfg);
+
+/* ---- lifetime ----------------------------------------------------------- */
+
+/* Create a cache over caller-owned device buffers:
+ *   k_pool, v_pool: pool_rows * head_dim elements of cfg->dtype each;
+ *   pos_pool:       pool_rows int32;
+ *   meta:           ra_meta_bytes(cfg) bytes (zeroed here on `stream`).
+ * Keys are stored row-major per region; values in tiles of 8 rows stored
+ * transposed ([row/8][head_dim][8]); positions row-major.  Sequences are
+ * placed by a first-fit allocator over the pool at ra_seq_begin. */
+ra_status ra_cache_create(const ra_config* cfg, void* k_pool, void* v_pool,
+                          int32_t* pos_pool, int64_t pool_rows, void* meta,
+                          size_t meta_bytes, void* stream, ra_cache** out);
+
+ra_status ra_cache_destroy(ra_cache* cache);
+
+/* ---- sequences ----------------------------------------------------------- */
+
+/* Pin a prompt into slot `seq` (Section 3: the prompt is never evicted).
+ * dev_k_prompt / dev_v_prompt: [L][Hkv][prompt_len][head_dim] row-major, or
+ * both NULL to leave the prompt rows unwritten (positions are still set;
+ * the rows are then expected from ra_write_rows).  `seed` and `request_id`
+ * key every eviction draw of this sequence.  Errors: RA_ERR_STATE if the
+ * slot is active, RA_ERR_BUDGET (TOTAL mode, lp > K), RA_ERR_CAPACITY if
+ * the pool has no room. */
+ra_status ra_seq_begin(ra_cache* cache, int32_t seq, int32_t prompt_len,
+                       uint64_t seed, uint64_t request_id,
+                       const void* dev_k_prompt, const void* dev_v_prompt,
+                       void* stream);
+
+/* Release slot `seq` and its pool rows. */
+ra_status ra_seq_end(ra_cache* cache, int32_t seq, void* stream);
+
+/* Host mirror of a slot (no device access). */
+ra_status ra_get_seq_info(const ra_cache* cache, int32_t seq, ra_seq_info* out);
+
+/* ---- decode step --------------------------------------------------------- */
+
+/* Append + attend for one layer of every active sequence (Section 2).
+ *   q:     [max_seqs][Hq][d]   this step's queries (inactive slots ignored)
+ *   k_new: [max_seqs][Hkv][d]  this step's key of each KV head
+ *   v_new: [max_seqs][Hkv][d]
+ *   out:   [max_seqs][Hq][d]   written for active slots only
+ *   workspace: ra_workspace_bytes(cfg) bytes of scratch.
+ * Each active sequence caches (k_new, v_new) at position lp + step in every
+ * KV head of `layer`, and query head h attends, with softmax over
+ * q.k/sqrt(d), to every cached pair of KV head h / G, the new one included.
+ * Each layer must be called once per step (RA_ERR_STATE otherwise) and
+ * RA_ERR_CAPACITY is returned before a region would overflow. */
+ra_status ra_decode_attention(ra_cache* cache, int32_t layer, const void* q,
+                              const void* k_new, const void* v_new, void* out,
+                              void* workspace, size_t workspace_bytes,
+                              void* stream);
+
+/* End the decode step of every active sequence: step += 1, then run the
+ * periodic eviction (Eq. 1 with Random Attention's scores, Appendix F
+ * trigger) on every (layer, KV head) of each sequence that is due.
+ * Requires every layer to have been appended this step.  If n_evicted is
+ * non-NULL it receives the number of sequences evicted (host mirror). */
+ra_status ra_end_step(ra_cache* cache, void* stream, int32_t* n_evicted);
+
+/* Run one eviction event on slot `seq` now, whatever the step count, if
+ * its evictable rows exceed k_keep (otherwise a no-op).  Not allowed in
+ * the middle of a step (RA_ERR_STATE). */
+ra_status ra_evict_now(ra_cache* cache, int32_t seq, void* stream);
+
+/* ---- state transfer and audit --------------------------------------------- */
+
+/* Advance every active sequence by n_steps decode steps touching positions
+ * only: each step caches position lp + step and the periodic eviction runs
+ * on the positions exactly as in a real decode, but no key/value rows are
+ * written or moved (rows of newly cached positions are left stale).  Used
+ * to reach a long-generation state quickly; follow with ra_write_rows. */
+ra_status ra_fast_forward(ra_cache* cache, int32_t n_steps, void* stream);
+
+/* Copy slot `seq`'s cached positions, [L][Hkv][len] int32 row-major, to
+ * device memory (dev_out holds at least L*Hkv*len int32). */
+ra_status ra_export_positions(ra_cache* cache, int32_t seq, int32_t* dev_out,
+                              int64_t out_elems, void* stream);
+
+/* Overwrite slot `seq`'s cached rows from row-major device arrays
+ * [L][Hkv][len][d] (row j belongs to the j-th cached position, the order of
+ * ra_export_positions). */
+ra_status ra_write_rows(ra_cache* cache, int32_t seq, const void* dev_k,
+                        const void* dev_v, void* stream);
+
+/* Copy the cached rows of one (seq, layer, KV head) to row-major device
+ * arrays [len][d] (values un-tiled).  Either output may be NULL. */
+ra_status ra_read_rows(ra_cache* cache, int32_t seq, int32_t layer,
+                       int32_t kv_head, void* dev_k_out, void* dev_v_out,
+                       void* stream);
+
+/* SYNCHRONOUS: copy one head's cached positions (ascending) to host
+ * memory; *n_out receives len.  RA_ERR_CAPACITY if host_cap < len (nothing
+ * copied).  Synchronizes `stream`. */
+ra_status ra_read_positions(ra_cache* cache, int32_t seq, int32_t layer,
+                            int32_t kv_head, int32_t* host_out,
+                            int32_t host_cap, int32_t* n_out, void* stream);
+
+/* ---- diagnostics ----------------------------------------------------------- */
+
+const char* ra_status_string(int32_t status);
+
+/* hipError_t of the last failed HIP call in this process (0 if none). */
+int32_t ra_last_hip_error(void);
+
+/* Keys per attention work item and work items per head that the next
+ * ra_decode_attention launch uses (host mirror; for measurement). */
+ra_status ra_attention_plan(const ra_cache* cache, int32_t* split_keys,
+                            int32_t* max_splits);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* RANDATTN_H */

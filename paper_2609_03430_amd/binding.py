@@ -1,0 +1,314 @@
+"""Thin ctypes binding of the C ABI in ``include/randattn.h``.
+
+Argument marshalling only: every function below has the name and argument
+order of the C entry point it wraps, takes torch tensors where the C call
+takes device pointers, takes ``stream=None`` for the current torch stream,
+and raises ``RandAttnError`` on a non-zero status.  All work runs in the HIP
+kernels of ``lib/librandattn.so``; there is no fallback, and a missing or
+unloadable library raises immediately.
+
+``Cache`` is a convenience owner: it sizes and allocates the pools, the
+metadata buffer and the workspace as torch CUDA tensors and keeps them alive
+for the lifetime of the C handle.
+"""
+
+import ctypes
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib",
+                         "librandattn.so")
+
+RA_OK = 0
+RA_ERR_INVALID_ARG = -1
+RA_ERR_CAPACITY = -2
+RA_ERR_BUDGET = -3
+RA_ERR_UNSUPPORTED = -4
+RA_ERR_HIP = -5
+RA_ERR_STATE = -6
+RA_F32, RA_BF16 = 0, 1
+RA_BUDGET_EVICTABLE, RA_BUDGET_TOTAL = 0, 1
+
+# Every entry point declared in include/randattn.h.
+EXPORTS = (
+    "ra_config_check", "ra_region_rows", "ra_seq_rows", "ra_meta_bytes",
+    "ra_workspace_bytes", "ra_cache_create", "ra_cache_destroy",
+    "ra_seq_begin", "ra_seq_end", "ra_get_seq_info", "ra_decode_attention",
+    "ra_end_step", "ra_evict_now", "ra_fast_forward", "ra_export_positions",
+    "ra_write_rows", "ra_read_rows", "ra_read_positions", "ra_status_string",
+    "ra_last_hip_error", "ra_attention_plan",
+)
+
+
+class RandAttnError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        msg = "%s failed: %s (%d)" % (where, status_string(status), status)
+        if status == RA_ERR_HIP:
+            msg += ", hipError %d" % _lib().ra_last_hip_error()
+        super().__init__(msg)
+
+
+class ra_config(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "num_layers", "num_q_heads", "num_kv_heads", "head_dim", "budget_k",
+        "recent_r", "evict_every", "budget_mode", "dtype", "max_seqs",
+        "attn_split")]
+
+
+class ra_seq_info(ctypes.Structure):
+    _fields_ = [("active", ctypes.c_int32), ("prompt_len", ctypes.c_int32),
+                ("len", ctypes.c_int32), ("step", ctypes.c_int32),
+                ("event", ctypes.c_int32), ("k_keep", ctypes.c_int32),
+                ("cap", ctypes.c_int32), ("base", ctypes.c_int64)]
+
+
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_U64 = ctypes.c_uint64
+_SZ = ctypes.c_size_t
+_CFG = ctypes.POINTER(ra_config)
+_SIGS = {
+    "ra_config_check": (_I32, [_CFG]),
+    "ra_region_rows": (_I64, [_CFG, _I32]),
+    "ra_seq_rows": (_I64, [_CFG, _I32]),
+    "ra_meta_bytes": (_SZ, [_CFG]),
+    "ra_workspace_bytes": (_SZ, [_CFG]),
+    "ra_cache_create": (_I32, [_CFG, _P, _P, _P, _I64, _P, _SZ, _P,
+                               ctypes.POINTER(_P)]),
+    "ra_cache_destroy": (_I32, [_P]),
+    "ra_seq_begin": (_I32, [_P, _I32, _I32, _U64, _U64, _P, _P, _P]),
+    "ra_seq_end": (_I32, [_P, _I32, _P]),
+    "ra_get_seq_info": (_I32, [_P, _I32, ctypes.POINTER(ra_seq_info)]),
+    "ra_decode_attention": (_I32, [_P, _I32, _P, _P, _P, _P, _P, _SZ, _P]),
+    "ra_end_step": (_I32, [_P, _P, ctypes.POINTER(_I32)]),
+    "ra_evict_now": (_I32, [_P, _I32, _P]),
+    "ra_fast_forward": (_I32, [_P, _I32, _P]),
+    "ra_export_positions": (_I32, [_P, _I32, _P, _I64, _P]),
+    "ra_write_rows": (_I32, [_P, _I32, _P, _P, _P]),
+    "ra_read_rows": (_I32, [_P, _I32, _I32, _I32, _P, _P, _P]),
+    "ra_read_positions": (_I32, [_P, _I32, _I32, _I32, _P, _I32,
+                                 ctypes.POINTER(_I32), _P]),
+    "ra_status_string": (ctypes.c_char_p, [_I32]),
+    "ra_last_hip_error": (_I32, []),
+    "ra_attention_plan": (_I32, [_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32)]),
+}
+
+_handle = None
+
+
+def library_path():
+    return _LIB_PATH
+
+
+def _lib():
+    """Load the shared library once; raise if it is missing."""
+    global _handle
+    if _handle is None:
+        if not os.path.exists(_LIB_PATH):
+            raise ImportError("%s is not built; run python -m "
+                              "paper_2609_03430_amd.build" % _LIB_PATH)
+        lib = ctypes.CDLL(_LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _handle = lib
+    return _handle
+
+
+def _check(status, where):
+    if status != RA_OK:
+        raise RandAttnError(status, where)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def make_config(num_layers, num_q_heads, num_kv_heads, budget_k, recent_r=64,
+                evict_every=64, budget_mode=RA_BUDGET_EVICTABLE, dtype=RA_BF16,
+                max_seqs=1, head_dim=128, attn_split=0):
+    return ra_config(num_layers, num_q_heads, num_kv_heads, head_dim, budget_k,
+                     recent_r, evict_every, budget_mode, dtype, max_seqs,
+                     attn_split)
+
+
+# ---- one wrapper per C entry point ------------------------------------------
+
+def status_string(status):
+    return _lib().ra_status_string(int(status)).decode()
+
+
+def ra_status_string(status):
+    return status_string(status)
+
+
+def ra_last_hip_error():
+    return _lib().ra_last_hip_error()
+
+
+def ra_config_check(cfg):
+    return _lib().ra_config_check(ctypes.byref(cfg))
+
+
+def ra_region_rows(cfg, prompt_len):
+    return _lib().ra_region_rows(ctypes.byref(cfg), int(prompt_len))
+
+
+def ra_seq_rows(cfg, prompt_len):
+    return _lib().ra_seq_rows(ctypes.byref(cfg), int(prompt_len))
+
+
+def ra_meta_bytes(cfg):
+    return _lib().ra_meta_bytes(ctypes.byref(cfg))
+
+
+def ra_workspace_bytes(cfg):
+    return _lib().ra_workspace_bytes(ctypes.byref(cfg))
+
+
+def ra_cache_create(cfg, k_pool, v_pool, pos_pool, pool_rows, meta, stream=None):
+    out = ctypes.c_void_p()
+    _check(_lib().ra_cache_create(ctypes.byref(cfg), _ptr(k_pool), _ptr(v_pool),
+                                  _ptr(pos_pool), int(pool_rows), _ptr(meta),
+                                  meta.numel() * meta.element_size(),
+                                  _stream(stream), ctypes.byref(out)),
+           "ra_cache_create")
+    return out
+
+
+def ra_cache_destroy(handle):
+    _check(_lib().ra_cache_destroy(handle), "ra_cache_destroy")
+
+
+def ra_seq_begin(handle, seq, prompt_len, seed, request_id, k_prompt=None,
+                 v_prompt=None, stream=None):
+    _check(_lib().ra_seq_begin(handle, int(seq), int(prompt_len), int(seed),
+                               int(request_id), _ptr(k_prompt), _ptr(v_prompt),
+                               _stream(stream)), "ra_seq_begin")
+
+
+def ra_seq_end(handle, seq, stream=None):
+    _check(_lib().ra_seq_end(handle, int(seq), _stream(stream)), "ra_seq_end")
+
+
+def ra_get_seq_info(handle, seq):
+    info = ra_seq_info()
+    _check(_lib().ra_get_seq_info(handle, int(seq), ctypes.byref(info)),
+           "ra_get_seq_info")
+    return info
+
+
+def ra_decode_attention(handle, layer, q, k_new, v_new, out, workspace,
+                        stream=None):
+    _check(_lib().ra_decode_attention(handle, int(layer), _ptr(q), _ptr(k_new),
+                                      _ptr(v_new), _ptr(out), _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(),
+                                      _stream(stream)), "ra_decode_attention")
+
+
+def ra_end_step(handle, stream=None):
+    n = ctypes.c_int32(0)
+    _check(_lib().ra_end_step(handle, _stream(stream), ctypes.byref(n)),
+           "ra_end_step")
+    return n.value
+
+
+def ra_evict_now(handle, seq, stream=None):
+    _check(_lib().ra_evict_now(handle, int(seq), _stream(stream)), "ra_evict_now")
+
+
+def ra_fast_forward(handle, n_steps, stream=None):
+    _check(_lib().ra_fast_forward(handle, int(n_steps), _stream(stream)),
+           "ra_fast_forward")
+
+
+def ra_export_positions(handle, seq, out, stream=None):
+    _check(_lib().ra_export_positions(handle, int(seq), _ptr(out), out.numel(),
+                                      _stream(stream)), "ra_export_positions")
+
+
+def ra_write_rows(handle, seq, k_rows, v_rows, stream=None):
+    _check(_lib().ra_write_rows(handle, int(seq), _ptr(k_rows), _ptr(v_rows),
+                                _stream(stream)), "ra_write_rows")
+
+
+def ra_read_rows(handle, seq, layer, kv_head, k_out=None, v_out=None,
+                 stream=None):
+    _check(_lib().ra_read_rows(handle, int(seq), int(layer), int(kv_head),
+                               _ptr(k_out), _ptr(v_out), _stream(stream)),
+           "ra_read_rows")
+
+
+def ra_read_positions(handle, seq, layer, kv_head, cap, stream=None):
+    """Synchronous; returns a numpy int32 array of the head's positions."""
+    import numpy as np
+    buf = (ctypes.c_int32 * max(1, int(cap)))()
+    n = ctypes.c_int32(0)
+    _check(_lib().ra_read_positions(handle, int(seq), int(layer), int(kv_head),
+                                    ctypes.cast(buf, ctypes.c_void_p), int(cap),
+                                    ctypes.byref(n), _stream(stream)),
+           "ra_read_positions")
+    return np.frombuffer(buf, dtype=np.int32, count=n.value).copy()
+
+
+def ra_attention_plan(handle):
+    sk, ms = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(_lib().ra_attention_plan(handle, ctypes.byref(sk), ctypes.byref(ms)),
+           "ra_attention_plan")
+    return sk.value, ms.value
+
+
+# ---- owner of the device buffers ----------------------------------------------
+
+class Cache:
+    """Allocates pools, metadata and workspace with torch and owns the handle.
+
+    pool_rows: total rows (sum of ra_seq_rows over the sequences it will hold).
+    """
+
+    def __init__(self, cfg, pool_rows, device="cuda", stream=None):
+        self.cfg = cfg
+        self.device = torch.device(device)
+        _check(ra_config_check(cfg), "ra_config_check")
+        self.dtype = torch.bfloat16 if cfg.dtype == RA_BF16 else torch.float32
+        pool_rows = int(pool_rows)
+        pool_rows += (-pool_rows) % 32
+        self.pool_rows = pool_rows
+        d = cfg.head_dim
+        self.k_pool = torch.zeros(pool_rows, d, dtype=self.dtype, device=self.device)
+        self.v_pool = torch.zeros(pool_rows, d, dtype=self.dtype, device=self.device)
+        self.pos_pool = torch.zeros(pool_rows, dtype=torch.int32, device=self.device)
+        self.meta = torch.zeros(ra_meta_bytes(cfg), dtype=torch.uint8, device=self.device)
+        self.workspace = torch.empty(ra_workspace_bytes(cfg), dtype=torch.uint8,
+                                     device=self.device)
+        self.handle = ra_cache_create(cfg, self.k_pool, self.v_pool, self.pos_pool,
+                                      pool_rows, self.meta, stream)
+
+    def close(self):
+        if self.handle is not None:
+            ra_cache_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def decode(self, layer, q, k_new, v_new, out, stream=None):
+        ra_decode_attention(self.handle, layer, q, k_new, v_new, out,
+                            self.workspace, stream)

@@ -1,0 +1,517 @@
+// Host side of the C ABI (include/randattn.h): validation, the host mirror
+// of every slot's state, pool placement, and kernel launches.
+//
+// The host mirror replays the same integer rules as the device state
+// kernels (append one row per step, the Appendix F trigger, eviction back to
+// lp + k_keep + r), so every capacity and protocol error is reported before
+// any launch and the eviction kernel is launched only on steps where some
+// sequence is due.  The library never allocates device memory.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cmath>
+#include <map>
+#include <new>
+#include <vector>
+
+#include "randattn.h"
+#include "ra_internal.h"
+
+using ra::SeqMeta;
+
+namespace {
+
+std::atomic<int32_t> g_last_hip_error{0};
+
+ra_status hip_fail(hipError_t e) {
+  if (e == hipSuccess) return RA_OK;
+  g_last_hip_error.store(static_cast<int32_t>(e));
+  return RA_ERR_HIP;
+}
+
+#define RA_LAUNCH(expr)                         \
+  do {                                          \
+    const hipError_t e_ = (expr);               \
+    if (e_ != hipSuccess) return hip_fail(e_);  \
+  } while (0)
+
+int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
+
+int64_t keep_rows(const ra_config& c, int32_t lp) {
+  if (c.budget_mode == RA_BUDGET_EVICTABLE) return c.budget_k;
+  return static_cast<int64_t>(c.budget_k) - lp;
+}
+
+}  // namespace
+
+struct ra_cache {
+  ra_config cfg{};
+  int G = 0;
+  size_t elem = 0;
+  void* kpool = nullptr;
+  void* vpool = nullptr;
+  int32_t* pos = nullptr;
+  int64_t pool_rows = 0;
+  SeqMeta* meta = nullptr;
+  int32_t* counters = nullptr;
+  std::vector<SeqMeta> mirror;           // host copy of the device metadata
+  std::map<int64_t, int64_t> free_rows;  // first-fit free list: base -> rows
+  std::vector<uint8_t> appended;         // layers appended in the open step
+  int n_appended = 0;
+  int slot_lo = 0, slot_hi = 0;          // range covering the active slots
+
+  ra::Shape shape() const {
+    return ra::Shape{cfg.num_layers, cfg.num_q_heads, cfg.num_kv_heads, G,
+                     cfg.recent_r, cfg.evict_every, cfg.dtype};
+  }
+  bool step_open() const { return n_appended != 0; }
+  void update_range() {
+    slot_lo = 0;
+    slot_hi = 0;
+    bool any = false;
+    for (int s = 0; s < cfg.max_seqs; ++s) {
+      if (!mirror[s].active) continue;
+      if (!any) slot_lo = s;
+      slot_hi = s + 1;
+      any = true;
+    }
+  }
+  int max_candidates_due() const {
+    int mx = 0;
+    for (int s = slot_lo; s < slot_hi; ++s)
+      if (mirror[s].active && mirror[s].due)
+        mx = std::max(mx, mirror[s].plan_len - mirror[s].prompt_len - cfg.recent_r);
+    return mx;
+  }
+};
+
+namespace {
+
+// The host mirror of the device plan rule (state.hip).
+void mirror_plan(SeqMeta& M, int r, bool at_trigger) {
+  M.due = 0;
+  if (at_trigger && M.len - M.prompt_len - r > M.k_keep) {
+    M.due = 1;
+    M.plan_len = M.len;
+    M.plan_event = M.event;
+    M.len = M.prompt_len + M.k_keep + r;
+    M.event += 1;
+  }
+}
+
+void attention_plan(const ra_cache* c, int* split_keys, int* max_splits) {
+  int cap_max = 32, n_active = 0;
+  for (int s = c->slot_lo; s < c->slot_hi; ++s) {
+    if (!c->mirror[s].active) continue;
+    cap_max = std::max(cap_max, c->mirror[s].cap);
+    ++n_active;
+  }
+  const int heads = std::max(1, n_active * c->cfg.num_kv_heads);
+  int sk;
+  if (c->cfg.attn_split > 0) {
+    sk = c->cfg.attn_split;
+  } else {
+    // about 2048 wavefronts per launch (8 per CU on 256 CUs)
+    const int target = 2048;
+    const int splits = std::min(ra::kMaxSplits, std::max(1, (target + heads - 1) / heads));
+    sk = static_cast<int>(round_up((cap_max + splits - 1) / splits, 32));
+  }
+  sk = std::max<int>(sk, static_cast<int>(round_up((cap_max + ra::kMaxSplits - 1) / ra::kMaxSplits, 32)));
+  *split_keys = sk;
+  *max_splits = (cap_max + sk - 1) / sk;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ra_status_string(int32_t status) {
+  switch (status) {
+    case RA_OK: return "ok";
+    case RA_ERR_INVALID_ARG: return "invalid argument";
+    case RA_ERR_CAPACITY: return "capacity exceeded";
+    case RA_ERR_BUDGET: return "prompt exceeds the budget (TOTAL mode)";
+    case RA_ERR_UNSUPPORTED: return "unsupported configuration";
+    case RA_ERR_HIP: return "HIP error";
+    case RA_ERR_STATE: return "call out of protocol order";
+    default: return "unknown status";
+  }
+}
+
+int32_t ra_last_hip_error(void) { return g_last_hip_error.load(); }
+
+ra_status ra_config_check(const ra_config* c) {
+  if (!c) return RA_ERR_INVALID_ARG;
+  if (c->num_layers < 1 || c->num_q_heads < 1 || c->num_kv_heads < 1 ||
+      c->num_q_heads % c->num_kv_heads != 0 || c->budget_k < 0 ||
+      c->recent_r < 0 || c->evict_every < 1 || c->max_seqs < 1 ||
+      c->max_seqs > 65536 || c->attn_split < 0 || c->attn_split % 32 != 0 ||
+      (c->budget_mode != RA_BUDGET_EVICTABLE && c->budget_mode != RA_BUDGET_TOTAL) ||
+      (c->dtype != RA_F32 && c->dtype != RA_BF16) || c->num_layers > 4096 ||
+      c->num_kv_heads > 4096)
+    return RA_ERR_INVALID_ARG;
+  if (c->head_dim != ra::kHeadDim) return RA_ERR_UNSUPPORTED;
+  if (c->num_q_heads / c->num_kv_heads > ra::kMaxGroup) return RA_ERR_UNSUPPORTED;
+  if (c->evict_every > ra::kMaxEvery) return RA_ERR_UNSUPPORTED;
+  // the selection holds every candidate's score in registers
+  if (static_cast<int64_t>(c->budget_k) + c->evict_every > ra::kMaxCandidates)
+    return RA_ERR_UNSUPPORTED;
+  return RA_OK;
+}
+
+int64_t ra_region_rows(const ra_config* c, int32_t prompt_len) {
+  const ra_status st = ra_config_check(c);
+  if (st != RA_OK) return st;
+  if (prompt_len < 0) return RA_ERR_INVALID_ARG;
+  const int64_t k = keep_rows(*c, prompt_len);
+  if (k < 0) return RA_ERR_BUDGET;
+  const int64_t rows = round_up(static_cast<int64_t>(prompt_len) + k + c->recent_r +
+                                    c->evict_every, ra::kRegionAlign);
+  if (rows > (int64_t(1) << 30)) return RA_ERR_UNSUPPORTED;
+  return rows;
+}
+
+int64_t ra_seq_rows(const ra_config* c, int32_t prompt_len) {
+  const int64_t rows = ra_region_rows(c, prompt_len);
+  if (rows < 0) return rows;
+  return rows * c->num_layers * c->num_kv_heads;
+}
+
+size_t ra_meta_bytes(const ra_config* c) {
+  if (ra_config_check(c) != RA_OK) return 0;
+  const size_t metas = sizeof(SeqMeta) * static_cast<size_t>(c->max_seqs);
+  const size_t ctrs = sizeof(int32_t) * static_cast<size_t>(c->max_seqs) * c->num_kv_heads;
+  return round_up(static_cast<int64_t>(metas + ctrs), 256);
+}
+
+size_t ra_workspace_bytes(const ra_config* c) {
+  if (ra_config_check(c) != RA_OK) return 0;
+  const size_t G = c->num_q_heads / c->num_kv_heads;
+  const size_t items = static_cast<size_t>(c->max_seqs) * c->num_kv_heads * ra::kMaxSplits;
+  return items * G * (ra::kHeadDim + 2) * sizeof(float) + 256;
+}
+
+ra_status ra_cache_create(const ra_config* cfg, void* k_pool, void* v_pool,
+                          int32_t* pos_pool, int64_t pool_rows, void* meta,
+                          size_t meta_bytes, void* stream, ra_cache** out) {
+  if (!out) return RA_ERR_INVALID_ARG;
+  *out = nullptr;
+  const ra_status st = ra_config_check(cfg);
+  if (st != RA_OK) return st;
+  if (!k_pool || !v_pool || !pos_pool || !meta || pool_rows <= 0 ||
+      pool_rows % ra::kRegionAlign != 0 || meta_bytes < ra_meta_bytes(cfg))
+    return RA_ERR_INVALID_ARG;
+  const auto misaligned = [](const void* p) {
+    return (reinterpret_cast<uintptr_t>(p) & 15u) != 0;
+  };
+  if (misaligned(k_pool) || misaligned(v_pool) || misaligned(pos_pool) || misaligned(meta))
+    return RA_ERR_INVALID_ARG;
+  ra_cache* c = new (std::nothrow) ra_cache();
+  if (!c) return RA_ERR_CAPACITY;
+  c->cfg = *cfg;
+  c->G = cfg->num_q_heads / cfg->num_kv_heads;
+  c->elem = cfg->dtype == RA_BF16 ? 2 : 4;
+  c->kpool = k_pool;
+  c->vpool = v_pool;
+  c->pos = pos_pool;
+  c->pool_rows = pool_rows;
+  c->meta = static_cast<SeqMeta*>(meta);
+  c->counters = reinterpret_cast<int32_t*>(c->meta + cfg->max_seqs);
+  c->mirror.assign(cfg->max_seqs, SeqMeta{});
+  c->free_rows[0] = pool_rows;
+  c->appended.assign(cfg->num_layers, 0);
+  const hipError_t e = ra::launch_zero_words(static_cast<uint32_t*>(meta),
+                                             static_cast<int64_t>(ra_meta_bytes(cfg) / 4),
+                                             static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    delete c;
+    return hip_fail(e);
+  }
+  *out = c;
+  return RA_OK;
+}
+
+ra_status ra_cache_destroy(ra_cache* c) {
+  if (!c) return RA_ERR_INVALID_ARG;
+  delete c;
+  return RA_OK;
+}
+
+ra_status ra_get_seq_info(const ra_cache* c, int32_t seq, ra_seq_info* out) {
+  if (!c || !out || seq < 0 || seq >= c->cfg.max_seqs) return RA_ERR_INVALID_ARG;
+  const SeqMeta& M = c->mirror[seq];
+  out->active = M.active;
+  out->prompt_len = M.prompt_len;
+  out->len = M.len;
+  out->step = M.step;
+  out->event = M.event;
+  out->k_keep = M.k_keep;
+  out->cap = M.cap;
+  out->base = M.base;
+  return RA_OK;
+}
+
+ra_status ra_attention_plan(const ra_cache* c, int32_t* split_keys, int32_t* max_splits) {
+  if (!c || !split_keys || !max_splits) return RA_ERR_INVALID_ARG;
+  int sk, ms;
+  attention_plan(c, &sk, &ms);
+  *split_keys = sk;
+  *max_splits = ms;
+  return RA_OK;
+}
+
+ra_status ra_seq_begin(ra_cache* c, int32_t seq, int32_t prompt_len, uint64_t seed,
+                       uint64_t request_id, const void* dev_k_prompt,
+                       const void* dev_v_prompt, void* stream) {
+  if (!c || seq < 0 || seq >= c->cfg.max_seqs || prompt_len < 0 ||
+      (dev_k_prompt == nullptr) != (dev_v_prompt == nullptr))
+    return RA_ERR_INVALID_ARG;
+  if (c->step_open()) return RA_ERR_STATE;
+  if (c->mirror[seq].active) return RA_ERR_STATE;
+  const int64_t cap = ra_region_rows(&c->cfg, prompt_len);
+  if (cap < 0) return static_cast<ra_status>(cap);
+  const int64_t need = cap * c->cfg.num_layers * c->cfg.num_kv_heads;
+  auto it = c->free_rows.begin();
+  for (; it != c->free_rows.end(); ++it)
+    if (it->second >= need) break;
+  if (it == c->free_rows.end()) return RA_ERR_CAPACITY;
+  const int64_t base = it->first;
+
+  SeqMeta M{};
+  M.base = base;
+  M.cap = static_cast<int32_t>(cap);
+  M.prompt_len = prompt_len;
+  M.len = prompt_len;
+  M.k_keep = static_cast<int32_t>(keep_rows(c->cfg, prompt_len));
+  M.seed = seed;
+  M.rid = request_id;
+  M.active = 1;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  RA_LAUNCH(ra::launch_seq_set(c->meta, seq, M, s));
+  RA_LAUNCH(ra::launch_write_rows(c->shape(), base, M.cap, prompt_len, dev_k_prompt,
+                                  dev_v_prompt, nullptr, c->kpool, c->vpool, c->pos, s));
+  const int64_t rest = it->second - need;
+  c->free_rows.erase(it);
+  if (rest > 0) c->free_rows[base + need] = rest;
+  c->mirror[seq] = M;
+  c->update_range();
+  return RA_OK;
+}
+
+ra_status ra_seq_end(ra_cache* c, int32_t seq, void* stream) {
+  if (!c || seq < 0 || seq >= c->cfg.max_seqs) return RA_ERR_INVALID_ARG;
+  if (c->step_open()) return RA_ERR_STATE;
+  SeqMeta& M = c->mirror[seq];
+  if (!M.active) return RA_ERR_STATE;
+  SeqMeta off{};
+  RA_LAUNCH(ra::launch_seq_set(c->meta, seq, off, static_cast<hipStream_t>(stream)));
+  int64_t base = M.base;
+  int64_t rows = static_cast<int64_t>(M.cap) * c->cfg.num_layers * c->cfg.num_kv_heads;
+  // return the rows to the free list, merging with neighbours
+  auto next = c->free_rows.lower_bound(base);
+  if (next != c->free_rows.end() && base + rows == next->first) {
+    rows += next->second;
+    next = c->free_rows.erase(next);
+  }
+  if (next != c->free_rows.begin()) {
+    auto prev = std::prev(next);
+    if (prev->first + prev->second == base) {
+      base = prev->first;
+      rows += prev->second;
+      c->free_rows.erase(prev);
+    }
+  }
+  c->free_rows[base] = rows;
+  M = SeqMeta{};
+  c->update_range();
+  return RA_OK;
+}
+
+ra_status ra_decode_attention(ra_cache* c, int32_t layer, const void* q,
+                              const void* k_new, const void* v_new, void* out,
+                              void* workspace, size_t workspace_bytes,
+                              void* stream) {
+  if (!c || layer < 0 || layer >= c->cfg.num_layers || !q || !k_new || !v_new ||
+      !out || !workspace)
+    return RA_ERR_INVALID_ARG;
+  if (workspace_bytes < ra_workspace_bytes(&c->cfg)) return RA_ERR_INVALID_ARG;
+  if (c->appended[layer]) return RA_ERR_STATE;
+  for (int s = c->slot_lo; s < c->slot_hi; ++s)
+    if (c->mirror[s].active && c->mirror[s].len + 1 > c->mirror[s].cap) return RA_ERR_CAPACITY;
+  c->appended[layer] = 1;
+  ++c->n_appended;
+  if (c->slot_hi <= c->slot_lo) return RA_OK;
+  int sk, ms;
+  attention_plan(c, &sk, &ms);
+  const size_t G = static_cast<size_t>(c->G);
+  const size_t items = static_cast<size_t>(c->cfg.max_seqs) * c->cfg.num_kv_heads * ra::kMaxSplits;
+  float* ws = static_cast<float*>(workspace);
+  ra::AttnLaunch a{};
+  a.meta = c->meta;
+  a.kpool = c->kpool;
+  a.vpool = c->vpool;
+  a.pos = c->pos;
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.out = out;
+  a.ws_o = ws;
+  a.ws_ml = ws + items * G * ra::kHeadDim;
+  a.counters = c->counters;
+  a.layer = layer;
+  a.max_seqs = c->slot_hi;
+  a.split_keys = sk;
+  a.max_splits = ms;
+  const hipError_t e = ra::launch_attention(c->shape(), a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    c->appended[layer] = 0;
+    --c->n_appended;
+    return hip_fail(e);
+  }
+  return RA_OK;
+}
+
+ra_status ra_end_step(ra_cache* c, void* stream, int32_t* n_evicted) {
+  if (!c) return RA_ERR_INVALID_ARG;
+  if (n_evicted) *n_evicted = 0;
+  bool any_active = c->slot_hi > c->slot_lo;
+  if (any_active && c->n_appended != c->cfg.num_layers) return RA_ERR_STATE;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  std::fill(c->appended.begin(), c->appended.end(), 0);
+  c->n_appended = 0;
+  if (!any_active) return RA_OK;
+  RA_LAUNCH(ra::launch_advance(c->meta, c->slot_lo, c->slot_hi, 1, c->cfg.recent_r,
+                               c->cfg.evict_every, s));
+  int due = 0;
+  for (int i = c->slot_lo; i < c->slot_hi; ++i) {
+    SeqMeta& M = c->mirror[i];
+    if (!M.active) continue;
+    M.step += 1;
+    M.len += 1;
+    mirror_plan(M, c->cfg.recent_r, M.step % c->cfg.evict_every == 0);
+    due += M.due;
+  }
+  if (due) {
+    RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos,
+                               c->slot_lo, c->slot_hi, c->max_candidates_due(), false, s));
+  }
+  if (n_evicted) *n_evicted = due;
+  return RA_OK;
+}
+
+ra_status ra_evict_now(ra_cache* c, int32_t seq, void* stream) {
+  if (!c || seq < 0 || seq >= c->cfg.max_seqs) return RA_ERR_INVALID_ARG;
+  if (c->step_open()) return RA_ERR_STATE;
+  SeqMeta& M = c->mirror[seq];
+  if (!M.active) return RA_ERR_STATE;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  RA_LAUNCH(ra::launch_plan_now(c->meta, seq, c->cfg.recent_r, s));
+  for (int i = c->slot_lo; i < c->slot_hi; ++i) c->mirror[i].due = 0;
+  mirror_plan(M, c->cfg.recent_r, true);
+  if (M.due) {
+    RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos, seq,
+                               seq + 1, M.plan_len - M.prompt_len - c->cfg.recent_r,
+                               false, s));
+  }
+  return RA_OK;
+}
+
+ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
+  if (!c || n_steps < 0) return RA_ERR_INVALID_ARG;
+  if (c->step_open()) return RA_ERR_STATE;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int every = c->cfg.evict_every;
+  int remaining = n_steps;
+  while (remaining > 0 && c->slot_hi > c->slot_lo) {
+    int run = remaining;
+    for (int i = c->slot_lo; i < c->slot_hi; ++i)
+      if (c->mirror[i].active) run = std::min(run, every - c->mirror[i].step % every);
+    for (int i = c->slot_lo; i < c->slot_hi; ++i) {
+      const SeqMeta& M = c->mirror[i];
+      if (M.active && M.len + run > M.cap) return RA_ERR_CAPACITY;
+    }
+    RA_LAUNCH(ra::launch_append_positions(c->meta, c->pos, c->slot_lo, c->slot_hi,
+                                          c->cfg.num_layers, c->cfg.num_kv_heads, run, s));
+    RA_LAUNCH(ra::launch_advance(c->meta, c->slot_lo, c->slot_hi, run, c->cfg.recent_r,
+                                 every, s));
+    int due = 0;
+    for (int i = c->slot_lo; i < c->slot_hi; ++i) {
+      SeqMeta& M = c->mirror[i];
+      if (!M.active) continue;
+      M.step += run;
+      M.len += run;
+      mirror_plan(M, c->cfg.recent_r, M.step % every == 0);
+      due += M.due;
+    }
+    if (due) {
+      RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos,
+                                 c->slot_lo, c->slot_hi, c->max_candidates_due(), true, s));
+    }
+    remaining -= run;
+  }
+  return RA_OK;
+}
+
+ra_status ra_export_positions(ra_cache* c, int32_t seq, int32_t* dev_out,
+                              int64_t out_elems, void* stream) {
+  if (!c || seq < 0 || seq >= c->cfg.max_seqs || !dev_out) return RA_ERR_INVALID_ARG;
+  if (c->step_open()) return RA_ERR_STATE;
+  const SeqMeta& M = c->mirror[seq];
+  if (!M.active) return RA_ERR_STATE;
+  if (out_elems < static_cast<int64_t>(M.len) * c->cfg.num_layers * c->cfg.num_kv_heads)
+    return RA_ERR_CAPACITY;
+  RA_LAUNCH(ra::launch_export_positions(c->shape(), M.base, M.cap, M.len, c->pos, dev_out,
+                                        static_cast<hipStream_t>(stream)));
+  return RA_OK;
+}
+
+ra_status ra_write_rows(ra_cache* c, int32_t seq, const void* dev_k, const void* dev_v,
+                        void* stream) {
+  if (!c || seq < 0 || seq >= c->cfg.max_seqs || !dev_k || !dev_v) return RA_ERR_INVALID_ARG;
+  if (c->step_open()) return RA_ERR_STATE;
+  const SeqMeta& M = c->mirror[seq];
+  if (!M.active) return RA_ERR_STATE;
+  // positions are left as they are: pass the region's own positions through
+  RA_LAUNCH(ra::launch_write_rows(c->shape(), M.base, M.cap, M.len, dev_k, dev_v, nullptr,
+                                  c->kpool, c->vpool, nullptr, static_cast<hipStream_t>(stream)));
+  return RA_OK;
+}
+
+ra_status ra_read_rows(ra_cache* c, int32_t seq, int32_t layer, int32_t kv_head,
+                       void* dev_k_out, void* dev_v_out, void* stream) {
+  if (!c || seq < 0 || seq >= c->cfg.max_seqs || layer < 0 ||
+      layer >= c->cfg.num_layers || kv_head < 0 || kv_head >= c->cfg.num_kv_heads)
+    return RA_ERR_INVALID_ARG;
+  if (c->step_open()) return RA_ERR_STATE;
+  const SeqMeta& M = c->mirror[seq];
+  if (!M.active) return RA_ERR_STATE;
+  const int64_t region = M.base + static_cast<int64_t>(layer * c->cfg.num_kv_heads + kv_head) * M.cap;
+  RA_LAUNCH(ra::launch_read_rows(c->shape(), region, M.len, c->kpool, c->vpool, dev_k_out,
+                                 dev_v_out, static_cast<hipStream_t>(stream)));
+  return RA_OK;
+}
+
+ra_status ra_read_positions(ra_cache* c, int32_t seq, int32_t layer, int32_t kv_head,
+                            int32_t* host_out, int32_t host_cap, int32_t* n_out,
+                            void* stream) {
+  if (!c || seq < 0 || seq >= c->cfg.max_seqs || layer < 0 ||
+      layer >= c->cfg.num_layers || kv_head < 0 || kv_head >= c->cfg.num_kv_heads ||
+      !host_out || !n_out)
+    return RA_ERR_INVALID_ARG;
+  if (c->step_open()) return RA_ERR_STATE;
+  const SeqMeta& M = c->mirror[seq];
+  if (!M.active) return RA_ERR_STATE;
+  *n_out = M.len;
+  if (host_cap < M.len) return RA_ERR_CAPACITY;
+  const int64_t region = M.base + static_cast<int64_t>(layer * c->cfg.num_kv_heads + kv_head) * M.cap;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (M.len > 0) {
+    RA_LAUNCH(hipMemcpyAsync(host_out, c->pos + region, sizeof(int32_t) * M.len,
+                             hipMemcpyDeviceToHost, s));
+  }
+  RA_LAUNCH(hipStreamSynchronize(s));
+  return RA_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,483 @@
+// Grouped-query decode attention over the compressed per-KV-head cache, with
+// the step's append fused in (Section 2, "Notation": o = sum_i alpha_i v_i,
+// alpha = softmax_i(q . k_i / sqrt(d)); Appendix F: the G query heads of a
+// group read their KV head's cache).
+//
+// Work decomposition: one wavefront per (sequence, KV head, split of
+// `split_keys` keys).  Each wavefront reads its keys and values exactly once
+// for all G query heads of the group, keeps an online softmax (running max
+// and sum, combined across lanes with wavefront shuffles), and writes an
+// unnormalised partial.  The last wavefront of a head to finish (a device
+// atomic counter) merges the partials and writes the output, then resets the
+// counter for the next launch.  The step's new key/value is read from the
+// input buffers by the wavefront that owns the last key, which also stores
+// it into the cache after its reads, so no wavefront of the launch reads a
+// row that is being written.
+//
+// bf16 path (MFMA, v_mfma_f32_16x16x32_bf16, 16x16 output tiles):
+//   S^T[key][query] = K . Q^T   A = 16 key rows x 32 channels, B = Q^T with
+//                               the group's G queries on the N side (padded
+//                               to 16 with zeros);
+//   O^T[ch][query] += V^T . P^T A = 16 channels x 32 keys from the
+//                               transposed value tiles, B = P^T.
+// A lane's 8 operand elements come from one 16-byte global load: key rows
+// are row-major and value rows are stored as transposed 8-row tiles.  The
+// key rows are assigned to the two 16-row S tiles so that each lane's
+// 8 softmax weights are exactly the 8 keys its P^T operand needs (tile t
+// row 4a+i holds key 8a+4t+i), so no data moves between lanes except the
+// two shuffles of the row maximum.
+// fp32 path (VALU): lanes own keys for the scores and channels for P.V.
+#include "ra_internal.h"
+
+namespace ra {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kNegInf = -__builtin_huge_valf();
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) {
+  bf16x8 r;
+  __builtin_memcpy(&r, &v, 16);
+  return r;
+}
+
+__device__ __forceinline__ u32x4 ld16(const void* p) {
+  return *reinterpret_cast<const u32x4*>(p);
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16(float x) {
+  __bf16 b = static_cast<__bf16>(x);   // round to nearest even
+  uint16_t h;
+  __builtin_memcpy(&h, &b, 2);
+  return h;
+}
+
+struct Work {
+  int slot, g, split;
+  int len, n_keys, k0, k1, nsplit;
+  int64_t region;  // first row of the (slot, layer, g) region
+  bool valid;
+};
+
+__device__ __forceinline__ Work locate(const SeqMeta* meta, int layer, int Hkv,
+                                       int split_keys) {
+  Work w;
+  w.split = blockIdx.x;
+  w.g = blockIdx.y;
+  w.slot = blockIdx.z;
+  const SeqMeta& M = meta[w.slot];
+  w.valid = false;
+  if (!M.active) return w;
+  w.len = M.len;
+  w.n_keys = w.len + 1;
+  w.k0 = w.split * split_keys;
+  if (w.k0 >= w.n_keys) return w;
+  w.k1 = min(w.k0 + split_keys, w.n_keys);
+  w.nsplit = (w.n_keys + split_keys - 1) / split_keys;
+  w.region = M.base + static_cast<int64_t>(layer * Hkv + w.g) * M.cap;
+  w.valid = true;
+  return w;
+}
+
+// Store the step's new pair into the cache (row `len` of the region).
+template <typename E>
+__device__ __forceinline__ void append_row(const Work& w, const SeqMeta* meta,
+                                           int Hkv, const E* k_new,
+                                           const E* v_new, E* kpool, E* vpool,
+                                           int32_t* pos) {
+  const int lane = threadIdx.x;
+  const int64_t src = (static_cast<int64_t>(w.slot) * Hkv + w.g) * kHeadDim;
+  const int64_t row = w.region + w.len;
+  for (int c = lane; c < kHeadDim; c += 64) {
+    kpool[row * kHeadDim + c] = k_new[src + c];
+    vpool[(row & ~int64_t(7)) * kHeadDim + c * 8 + (row & 7)] = v_new[src + c];
+  }
+  if (lane == 0) pos[row] = meta[w.slot].prompt_len + meta[w.slot].step;
+}
+
+// Publish the partial and, in the last wavefront of the head, merge them.
+// Partial layout: ws_o[((head * kMaxSplits + split) * G + q) * 128 + c]
+// (numerator, scaled by 2^-m) and ws_ml[... * 2 + {0,1}] = (m, l) with m the
+// running max in log2 units and l the sum of 2^(s - m).
+template <typename E>
+__device__ __forceinline__ void finish_head(const Work& w, const AttnLaunch& a,
+                                            int G, int Hq, int Hkv) {
+  const int lane = threadIdx.x;
+  const int head = w.slot * Hkv + w.g;
+  __threadfence();
+  int prev = 0;
+  if (lane == 0) prev = atomicAdd(&a.counters[head], 1);
+  prev = __shfl(prev, 0, 64);
+  if (prev != w.nsplit - 1) return;
+  __threadfence();
+  const float* ml = a.ws_ml + static_cast<int64_t>(head) * kMaxSplits * G * 2;
+  const float* po = a.ws_o + static_cast<int64_t>(head) * kMaxSplits * G * kHeadDim;
+  E* out = static_cast<E*>(a.out);
+  for (int q = 0; q < G; ++q) {
+    float mx = kNegInf;
+    for (int s = 0; s < w.nsplit; ++s) mx = fmaxf(mx, ml[(s * G + q) * 2]);
+    float lsum = 0.f, o0 = 0.f, o1 = 0.f;
+    for (int s = 0; s < w.nsplit; ++s) {
+      const float sc = exp2f(ml[(s * G + q) * 2] - mx);
+      lsum += ml[(s * G + q) * 2 + 1] * sc;
+      const float* row = po + static_cast<int64_t>(s * G + q) * kHeadDim;
+      o0 += row[lane] * sc;
+      o1 += row[lane + 64] * sc;
+    }
+    const float inv = 1.f / lsum;
+    const int64_t orow = (static_cast<int64_t>(w.slot) * Hq + w.g * G + q) * kHeadDim;
+    if constexpr (sizeof(E) == 2) {
+      out[orow + lane] = f32_to_bf16(o0 * inv);
+      out[orow + lane + 64] = f32_to_bf16(o1 * inv);
+    } else {
+      out[orow + lane] = o0 * inv;
+      out[orow + lane + 64] = o1 * inv;
+    }
+  }
+  if (lane == 0) a.counters[head] = 0;
+}
+
+// ---------------------------------------------------------------------------
+// bf16, MFMA
+// ---------------------------------------------------------------------------
+
+struct BlockRegs {
+  u32x4 k[2][4];  // [S tile][k-step]
+  u32x4 v[8];     // [16-channel tile]
+};
+
+// Offsets (in elements) of this lane's operand loads within a 32-key block.
+struct LaneMap {
+  int krow[2];   // key row within the block for S tile 0 / 1
+  int kcol;      // first channel of the lane's 64-byte key slice
+  int vrow;      // first key row of the lane's value tile
+  int vch;       // channel within each 16-channel tile
+};
+
+__device__ __forceinline__ LaneMap lane_map() {
+  const int lane = threadIdx.x, r = lane & 15, grp = lane >> 4;
+  LaneMap m;
+  m.krow[0] = 8 * (r >> 2) + (r & 3);
+  m.krow[1] = 8 * (r >> 2) + 4 + (r & 3);
+  m.kcol = 32 * grp;
+  m.vrow = 8 * grp;
+  m.vch = r;
+  return m;
+}
+
+__device__ __forceinline__ void load_block(BlockRegs& b, const uint16_t* Kr,
+                                           const uint16_t* Vr, int kb,
+                                           const LaneMap& lm) {
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const uint16_t* row = Kr + static_cast<int64_t>(kb + lm.krow[t]) * kHeadDim + lm.kcol;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) b.k[t][s] = ld16(row + 8 * s);
+  }
+  const uint16_t* vt = Vr + static_cast<int64_t>(kb + lm.vrow) * kHeadDim + lm.vch * 8;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) b.v[u] = ld16(vt + 16 * 8 * u);
+}
+
+struct Softmax {
+  float m;      // running max of the scaled scores (log2 units), per query
+  float l;      // this lane's share of the running sum
+  f32x4 acc[8]; // O^T tile u: channels 16u + 4*grp + i, query lane & 15
+};
+
+// One 32-key block.  `limit`: keys with index >= limit (block-relative) are
+// masked out (32 for a full block).
+__device__ __forceinline__ void compute_block(Softmax& st, const BlockRegs& b,
+                                              const bf16x8 (&qop)[4],
+                                              float scale_log2, int limit) {
+  f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(b.k[0][s]), qop[s], s0, 0, 0, 0);
+    s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(b.k[1][s]), qop[s], s1, 0, 0, 0);
+  }
+  const int grp = threadIdx.x >> 4;
+  float x[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[i] = s0[i] * scale_log2;
+    x[4 + i] = s1[i] * scale_log2;
+  }
+  if (limit < 32) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      if (8 * grp + e >= limit) x[e] = kNegInf;
+  }
+  float bm = x[0];
+#pragma unroll
+  for (int e = 1; e < 8; ++e) bm = fmaxf(bm, x[e]);
+  bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
+  bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
+  const float mn = fmaxf(st.m, bm);
+  const float alpha = exp2f(st.m - mn);
+  bf16x8 p;
+  float psum = 0.f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const __bf16 pb = static_cast<__bf16>(exp2f(x[e] - mn));
+    p[e] = pb;
+    psum += static_cast<float>(pb);
+  }
+  st.l = st.l * alpha + psum;
+  st.m = mn;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    st.acc[u] *= alpha;
+    st.acc[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(b.v[u]), p, st.acc[u], 0, 0, 0);
+  }
+}
+
+__global__ __launch_bounds__(64) void attn_bf16_kernel(AttnLaunch a, int G,
+                                                       int Hq, int Hkv,
+                                                       float scale_log2) {
+  const Work w = locate(a.meta, a.layer, Hkv, a.split_keys);
+  if (!w.valid) return;
+  const int lane = threadIdx.x, qi = lane & 15, grp = lane >> 4;
+  const LaneMap lm = lane_map();
+  const uint16_t* Kr = static_cast<const uint16_t*>(a.kpool) + w.region * kHeadDim;
+  const uint16_t* Vr = static_cast<const uint16_t*>(a.vpool) + w.region * kHeadDim;
+  const uint16_t* kn = static_cast<const uint16_t*>(a.k_new) +
+                       (static_cast<int64_t>(w.slot) * Hkv + w.g) * kHeadDim;
+  const uint16_t* vn = static_cast<const uint16_t*>(a.v_new) +
+                       (static_cast<int64_t>(w.slot) * Hkv + w.g) * kHeadDim;
+
+  // Q^T operand: query qi of the group, channels 32*grp + 8*s + [0, 8)
+  bf16x8 qop[4];
+  {
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) +
+        (static_cast<int64_t>(w.slot) * Hq + w.g * G + qi) * kHeadDim + 32 * grp;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const u32x4 z = {0u, 0u, 0u, 0u};
+      qop[s] = as_bf16x8(qi < G ? ld16(qrow + 8 * s) : z);
+    }
+  }
+
+  Softmax st;
+  st.m = kNegInf;
+  st.l = 0.f;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) st.acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const bool owns_last = (w.k1 == w.n_keys);
+  // full blocks: every key a cached row
+  const int nfull = owns_last ? (w.len - w.k0) / 32 : (w.k1 - w.k0) / 32;
+  {
+    BlockRegs A, B;
+    int i = 0;
+    if (nfull > 0) load_block(A, Kr, Vr, w.k0, lm);
+    for (; i + 1 < nfull; i += 2) {
+      load_block(B, Kr, Vr, w.k0 + 32 * (i + 1), lm);
+      compute_block(st, A, qop, scale_log2, 32);
+      if (i + 2 < nfull) load_block(A, Kr, Vr, w.k0 + 32 * (i + 2), lm);
+      compute_block(st, B, qop, scale_log2, 32);
+    }
+    if (i < nfull) compute_block(st, A, qop, scale_log2, 32);
+  }
+  if (owns_last) {
+    // tail block: cached rows below len, the new pair at len, masked above
+    const int kb = w.k0 + 32 * nfull;
+    const int limit = w.n_keys - kb;       // 1..32 valid keys
+    BlockRegs b;
+    const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      const int key = kb + lm.krow[t];
+      const uint16_t* row = key < w.len ? Kr + static_cast<int64_t>(key) * kHeadDim : kn;
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        b.k[t][s] = key <= w.len ? ld16(row + lm.kcol + 8 * s) : z;
+    }
+    const int key0 = kb + lm.vrow;         // first key of this lane's tile
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int ch = 16 * u + lm.vch;
+      u32x4 v = key0 < w.len ? ld16(Vr + static_cast<int64_t>(key0) * kHeadDim + ch * 8) : z;
+      uint16_t e8[8];
+      __builtin_memcpy(e8, &v, 16);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (key0 + e == w.len) e8[e] = vn[ch];
+        else if (key0 + e > w.len) e8[e] = 0;
+      }
+      __builtin_memcpy(&v, e8, 16);
+      b.v[u] = v;
+    }
+    compute_block(st, b, qop, scale_log2, limit);
+  }
+
+  // lane sums of the same query -> full sum
+  st.l += __shfl_xor(st.l, 16, 64);
+  st.l += __shfl_xor(st.l, 32, 64);
+
+  if (owns_last)
+    append_row<uint16_t>(w, a.meta, Hkv, static_cast<const uint16_t*>(a.k_new),
+                         static_cast<const uint16_t*>(a.v_new),
+                         static_cast<uint16_t*>(a.kpool),
+                         static_cast<uint16_t*>(a.vpool), a.pos);
+
+  const int head = w.slot * Hkv + w.g;
+  const int64_t item = static_cast<int64_t>(head) * kMaxSplits + w.split;
+  if (qi < G) {
+    float* po = a.ws_o + (item * G + qi) * kHeadDim;
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      *reinterpret_cast<f32x4*>(po + 16 * u + 4 * grp) = st.acc[u];
+    if (grp == 0) {
+      a.ws_ml[(item * G + qi) * 2] = st.m;
+      a.ws_ml[(item * G + qi) * 2 + 1] = st.l;
+    }
+  }
+  finish_head<uint16_t>(w, a, G, Hq, Hkv);
+}
+
+// ---------------------------------------------------------------------------
+// fp32, VALU
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G,
+                                                      int Hq, int Hkv,
+                                                      float scale_log2) {
+  __shared__ float qs[kMaxGroup][kHeadDim];
+  __shared__ float ps[kMaxGroup][64];
+  const Work w = locate(a.meta, a.layer, Hkv, a.split_keys);
+  if (!w.valid) return;
+  const int lane = threadIdx.x;
+  const float* Kr = static_cast<const float*>(a.kpool) + w.region * kHeadDim;
+  const float* Vr = static_cast<const float*>(a.vpool) + w.region * kHeadDim;
+  const float* kn = static_cast<const float*>(a.k_new) +
+                    (static_cast<int64_t>(w.slot) * Hkv + w.g) * kHeadDim;
+  const float* vn = static_cast<const float*>(a.v_new) +
+                    (static_cast<int64_t>(w.slot) * Hkv + w.g) * kHeadDim;
+  const float* qg = static_cast<const float*>(a.q) +
+                    (static_cast<int64_t>(w.slot) * Hq + w.g * G) * kHeadDim;
+  for (int i = lane; i < G * kHeadDim; i += 64) qs[i / kHeadDim][i % kHeadDim] = qg[i];
+  __syncthreads();
+
+  float m[kMaxGroup], l[kMaxGroup], acc[kMaxGroup][2];
+#pragma unroll
+  for (int q = 0; q < kMaxGroup; ++q) {
+    m[q] = kNegInf;
+    l[q] = 0.f;
+    acc[q][0] = acc[q][1] = 0.f;
+  }
+  for (int kb = w.k0; kb < w.k1; kb += 64) {
+    const int key = kb + lane;
+    const bool valid = key < w.k1;
+    const float* krow = key < w.len ? Kr + static_cast<int64_t>(key) * kHeadDim : kn;
+    float s[kMaxGroup];
+#pragma unroll
+    for (int q = 0; q < kMaxGroup; ++q) s[q] = 0.f;
+    if (valid) {
+      for (int c = 0; c < kHeadDim; c += 4) {
+        const float4 kv = *reinterpret_cast<const float4*>(krow + c);
+#pragma unroll
+        for (int q = 0; q < kMaxGroup; ++q) {
+          if (q < G)
+            s[q] += kv.x * qs[q][c] + kv.y * qs[q][c + 1] + kv.z * qs[q][c + 2] +
+                    kv.w * qs[q][c + 3];
+        }
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kMaxGroup; ++q) {
+      if (q < G) {
+        const float x = valid ? s[q] * scale_log2 : kNegInf;
+        const float mn = fmaxf(m[q], wave_max(x));
+        const float alpha = exp2f(m[q] - mn);
+        const float p = exp2f(x - mn);
+        l[q] = l[q] * alpha + wave_sum(p);
+        acc[q][0] *= alpha;
+        acc[q][1] *= alpha;
+        m[q] = mn;
+        ps[q][lane] = p;
+      }
+    }
+    __syncthreads();
+    const int nk = min(64, w.k1 - kb);
+    for (int j = 0; j < nk; ++j) {
+      const int kj = kb + j;
+      float v0, v1;
+      if (kj < w.len) {
+        const float* vt = Vr + static_cast<int64_t>(kj & ~7) * kHeadDim + (kj & 7);
+        v0 = vt[lane * 8];
+        v1 = vt[(lane + 64) * 8];
+      } else {
+        v0 = vn[lane];
+        v1 = vn[lane + 64];
+      }
+#pragma unroll
+      for (int q = 0; q < kMaxGroup; ++q) {
+        if (q < G) {
+          acc[q][0] += ps[q][j] * v0;
+          acc[q][1] += ps[q][j] * v1;
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  if (w.k1 == w.n_keys)
+    append_row<float>(w, a.meta, Hkv, static_cast<const float*>(a.k_new),
+                      static_cast<const float*>(a.v_new),
+                      static_cast<float*>(a.kpool),
+                      static_cast<float*>(a.vpool), a.pos);
+
+  const int head = w.slot * Hkv + w.g;
+  const int64_t item = static_cast<int64_t>(head) * kMaxSplits + w.split;
+#pragma unroll
+  for (int q = 0; q < kMaxGroup; ++q) {
+    if (q < G) {
+      float* po = a.ws_o + (item * G + q) * kHeadDim;
+      po[lane] = acc[q][0];
+      po[lane + 64] = acc[q][1];
+      if (lane == 0) {
+        a.ws_ml[(item * G + q) * 2] = m[q];
+        a.ws_ml[(item * G + q) * 2 + 1] = l[q];
+      }
+    }
+  }
+  finish_head<float>(w, a, G, Hq, Hkv);
+}
+
+}  // namespace
+
+hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s) {
+  const dim3 grid(a.max_splits, sh.Hkv, a.max_seqs);
+  // scores in log2 units: q.k / sqrt(d) * log2(e)
+  const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(kHeadDim));
+  if (sh.dtype == 1) {
+    hipLaunchKernelGGL(attn_bf16_kernel, grid, dim3(64), 0, s, a, sh.G, sh.Hq,
+                       sh.Hkv, scale_log2);
+  } else {
+    hipLaunchKernelGGL(attn_f32_kernel, grid, dim3(64), 0, s, a, sh.G, sh.Hq,
+                       sh.Hkv, scale_log2);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace ra

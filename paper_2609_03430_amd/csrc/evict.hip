@@ -1,0 +1,306 @@
+// Random Attention eviction on gfx950: uniform per-head scores, selection of
+// the dropped candidates, and the order-preserving in-place compaction.
+//
+// One workgroup owns one (sequence, layer, KV head) region for the whole
+// event (Eq. 1 with Section 3's scores; Appendix F: per-KV-head eviction,
+// keep-sets sorted chronologically, compaction by a gather):
+//   1. every candidate slot (outside the prompt and the r most recent rows)
+//      gets its 64-bit Philox score, held in registers (KPT per thread, in
+//      slot order);
+//   2. an MSB-first radix select over the composite (score, candidate index)
+//      finds the m = |C| - k_keep smallest, 8 bits per pass in an LDS
+//      histogram (usually 2 passes: after 16 bits the bucket is exact);
+//   3. a block scan turns the drop flags into the sorted drop list, stored as
+//      f[k] = d_k - k, so that destination row j receives source row
+//      j + #{k : f[k] <= j};
+//   4. the surviving rows are moved down in chunks of 64 destination rows:
+//      every thread gathers its part of the chunk into registers, the block
+//      waits until all loads have returned and synchronises, then writes.
+//      Sources are never below destinations and a chunk's writes land below
+//      the next chunk's sources, so the in-place move is race-free.
+#include "philox.h"
+#include "ra_internal.h"
+
+namespace ra {
+namespace {
+
+using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
+
+constexpr int kChunk = 64;
+
+__device__ __forceinline__ int score_digit(int level, uint64_t score, int c) {
+  if (level < 8) return static_cast<int>((score >> (56 - 8 * level)) & 0xFF);
+  return level == 8 ? ((c >> 8) & 0xFF) : (c & 0xFF);
+}
+
+__device__ __forceinline__ int wave_inclusive_scan(int x) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+
+// Number of f[k] <= x for the non-decreasing list f[0..m).
+__device__ __forceinline__ int count_le(const int* f, int m, int x) {
+  int lo = 0, hi = m;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (f[mid] <= x) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ int64_t vt_index(int64_t row, int ch) {
+  // element index of (row, channel) in the transposed 8-row value tiles
+  return (row & ~int64_t(7)) * kHeadDim + ch * 8 + (row & 7);
+}
+
+template <int NT, int KPT, typename E, bool POS_ONLY>
+__global__ __launch_bounds__(NT) void evict_kernel(
+    const SeqMeta* __restrict__ meta, E* __restrict__ kpool,
+    E* __restrict__ vpool, int32_t* __restrict__ pos, int L, int Hkv, int r,
+    int slot_lo) {
+  static_assert(KPT <= 32, "drop flags live in one 32-bit mask");
+  constexpr int kWaves = NT / 64;
+  constexpr int kEpu = 16 / sizeof(E);            // elements per 16-byte unit
+  constexpr int kKUnitsRow = kHeadDim / kEpu;     // 16-byte units per key row
+  constexpr int kVUnitsCh = 8 / kEpu;             // units per (tile, channel)
+  constexpr int kKUnits = kChunk * kKUnitsRow;
+  constexpr int kVUnits = (kChunk / 8) * kHeadDim * kVUnitsCh;
+  constexpr int kKPer = (kKUnits + NT - 1) / NT;
+  constexpr int kVPer = (kVUnits + NT - 1) / NT;
+
+  __shared__ int hist[256];
+  __shared__ int f[kMaxEvery];
+  __shared__ int src_of[kChunk];
+  __shared__ int wave_tot[kWaves];
+  __shared__ int sel[3];
+
+  const int per_seq = L * Hkv;
+  const int slot = slot_lo + static_cast<int>(blockIdx.x) / per_seq;
+  const int lg = static_cast<int>(blockIdx.x) % per_seq;
+  const int layer = lg / Hkv, g = lg % Hkv;
+  const SeqMeta& Mref = meta[slot];
+  if (!Mref.active || !Mref.due) return;
+  const int lp = Mref.prompt_len, old_len = Mref.plan_len;
+  const int event = Mref.plan_event;
+  const uint64_t seed = Mref.seed, rid = Mref.rid;
+  const int C = old_len - lp - r;
+  const int m = C - Mref.k_keep;
+  if (m <= 0) return;
+  const int new_len = old_len - m;
+  const int64_t region = Mref.base + static_cast<int64_t>(lg) * Mref.cap;
+  int32_t* P = pos + region;
+  const int t = threadIdx.x;
+
+  // 1. scores of this thread's KPT consecutive candidates
+  uint64_t score[KPT];
+  uint32_t undecided = 0, drop = 0;
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    const int c = t * KPT + i;
+    score[i] = 0;
+    if (c < C) {
+      score[i] = philox_score(static_cast<uint64_t>(P[lp + c]),
+                              static_cast<uint64_t>(event),
+                              static_cast<uint64_t>(layer),
+                              static_cast<uint64_t>(g), seed, rid);
+      undecided |= 1u << i;
+    }
+  }
+
+  // 2. radix select of the m smallest (score, index)
+  int remaining = m;
+  for (int level = 0; level < 10; ++level) {
+    for (int i = t; i < 256; i += NT) hist[i] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < KPT; ++i)
+      if ((undecided >> i) & 1)
+        atomicAdd(&hist[score_digit(level, score[i], t * KPT + i)], 1);
+    __syncthreads();
+    if (t < 64) {
+      const int h0 = hist[4 * t], h1 = hist[4 * t + 1];
+      const int h2 = hist[4 * t + 2], h3 = hist[4 * t + 3];
+      const int s = h0 + h1 + h2 + h3;
+      int cum = wave_inclusive_scan(s) - s;
+      const int hs[4] = {h0, h1, h2, h3};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        if (cum < remaining && remaining <= cum + hs[j]) {
+          sel[0] = 4 * t + j;
+          sel[1] = cum;
+          sel[2] = hs[j];
+        }
+        cum += hs[j];
+      }
+    }
+    __syncthreads();
+    const int v = sel[0], below = sel[1], cnt = sel[2];
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      if ((undecided >> i) & 1) {
+        const int dg = score_digit(level, score[i], t * KPT + i);
+        if (dg < v) {
+          drop |= 1u << i;
+          undecided &= ~(1u << i);
+        } else if (dg > v) {
+          undecided &= ~(1u << i);
+        }
+      }
+    }
+    remaining -= below;
+    if (cnt == remaining) {       // the whole bucket goes: selection complete
+      drop |= undecided;
+      undecided = 0;
+      break;
+    }
+    __syncthreads();
+  }
+
+  // 3. sorted drop list as f[k] = d_k - k
+  const int mine = __popc(drop);
+  const int incl = wave_inclusive_scan(mine);
+  if ((t & 63) == 63) wave_tot[t >> 6] = incl;
+  __syncthreads();
+  int k = incl - mine;
+  for (int w = 0; w < (t >> 6); ++w) k += wave_tot[w];
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    if ((drop >> i) & 1) {
+      f[k] = lp + t * KPT + i - k;
+      ++k;
+    }
+  }
+  __syncthreads();
+  const int d0 = f[0];
+
+  // 4. order-preserving in-place compaction of positions, keys and values
+  const E zero_e = E(0);
+  for (int j0 = d0 & ~7; j0 < new_len; j0 += kChunk) {
+    if (t < kChunk) src_of[t] = j0 + t + count_le(f, m, j0 + t);
+    __syncthreads();
+
+    int pval = 0;
+    const bool pos_mine = t < kChunk && j0 + t >= d0 && j0 + t < new_len;
+    if (pos_mine) pval = P[src_of[t]];
+    u32x4 kbuf[POS_ONLY ? 1 : kKPer];
+    E vbuf[POS_ONLY ? 1 : kVPer][kEpu];
+    if constexpr (!POS_ONLY) {
+#pragma unroll
+      for (int q = 0; q < kKPer; ++q) {
+        const int u = t + q * NT;
+        const int row = u / kKUnitsRow, col = u % kKUnitsRow;
+        const int j = j0 + row;
+        if (u < kKUnits && j >= d0 && j < new_len) {
+          const E* src = kpool + (region + src_of[row]) * kHeadDim + col * kEpu;
+          kbuf[q] = *reinterpret_cast<const u32x4*>(src);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kVPer; ++q) {
+        const int u = t + q * NT;
+        const int tile = u / (kHeadDim * kVUnitsCh);
+        const int rem = u % (kHeadDim * kVUnitsCh);
+        const int ch = rem / kVUnitsCh, part = rem % kVUnitsCh;
+        const int jt = j0 + tile * 8 + part * kEpu;
+        if (u < kVUnits && j0 + tile * 8 < new_len) {
+#pragma unroll
+          for (int e = 0; e < kEpu; ++e) {
+            const int sj = src_of[jt + e - j0];
+            vbuf[q][e] = sj < old_len ? vpool[vt_index(region + sj, ch)] : zero_e;
+          }
+        }
+      }
+    }
+    // every load of this chunk has returned before any thread writes
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+
+    if (pos_mine) P[j0 + t] = pval;
+    if constexpr (!POS_ONLY) {
+#pragma unroll
+      for (int q = 0; q < kKPer; ++q) {
+        const int u = t + q * NT;
+        const int row = u / kKUnitsRow, col = u % kKUnitsRow;
+        const int j = j0 + row;
+        if (u < kKUnits && j >= d0 && j < new_len) {
+          E* dst = kpool + (region + j) * kHeadDim + col * kEpu;
+          *reinterpret_cast<u32x4*>(dst) = kbuf[q];
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kVPer; ++q) {
+        const int u = t + q * NT;
+        const int tile = u / (kHeadDim * kVUnitsCh);
+        const int rem = u % (kHeadDim * kVUnitsCh);
+        const int ch = rem / kVUnitsCh, part = rem % kVUnitsCh;
+        if (u < kVUnits && j0 + tile * 8 < new_len) {
+          E* dst = vpool + vt_index(region + j0 + tile * 8, ch) + part * kEpu;
+          u32x4 w;
+          __builtin_memcpy(&w, vbuf[q], 16);
+          *reinterpret_cast<u32x4*>(dst) = w;
+        }
+      }
+    }
+  }
+}
+
+template <int NT, int KPT, bool POS_ONLY>
+hipError_t launch_kpt(const Shape& sh, const SeqMeta* meta, void* kpool,
+                      void* vpool, int32_t* pos, int slot_lo, int slot_hi,
+                      hipStream_t s) {
+  const dim3 grid((slot_hi - slot_lo) * sh.L * sh.Hkv);
+  if (sh.dtype == 1) {
+    hipLaunchKernelGGL((evict_kernel<NT, KPT, uint16_t, POS_ONLY>), grid,
+                       dim3(NT), 0, s, meta, static_cast<uint16_t*>(kpool),
+                       static_cast<uint16_t*>(vpool), pos, sh.L, sh.Hkv, sh.r,
+                       slot_lo);
+  } else {
+    hipLaunchKernelGGL((evict_kernel<NT, KPT, float, POS_ONLY>), grid,
+                       dim3(NT), 0, s, meta, static_cast<float*>(kpool),
+                       static_cast<float*>(vpool), pos, sh.L, sh.Hkv, sh.r,
+                       slot_lo);
+  }
+  return hipGetLastError();
+}
+
+template <bool POS_ONLY>
+hipError_t launch_mode(const Shape& sh, const SeqMeta* meta, void* kpool,
+                       void* vpool, int32_t* pos, int slot_lo, int slot_hi,
+                       int max_candidates, hipStream_t s) {
+  if (max_candidates <= 512 * 1)
+    return launch_kpt<512, 1, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+  if (max_candidates <= 512 * 2)
+    return launch_kpt<512, 2, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+  if (max_candidates <= 512 * 4)
+    return launch_kpt<512, 4, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+  if (max_candidates <= 512 * 8)
+    return launch_kpt<512, 8, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+  if (max_candidates <= 512 * 16)
+    return launch_kpt<512, 16, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+  if (max_candidates <= 512 * 32)
+    return launch_kpt<512, 32, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+  if (max_candidates <= kMaxCandidates)
+    return launch_kpt<1024, 32, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_evict(const Shape& sh, const SeqMeta* meta, void* kpool,
+                        void* vpool, int32_t* pos, int slot_lo, int slot_hi,
+                        int max_candidates, bool positions_only,
+                        hipStream_t s) {
+  if (slot_hi <= slot_lo) return hipSuccess;
+  if (positions_only)
+    return launch_mode<true>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi,
+                             max_candidates, s);
+  return launch_mode<false>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi,
+                            max_candidates, s);
+}
+
+}  // namespace ra

@@ -1,0 +1,93 @@
+// Internal definitions shared by the host library and the HIP kernels.
+//
+// HBM layout (one ra_cache):
+//   K pool  [pool_rows][128]          row-major rows, dtype E
+//   V pool  [pool_rows / 8][128][8]   tiles of 8 rows stored transposed, so a
+//                                     16-byte load holds 8 consecutive rows of
+//                                     one channel (the MFMA operand shape of
+//                                     the P.V product)
+//   pos     [pool_rows]               int32 token position of each row
+// A sequence owns L * Hkv consecutive regions of `cap` rows (cap a multiple
+// of 32); region (l, g) starts at row base + (l * Hkv + g) * cap.  Rows
+// [0, len) of a region are cached, in chronological order.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ra {
+
+constexpr int kHeadDim = 128;
+constexpr int kMaxGroup = 16;       // query heads per KV head (MFMA N tile)
+constexpr int kMaxSplits = 64;      // attention work items per head
+constexpr int kMaxEvery = 1024;     // evict_every limit: drops per event <= this
+constexpr int kMaxCandidates = 32768;
+constexpr int kRegionAlign = 32;    // region rows rounded to the key block
+
+// Per-slot device state, 64 bytes.  The hot-path kernels read it; the
+// end-of-step and plan kernels update it; the host keeps an identical mirror.
+struct SeqMeta {
+  int64_t base;        // first pool row of the sequence's regions
+  int32_t cap;         // rows per (layer, KV head) region
+  int32_t prompt_len;  // lp
+  int32_t len;         // cached rows per region between steps
+  int32_t step;        // completed decode steps
+  int32_t event;       // eviction events performed
+  int32_t k_keep;      // evictable rows kept per head
+  uint64_t seed;       // Philox key word 0
+  uint64_t rid;        // Philox key word 1 (request id)
+  int32_t active;
+  int32_t due;         // 1: an eviction is planned for this sequence
+  int32_t plan_len;    // rows per region before the planned eviction
+  int32_t plan_event;  // event index of the planned eviction
+};
+static_assert(sizeof(SeqMeta) == 64, "SeqMeta must stay 64 bytes");
+
+struct Shape {
+  int L, Hq, Hkv, G, r, every, dtype;  // dtype: 0 f32, 1 bf16
+};
+
+// ---- launch wrappers (defined in the .hip files) ----------------------------
+
+hipError_t launch_zero_words(uint32_t* p, int64_t n_words, hipStream_t s);
+hipError_t launch_seq_set(SeqMeta* meta, int slot, const SeqMeta& v, hipStream_t s);
+hipError_t launch_advance(SeqMeta* meta, int slot_lo, int slot_hi, int n_steps,
+                          int r, int every, hipStream_t s);
+hipError_t launch_plan_now(SeqMeta* meta, int slot, int r, hipStream_t s);
+hipError_t launch_append_positions(const SeqMeta* meta, int32_t* pos, int slot_lo,
+                                   int slot_hi, int L, int Hkv, int run,
+                                   hipStream_t s);
+hipError_t launch_evict(const Shape& sh, const SeqMeta* meta, void* kpool,
+                        void* vpool, int32_t* pos, int slot_lo, int slot_hi,
+                        int max_candidates, bool positions_only, hipStream_t s);
+hipError_t launch_write_rows(const Shape& sh, int64_t base, int cap, int len,
+                             const void* k_src, const void* v_src,
+                             const int32_t* pos_src, void* kpool, void* vpool,
+                             int32_t* pos, hipStream_t s);
+hipError_t launch_read_rows(const Shape& sh, int64_t region_row, int len,
+                            const void* kpool, const void* vpool, void* k_out,
+                            void* v_out, hipStream_t s);
+hipError_t launch_export_positions(const Shape& sh, int64_t base, int cap,
+                                   int len, const int32_t* pos, int32_t* out,
+                                   hipStream_t s);
+
+struct AttnLaunch {
+  const SeqMeta* meta;
+  void* kpool;
+  void* vpool;
+  int32_t* pos;
+  const void* q;
+  const void* k_new;
+  const void* v_new;
+  void* out;
+  float* ws_o;         // [heads][kMaxSplits][G][128] partial numerators
+  float* ws_ml;        // [heads][kMaxSplits][G][2]  running max (log2), sum
+  int32_t* counters;   // [heads] completed work items of this launch
+  int layer;
+  int max_seqs;
+  int split_keys;
+  int max_splits;
+};
+hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s);
+
+}  // namespace ra

@@ -1,0 +1,163 @@
+"""Helpers shared by the GPU parity tests (not collected by pytest).
+
+A ``Run`` drives the HIP path through the C ABI (via the ctypes binding) on
+seeded synthetic rows; ``OracleSeq`` replays the same sequence with the CPU
+oracle on the same rows.  The two share only the workload generator.
+"""
+
+import numpy as np
+import torch
+
+from oracle.attention import gqa_decode
+from oracle.evict import SequenceReplay, keep_count
+from paper_2609_03430_amd import binding as B
+from paper_2609_03430_amd.synth import Workload
+
+DEV = "cuda"
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+class Run:
+    """One cache with several sequences, stepped in lock-step."""
+
+    def __init__(self, L, Hq, Hkv, K, lps, r=64, every=64, dtype=B.RA_BF16,
+                 mode=B.RA_BUDGET_EVICTABLE, seeds=None, rids=None,
+                 scaled=True, wl_seed=1000, ring=None, attn_split=0,
+                 max_seqs=None, write_prompt=True):
+        self.L, self.Hq, self.Hkv, self.K, self.r, self.every = L, Hq, Hkv, K, r, every
+        self.G = Hq // Hkv
+        self.lps = list(lps)
+        n = len(self.lps)
+        self.n = n
+        self.max_seqs = max_seqs or n
+        self.seeds = list(seeds) if seeds is not None else [7 + 13 * i for i in range(n)]
+        self.rids = list(rids) if rids is not None else list(range(n))
+        self.mode = mode
+        self.tdtype = torch.bfloat16 if dtype == B.RA_BF16 else torch.float32
+        self.cfg = B.make_config(L, Hq, Hkv, K, r, every, mode, dtype, self.max_seqs,
+                                 attn_split=attn_split)
+        rows = sum(B.ra_seq_rows(self.cfg, lp) for lp in self.lps)
+        self.cache = B.Cache(self.cfg, rows)
+        self.h = self.cache.handle
+        self.wl = Workload(wl_seed, L, Hq, Hkv, 128, self.tdtype, scaled, ring=ring,
+                           device=DEV)
+        self.slots = list(range(n))
+        self.steps = [0] * n
+        for slot, lp in enumerate(self.lps):
+            kp = vp = None
+            if write_prompt and lp > 0:
+                kp, vp = self.prompt_rows(slot, lp)
+            B.ra_seq_begin(self.h, slot, lp, self.seeds[slot], self.rids[slot], kp, vp)
+
+    def k_keep(self, slot):
+        return keep_count(self.K, self.lps[slot], self.mode)
+
+    def prompt_rows(self, slot, lp):
+        l = torch.arange(self.L, device=DEV).view(-1, 1, 1)
+        g = torch.arange(self.Hkv, device=DEV).view(1, -1, 1)
+        p = torch.arange(lp, device=DEV).view(1, 1, -1)
+        rid = self.rids[slot]
+        return (self.wl.k_rows(rid, l, g, p, lp).contiguous(),
+                self.wl.v_rows(rid, l, g, p, lp).contiguous())
+
+    def step_inputs(self, layer):
+        """q [max_seqs,Hq,d], k/v [max_seqs,Hkv,d] for the current step."""
+        q = torch.zeros(self.max_seqs, self.Hq, 128, dtype=self.tdtype, device=DEV)
+        k = torch.zeros(self.max_seqs, self.Hkv, 128, dtype=self.tdtype, device=DEV)
+        v = torch.zeros_like(k)
+        rids = torch.tensor([self.rids[s] for s in self.slots], device=DEV)
+        steps = torch.tensor(self.steps, device=DEV)
+        lps = torch.tensor(self.lps, device=DEV)
+        q[: self.n] = self.wl.q_step(rids, layer, steps)
+        kk, vv = self.wl.kv_step(rids, layer, lps + steps, lps)
+        k[: self.n] = kk
+        v[: self.n] = vv
+        return q, k, v
+
+    def step(self):
+        """One decode step of every sequence; returns out [L, max_seqs, Hq, d]."""
+        outs = torch.empty(self.L, self.max_seqs, self.Hq, 128, dtype=self.tdtype,
+                           device=DEV)
+        for layer in range(self.L):
+            q, k, v = self.step_inputs(layer)
+            self.cache.decode(layer, q, k, v, outs[layer])
+        evicted = B.ra_end_step(self.h)
+        self.steps = [s + 1 for s in self.steps]
+        return outs, evicted
+
+    def fast_forward(self, n):
+        B.ra_fast_forward(self.h, n)
+        self.steps = [s + n for s in self.steps]
+
+    def materialise(self, slot):
+        """Write the rows of the currently cached positions (after a fast
+        forward) from the workload generator."""
+        info = B.ra_get_seq_info(self.h, slot)
+        n = info.len
+        pos = torch.empty(self.L * self.Hkv * n, dtype=torch.int32, device=DEV)
+        B.ra_export_positions(self.h, slot, pos)
+        pos = pos.view(self.L, self.Hkv, n).long()
+        l = torch.arange(self.L, device=DEV).view(-1, 1, 1)
+        g = torch.arange(self.Hkv, device=DEV).view(1, -1, 1)
+        rid = self.rids[slot]
+        lp = self.lps[slot]
+        k = self.wl.k_rows(rid, l, g, pos, lp).contiguous()
+        v = self.wl.v_rows(rid, l, g, pos, lp).contiguous()
+        B.ra_write_rows(self.h, slot, k, v)
+        torch.cuda.synchronize()
+
+    def positions(self, slot, layer, g):
+        info = B.ra_get_seq_info(self.h, slot)
+        return B.ra_read_positions(self.h, slot, layer, g, info.cap)
+
+    def rows(self, slot, layer, g):
+        info = B.ra_get_seq_info(self.h, slot)
+        k = torch.empty(info.len, 128, dtype=self.tdtype, device=DEV)
+        v = torch.empty_like(k)
+        B.ra_read_rows(self.h, slot, layer, g, k, v)
+        torch.cuda.synchronize()
+        return k.cpu(), v.cpu()
+
+    def close(self):
+        self.cache.close()
+
+
+class OracleSeq:
+    """The CPU oracle's view of one sequence of a Run (same rows)."""
+
+    def __init__(self, run, slot, heads=None):
+        self.run = run
+        self.slot = slot
+        self.lp = run.lps[slot]
+        self.rid = run.rids[slot]
+        self.heads = heads or [(l, g) for l in range(run.L) for g in range(run.Hkv)]
+        self.rep = SequenceReplay(self.lp, run.k_keep(slot), run.r, run.every,
+                                  run.seeds[slot], self.rid, self.heads)
+        self.wl = run.wl.to("cpu")
+
+    def advance(self, n):
+        self.rep.advance(n)
+
+    def rows(self, layer, g, P):
+        k = self.wl.k_rows(self.rid, layer, g, torch.as_tensor(P), self.lp)
+        v = self.wl.v_rows(self.rid, layer, g, torch.as_tensor(P), self.lp)
+        return k, v
+
+    def attend(self, layer, step0):
+        """Outputs [Hq, d] float64 of `layer` at 0-based step ``step0``; the
+        replay must hold the cache after that step's append."""
+        run = self.run
+        q = self.wl.q_rows(self.rid, layer, torch.arange(run.Hq), step0)
+        Ks, Vs = [], []
+        for g in range(run.Hkv):
+            k, v = self.rows(layer, g, self.rep.P[(layer, g)])
+            Ks.append(k.double().numpy())
+            Vs.append(v.double().numpy())
+        return gqa_decode(q.double().numpy(), Ks, Vs)
+
+
+def max_abs(a, b):
+    return float(np.max(np.abs(np.asarray(a, dtype=np.float64) - np.asarray(b, dtype=np.float64))))

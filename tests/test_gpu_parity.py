@@ -1,0 +1,167 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Kept-position sets and the compacted key/value rows must match bit-exactly;
+attention outputs within max abs error 1e-5 (fp32) / 2e-2 (bf16) of the
+fp64 oracle, the tolerances the workloads fix.  Inputs come from the seeded
+workload generator; the oracle computes its own kept sets from the seeds.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_harness import OracleSeq, Run, log, max_abs
+from paper_2609_03430_amd import binding as B
+
+pytestmark = pytest.mark.gpu
+
+TOL = {B.RA_BF16: 2e-2, B.RA_F32: 1e-5}
+
+
+def _check_heads(run, oracles, rows=True):
+    for o in oracles:
+        for (layer, g) in o.heads:
+            got = run.positions(o.slot, layer, g)
+            want = o.rep.P[(layer, g)]
+            assert np.array_equal(got, want), (o.slot, layer, g, o.rep.step)
+            if rows:
+                k, v = run.rows(o.slot, layer, g)
+                kw, vw = o.rows(layer, g, want)
+                assert torch.equal(k, kw), (o.slot, layer, g)
+                assert torch.equal(v, vw), (o.slot, layer, g)
+
+
+@pytest.mark.parametrize("dtype", [B.RA_BF16, B.RA_F32])
+def test_small_decode_parity(dtype):
+    """Three sequences (prompts 5, 0, 17), r=8, every=8, K=40, 150 steps:
+    every output, and every head's positions and rows after every event."""
+    log("small decode parity dtype=%d" % dtype)
+    run = Run(L=2, Hq=4, Hkv=2, K=40, lps=[5, 0, 17], r=8, every=8, dtype=dtype)
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    worst = 0.0
+    events = 0
+    for t in range(150):
+        outs, ev = run.step()
+        outs = outs.float().cpu()
+        for o in oracles:
+            o.rep.append()
+            for layer in range(run.L):
+                want = o.attend(layer, t)
+                err = max_abs(outs[layer, o.slot], want)
+                worst = max(worst, err)
+                assert err <= TOL[dtype], (t, o.slot, layer, err)
+            o.rep.end_step()
+        if ev:
+            events += 1
+            _check_heads(run, oracles)
+    log("  events=%d worst=%.3g" % (events, worst))
+    assert events >= 10
+    run.close()
+
+
+@pytest.mark.parametrize("lp,K,r,every,mode", [
+    (37, 100, 16, 16, B.RA_BUDGET_EVICTABLE),
+    (0, 64, 0, 1, B.RA_BUDGET_EVICTABLE),
+    (300, 300, 64, 64, B.RA_BUDGET_TOTAL),        # k_keep = 0
+    (5, 1000, 64, 64, B.RA_BUDGET_EVICTABLE),
+    (129, 8192, 64, 64, B.RA_BUDGET_EVICTABLE),   # 8256 candidates
+])
+def test_fast_forward_and_evict_now(lp, K, r, every, mode):
+    """Positions-only fast forward and explicit events at arbitrary steps
+    keep the same sets as the oracle; rows written afterwards are compacted
+    exactly by a full event."""
+    log("fast forward lp=%d K=%d r=%d every=%d mode=%d" % (lp, K, r, every, mode))
+    run = Run(L=2, Hq=2, Hkv=2, K=K, lps=[lp, max(0, lp - 3)], r=r, every=every, mode=mode,
+              seeds=[2**63 + 11, 5], rids=[2**40 + 1, 9])
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    rng = np.random.default_rng(lp + K)
+    for rep in range(3 if K <= 1000 else 1):
+        n = int(rng.integers(1, 2 * (K + r + every)))
+        run.fast_forward(n)
+        for o in oracles:
+            o.advance(n)
+        _check_heads(run, oracles, rows=False)
+        for s in range(run.n):
+            run.materialise(s)
+        # append a few rows so the event has candidates, then evict now
+        for _ in range(int(rng.integers(1, max(2, every)))):
+            run.step()
+            for o in oracles:
+                o.rep.append()
+                o.rep.end_step()
+        for s in range(run.n):
+            B.ra_evict_now(run.h, s)
+            oracles[s].rep.evict_now()
+        _check_heads(run, oracles, rows=True)
+    run.close()
+
+
+def test_batching_invariance():
+    """A request keeps the same sets alone in slot 0 and inside a batch in
+    slot 3 (the scores depend on the request, not on the memory slot)."""
+    log("batching invariance")
+    alone = Run(L=1, Hq=4, Hkv=4, K=50, lps=[20], r=8, every=8, seeds=[99], rids=[4242])
+    batch = Run(L=1, Hq=4, Hkv=4, K=50, lps=[3, 40, 7, 20], r=8, every=8,
+                seeds=[1, 2, 3, 99], rids=[1, 2, 3, 4242])
+    for _ in range(200):
+        alone.step()
+        batch.step()
+    for g in range(4):
+        assert np.array_equal(alone.positions(0, 0, g), batch.positions(3, 0, g))
+        ka, va = alone.rows(0, 0, g)
+        kb, vb = batch.rows(3, 0, g)
+        assert torch.equal(ka, kb) and torch.equal(va, vb)
+    alone.close()
+    batch.close()
+
+
+@pytest.mark.parametrize("dtype", [B.RA_BF16, B.RA_F32])
+@pytest.mark.parametrize("Hq,Hkv,split", [(1, 1, 32), (4, 2, 64), (10, 2, 0),
+                                          (8, 1, 32), (16, 1, 96), (40, 8, 0)])
+def test_attention_shapes(dtype, Hq, Hkv, split):
+    """Group sizes 1..16, forced small splits (many partials merged), ragged
+    lengths within a batch, and a first step with a single cached row."""
+    log("attention shapes dtype=%d Hq=%d Hkv=%d split=%d" % (dtype, Hq, Hkv, split))
+    lps = [0, 1, 31, 32, 33, 250]
+    run = Run(L=1, Hq=Hq, Hkv=Hkv, K=200, lps=lps, r=16, every=16, dtype=dtype,
+              attn_split=split)
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    checked = 0
+    for t in range(70):
+        outs, _ = run.step()
+        outs = outs.float().cpu()
+        for o in oracles:
+            o.rep.append()
+            if t in (0, 1, 2, 31, 32, 47, 69):
+                err = max_abs(outs[0, o.slot], o.attend(0, t))
+                assert err <= TOL[dtype], (t, o.slot, err)
+                checked += 1
+            o.rep.end_step()
+    assert checked == 7 * len(lps)
+    run.close()
+
+
+def test_tiny_config_full_run():
+    """The tiny single-layer case in full: 1 sequence, 4 query / 2 KV heads,
+    fp32, prompt 128, r=64, K=256, 1024 decode steps, evicting every 64 steps
+    once over budget.  Every output of every step within 1e-5 of the fp64
+    oracle; kept sets bit-exact after each of the 11 events."""
+    log("tiny config full run")
+    run = Run(L=1, Hq=4, Hkv=2, K=256, lps=[128], r=64, every=64, dtype=B.RA_F32,
+              scaled=False, seeds=[1000], rids=[0])
+    o = OracleSeq(run, 0)
+    worst = 0.0
+    events = 0
+    for t in range(1024):
+        outs, ev = run.step()
+        o.rep.append()
+        err = max_abs(outs[0, 0].cpu(), o.attend(0, t))
+        worst = max(worst, err)
+        assert err <= 1e-5, (t, err)
+        o.rep.end_step()
+        if ev:
+            events += 1
+            _check_heads(run, [o])
+    log("  events=%d worst=%.3g" % (events, worst))
+    assert events == 11
+    run.close()
