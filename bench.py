@@ -1,0 +1,325 @@
+#!/usr/bin/env python
+"""Decode throughput of the Random Attention hot path on one MI355X.
+
+A step is one decode step of the whole attention stack for every sequence
+of the batch: for each layer, append the new key/value and run GQA decode
+attention over the compressed cache; then the end-of-step eviction (every
+64 steps, per KV head, uniform random, with compaction).  Model projections
+and MLPs are not part of the path and are not run.
+
+Default workload: the Qwen3-14B-shaped headline case (40 layers, 40 query /
+8 KV heads, head_dim 128, bf16, batch 32, prompt 1024, K=8192, r=64,
+eviction every 64 steps) in its steady state at the end of a 32k-token
+generation: the state at step T - warmup - steps is reached with the
+positions-only fast forward (the same sampler and trigger), the kept rows
+are materialised from the seeded generator, then `warmup` untimed and
+`steps` timed decode steps run up to step 32768.  Inputs (a 64-step ring of
+q, k_new, v_new for every layer) are resident in HBM before timing.
+
+Prints one JSON line.  `value` is tokens/s = batch * steps / wall time.
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("decode tokens/s incl. eviction at 32k gen; attention+compaction "
+          "HBM GB/s vs peak")
+PEAK_HBM_GBS = 8000.0     # MI355X HBM3E, AMD published
+
+WORKLOADS = {
+    "qwen3-14b": dict(L=40, Hq=40, Hkv=8, B=32, lp=1024, T=32768, K=8192,
+                      desc="Qwen3-14B-shaped attention stack: 40 layers, 40 Q / 8 KV "
+                           "heads, head_dim 128, bf16, batch 32, prompt 1024, 32768 "
+                           "generated tokens, K=8192, r=64, evict every 64 steps"),
+    "qwen3-4b": dict(L=36, Hq=32, Hkv=8, B=16, lp=512, T=32768, K=8192,
+                     desc="Qwen3-4B-shaped attention stack: 36 layers, 32 Q / 8 KV "
+                          "heads, head_dim 128, bf16, batch 16, prompt 512, 32768 "
+                          "generated tokens, K=8192, r=64, evict every 64 steps"),
+    "qwen3-32b": dict(L=64, Hq=64, Hkv=8, B=16, lp=4096, T=32768, K=4096,
+                      desc="Qwen3-32B-shaped attention stack: 64 layers, 64 Q / 8 KV "
+                           "heads, head_dim 128, bf16, batch 16, prompt 4096, 32768 "
+                           "generated tokens, K=4096, r=64, evict every 64 steps"),
+}
+R = 64
+EVERY = 64
+RING = 64
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for name in ("attention.hip", "evict.hip"):
+        with open(os.path.join(ROOT, "paper_2609_03430_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload):
+    """HBM traffic per attention launch measured with rocprofv3 counters, if a
+    summary for the current kernel sources exists under profiles/."""
+    path = os.path.join(ROOT, "profiles", "attention_traffic_%s.json" % workload)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(w, seed, t0, steps):
+    """The CPU oracle, untuned, on one sequence x one layer x all KV heads for
+    `steps` steady-state decode steps (one eviction event included)."""
+    import numpy as np
+    import torch
+    from oracle.attention import gqa_decode
+    from oracle.evict import SequenceReplay
+    from paper_2609_03430_amd.synth import Workload
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    L, Hq, Hkv, lp, K = w["L"], w["Hq"], w["Hkv"], w["lp"], w["K"]
+    wl = Workload(seed, L, Hq, Hkv, 128, torch.bfloat16, True, ring=RING)
+    layer, rid = 0, 0
+    heads = [(layer, g) for g in range(Hkv)]
+    rep = SequenceReplay(lp, K, R, EVERY, seed, rid, heads)
+    rep.advance(t0)
+    # rows resident in RAM before timing, as the GPU's are in HBM
+    new = np.arange(lp + t0, lp + t0 + steps)
+    tables = []
+    for g in range(Hkv):
+        P = np.union1d(rep.P[(layer, g)], new)
+        k = wl.k_rows(rid, layer, g, torch.as_tensor(P), lp).double().numpy()
+        v = wl.v_rows(rid, layer, g, torch.as_tensor(P), lp).double().numpy()
+        tables.append((P, k, v))
+    qs = [wl.q_rows(rid, layer, torch.arange(Hq), t0 + s).double().numpy()
+          for s in range(steps)]
+    t_start = time.perf_counter()
+    for s in range(steps):
+        rep.append()
+        Ks, Vs = [], []
+        for g in range(Hkv):
+            P, k, v = tables[g]
+            idx = np.searchsorted(P, rep.P[(layer, g)])
+            Ks.append(k[idx])
+            Vs.append(v[idx])
+        gqa_decode(qs[s], Ks, Vs)
+        rep.end_step()
+    elapsed = time.perf_counter() - t_start
+    return {
+        "value": steps / (elapsed * L),
+        "unit": "tokens/s",
+        "cores": int(threads),
+        "kind": "oracle",
+        "sample": ("1 sequence x 1 layer x %d KV heads (%d query heads), %d decode "
+                   "steps at steps %d..%d incl. %d eviction event(s), numpy fp64; "
+                   "tokens/s = steps / (time x %d layers), i.e. the oracle's rate on "
+                   "the whole job" % (Hkv, Hq, steps, t0 + 1, t0 + steps,
+                                      len([1 for st, _ in rep.log if st > t0]), L)),
+        "seconds": elapsed,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=256)
+    ap.add_argument("--warmup", type=int, default=64)
+    ap.add_argument("--workload", default="qwen3-14b", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-steps", type=int, default=96)
+    ap.add_argument("--attn-split", type=int, default=0)
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: the hot path has no cross-GPU step; "
+              "--gpus %d is not supported" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_03430_amd import binding as B
+    from paper_2609_03430_amd.synth import Workload
+
+    w = WORKLOADS[args.workload]
+    L, Hq, Hkv, Bsz, lp, T, K = (w[k] for k in ("L", "Hq", "Hkv", "B", "lp", "T", "K"))
+    seed = 1000 + {"qwen3-4b": 1, "qwen3-14b": 2, "qwen3-32b": 3}[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+
+    def log(msg):
+        print("[bench] " + msg, file=sys.stderr, flush=True)
+
+    total = args.warmup + args.steps
+    t0 = T - total
+    assert t0 >= 0
+    cfg = B.make_config(L, Hq, Hkv, K, R, EVERY, B.RA_BUDGET_EVICTABLE, B.RA_BF16, Bsz,
+                        attn_split=args.attn_split)
+    rows = B.ra_seq_rows(cfg, lp) * Bsz
+    log("workload %s: pools %.1f GB" % (args.workload, rows * 128 * 2 * 2 / 1e9))
+    cache = B.Cache(cfg, rows, device=dev)
+    h = cache.handle
+    wl = Workload(seed, L, Hq, Hkv, 128, torch.bfloat16, True, ring=RING, device=dev)
+    for b in range(Bsz):
+        B.ra_seq_begin(h, b, lp, seed * 1000003 + b, b)
+    t_ff = time.time()
+    B.ra_fast_forward(h, t0)
+    torch.cuda.synchronize()
+    log("fast forward to step %d: %.2fs" % (t0, time.time() - t_ff))
+    ls = torch.arange(L, device=dev).view(-1, 1, 1)
+    gs = torch.arange(Hkv, device=dev).view(1, -1, 1)
+    for b in range(Bsz):
+        n = B.ra_get_seq_info(h, b).len
+        pos = torch.empty(L * Hkv * n, dtype=torch.int32, device=dev)
+        B.ra_export_positions(h, b, pos)
+        pos = pos.view(L, Hkv, n).long()
+        B.ra_write_rows(h, b, wl.k_rows(b, ls, gs, pos, lp).contiguous(),
+                        wl.v_rows(b, ls, gs, pos, lp).contiguous())
+        del pos
+    torch.cuda.synchronize()
+    log("rows materialised: %.2fs" % (time.time() - t_ff))
+
+    # 64-step input ring for every layer, resident before timing
+    bidx = torch.arange(Bsz, device=dev)
+    q_ring = torch.empty(RING, L, Bsz, Hq, 128, dtype=torch.bfloat16, device=dev)
+    k_ring = torch.empty(RING, L, Bsz, Hkv, 128, dtype=torch.bfloat16, device=dev)
+    v_ring = torch.empty_like(k_ring)
+    for j in range(RING):
+        for l in range(L):
+            q_ring[j, l] = wl.q_step(bidx, l, torch.full((Bsz,), j, device=dev))
+            k, v = wl.kv_step(bidx, l, torch.full((Bsz,), lp + j, device=dev),
+                              torch.full((Bsz,), lp, device=dev))
+            k_ring[j, l] = k
+            v_ring[j, l] = v
+    out = torch.empty(Bsz, Hq, 128, dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    split_keys, max_splits = B.ra_attention_plan(h)
+    log("inputs ready; attention split %d keys x %d" % (split_keys, max_splits))
+
+    def run_steps(first, n, timed):
+        rec = []
+        for i in range(n):
+            s = first + i
+            j = s % RING
+            lens = [B.ra_get_seq_info(h, b).len for b in range(Bsz)] if timed else None
+            evs = []
+            for l in range(L):
+                if timed:
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                B.ra_decode_attention(h, l, q_ring[j, l], k_ring[j, l], v_ring[j, l], out,
+                                      cache.workspace, stream)
+                if timed:
+                    e1.record(stream)
+                    evs.append((e0, e1))
+            if timed:
+                x0 = torch.cuda.Event(enable_timing=True)
+                x1 = torch.cuda.Event(enable_timing=True)
+                x0.record(stream)
+            nev = B.ra_end_step(h, stream)
+            if timed:
+                x1.record(stream)
+                rec.append((lens, evs, (x0, x1), nev))
+        return rec
+
+    run_steps(t0, args.warmup, False)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    rec = run_steps(t0 + args.warmup, args.steps, True)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    tokens = Bsz * args.steps
+    assert B.ra_get_seq_info(h, 0).step == T
+
+    # per-launch durations and algorithmic bytes
+    s_el = 2
+    attn_ms, attn_bytes = [], []
+    ev_ms, ev_bytes = [], []
+    n_events = 0
+    for lens, evs, (x0, x1), nev in rec:
+        per_launch = sum(Hkv * ((n + 1) * 2 * 128 * s_el + (2 * 128 * s_el + 4)) +
+                         2 * Hq * 128 * s_el for n in lens)
+        for e0, e1 in evs:
+            attn_ms.append(e0.elapsed_time(e1))
+            attn_bytes.append(per_launch)
+        if nev:
+            n_events += 1
+            C = K + EVERY
+            m = EVERY
+            moved = (lp + K + R) - (lp + (C - m) / (m + 1))
+            per_head = moved * (2 * 128 * s_el + 4) * 2 + C * 4
+            ev_ms.append(x0.elapsed_time(x1))
+            ev_bytes.append(per_head * nev * L * Hkv)
+    attn_avg_ms = sum(attn_ms) / len(attn_ms)
+    attn_gbs = sum(attn_bytes) / (sum(attn_ms) * 1e-3) / 1e9
+    comp = None
+    if ev_ms:
+        comp = {
+            "events_timed": n_events,
+            "avg_ms_per_event": sum(ev_ms) / len(ev_ms),
+            "achieved_gbs": sum(ev_bytes) / (sum(ev_ms) * 1e-3) / 1e9,
+            "peak_gbs": PEAK_HBM_GBS,
+            "frac": sum(ev_bytes) / (sum(ev_ms) * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "bytes_note": "expected rows moved by the order-preserving shift "
+                          "(prompt + first drop onward) x (key + value + position) x 2, "
+                          "plus candidate positions read",
+        }
+    total_bytes = sum(attn_bytes) + sum(ev_bytes)
+    result = {
+        "metric": METRIC,
+        "value": tokens / wall,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall * 1e3 / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": w["desc"],
+            "timed_window": "decode steps %d..%d of %d (steady state, %d eviction events)"
+                            % (t0 + args.warmup + 1, T, T, n_events),
+            "global_batch": Bsz,
+            "seq_len": lp + T,
+            "attn_split_keys": split_keys,
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "attn_bf16_kernel",
+            "achieved": attn_gbs,
+            "peak": PEAK_HBM_GBS,
+            "unit": "GB/s",
+            "frac": attn_gbs / PEAK_HBM_GBS,
+            "traffic": read_traffic(args.workload),
+            "avg_launch_ms": attn_avg_ms,
+            "bytes_per_launch": sum(attn_bytes) / len(attn_bytes),
+        },
+        "compaction": comp,
+        "end_to_end_gbs": total_bytes / wall / 1e9,
+        "end_to_end_frac": total_bytes / wall / 1e9 / PEAK_HBM_GBS,
+    }
+    cache.close()
+    del q_ring, k_ring, v_ring
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        # start 32 steps before an eviction step so the sample contains one
+        c0 = T - 256 - 32
+        result["cpu_baseline"] = cpu_baseline(w, seed, c0, args.cpu_steps)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()
