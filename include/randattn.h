@@ -117,8 +117,8 @@ int64_t ra_region_rows(const ra_config* cfg, int32_t prompt_len);
  * pool_rows int32.  Negative ra_status on error. */
 int64_t ra_seq_rows(const ra_config* cfg, int32_t prompt_len);
 
-/* Bytes of the persistent device metadata buffer (per-slot state and
- * attention completion counters).  0 on a bad config. */
+/* Bytes of the persistent device metadata buffer (per-slot state).
+ * 0 on a bad config. */
 size_t ra_meta_bytes(const ra_config* cfg);
 
 /* Bytes of the attention workspace (split partial results) that

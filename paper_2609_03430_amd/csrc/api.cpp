@@ -54,7 +54,6 @@ struct ra_cache {
   int32_t* pos = nullptr;
   int64_t pool_rows = 0;
   SeqMeta* meta = nullptr;
-  int32_t* counters = nullptr;
   std::vector<SeqMeta> mirror;           // host copy of the device metadata
   std::map<int64_t, int64_t> free_rows;  // first-fit free list: base -> rows
   std::vector<uint8_t> appended;         // layers appended in the open step
@@ -181,8 +180,7 @@ int64_t ra_seq_rows(const ra_config* c, int32_t prompt_len) {
 size_t ra_meta_bytes(const ra_config* c) {
   if (ra_config_check(c) != RA_OK) return 0;
   const size_t metas = sizeof(SeqMeta) * static_cast<size_t>(c->max_seqs);
-  const size_t ctrs = sizeof(int32_t) * static_cast<size_t>(c->max_seqs) * c->num_kv_heads;
-  return round_up(static_cast<int64_t>(metas + ctrs), 256);
+  return round_up(static_cast<int64_t>(metas), 256);
 }
 
 size_t ra_workspace_bytes(const ra_config* c) {
@@ -217,7 +215,6 @@ ra_status ra_cache_create(const ra_config* cfg, void* k_pool, void* v_pool,
   c->pos = pos_pool;
   c->pool_rows = pool_rows;
   c->meta = static_cast<SeqMeta*>(meta);
-  c->counters = reinterpret_cast<int32_t*>(c->meta + cfg->max_seqs);
   c->mirror.assign(cfg->max_seqs, SeqMeta{});
   c->free_rows[0] = pool_rows;
   c->appended.assign(cfg->num_layers, 0);
@@ -358,7 +355,6 @@ ra_status ra_decode_attention(ra_cache* c, int32_t layer, const void* q,
   a.out = out;
   a.ws_o = ws;
   a.ws_ml = ws + items * G * ra::kHeadDim;
-  a.counters = c->counters;
   a.layer = layer;
   a.max_seqs = c->slot_hi;
   a.split_keys = sk;

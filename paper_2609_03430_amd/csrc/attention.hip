@@ -7,9 +7,8 @@
 // `split_keys` keys).  Each wavefront reads its keys and values exactly once
 // for all G query heads of the group, keeps an online softmax (running max
 // and sum, combined across lanes with wavefront shuffles), and writes an
-// unnormalised partial.  The last wavefront of a head to finish (a device
-// atomic counter) merges the partials and writes the output, then resets the
-// counter for the next launch.  The step's new key/value is read from the
+// unnormalised partial; a small second kernel merges the partials of each
+// head and writes the output.  The step's new key/value is read from the
 // input buffers by the wavefront that owns the last key, which also stores
 // it into the cache after its reads, so no wavefront of the launch reads a
 // row that is being written.
@@ -114,46 +113,66 @@ __device__ __forceinline__ void append_row(const Work& w, const SeqMeta* meta,
   if (lane == 0) pos[row] = meta[w.slot].prompt_len + meta[w.slot].step;
 }
 
-// Publish the partial and, in the last wavefront of the head, merge them.
-// Partial layout: ws_o[((head * kMaxSplits + split) * G + q) * 128 + c]
-// (numerator, scaled by 2^-m) and ws_ml[... * 2 + {0,1}] = (m, l) with m the
-// running max in log2 units and l the sum of 2^(s - m).
+// Merge the split partials of one (sequence, KV head) into the output.  One
+// workgroup per head, launched after the attention kernel (the kernel
+// boundary makes every partial visible; no device-scope fences are needed in
+// the streaming kernel).  Partial layout:
+//   ws_o[((head * kMaxSplits + split) * G + q) * 128 + c]  numerator / 2^m
+//   ws_ml[((head * kMaxSplits + split) * G + q) * 2 + {0,1}] = (m, l)
+// with m the running max of the scores in log2 units and l the sum of
+// 2^(s - m) over the split's keys.
 template <typename E>
-__device__ __forceinline__ void finish_head(const Work& w, const AttnLaunch& a,
-                                            int G, int Hq, int Hkv) {
-  const int lane = threadIdx.x;
-  const int head = w.slot * Hkv + w.g;
-  __threadfence();
-  int prev = 0;
-  if (lane == 0) prev = atomicAdd(&a.counters[head], 1);
-  prev = __shfl(prev, 0, 64);
-  if (prev != w.nsplit - 1) return;
-  __threadfence();
+__global__ __launch_bounds__(256) void combine_kernel(AttnLaunch a, int G, int Hq,
+                                                      int Hkv) {
+  __shared__ float sm[kMaxSplits * kMaxGroup];   // split maxima, then weights
+  __shared__ float sl[kMaxSplits * kMaxGroup];   // split sums
+  __shared__ float inv_l[kMaxGroup];
+  const int g = blockIdx.x, slot = blockIdx.y;
+  const SeqMeta& M = a.meta[slot];
+  if (!M.active) return;
+  const int t = threadIdx.x;
+  const int n_keys = M.len + 1;
+  const int nsplit = (n_keys + a.split_keys - 1) / a.split_keys;
+  const int head = slot * Hkv + g;
   const float* ml = a.ws_ml + static_cast<int64_t>(head) * kMaxSplits * G * 2;
   const float* po = a.ws_o + static_cast<int64_t>(head) * kMaxSplits * G * kHeadDim;
-  E* out = static_cast<E*>(a.out);
-  for (int q = 0; q < G; ++q) {
+  for (int i = t; i < nsplit * G; i += blockDim.x) {
+    sm[i] = ml[2 * i];
+    sl[i] = ml[2 * i + 1];
+  }
+  __syncthreads();
+  // per query: global max, split weights 2^(m_s - max) and the total sum
+  if (t < G) {
     float mx = kNegInf;
-    for (int s = 0; s < w.nsplit; ++s) mx = fmaxf(mx, ml[(s * G + q) * 2]);
-    float lsum = 0.f, o0 = 0.f, o1 = 0.f;
-    for (int s = 0; s < w.nsplit; ++s) {
-      const float sc = exp2f(ml[(s * G + q) * 2] - mx);
-      lsum += ml[(s * G + q) * 2 + 1] * sc;
-      const float* row = po + static_cast<int64_t>(s * G + q) * kHeadDim;
-      o0 += row[lane] * sc;
-      o1 += row[lane + 64] * sc;
+    for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, sm[s * G + t]);
+    float lsum = 0.f;
+    for (int s = 0; s < nsplit; ++s) {
+      const float w = exp2f(sm[s * G + t] - mx);
+      sm[s * G + t] = w;
+      lsum += w * sl[s * G + t];
     }
-    const float inv = 1.f / lsum;
-    const int64_t orow = (static_cast<int64_t>(w.slot) * Hq + w.g * G + q) * kHeadDim;
-    if constexpr (sizeof(E) == 2) {
-      out[orow + lane] = f32_to_bf16(o0 * inv);
-      out[orow + lane + 64] = f32_to_bf16(o1 * inv);
-    } else {
-      out[orow + lane] = o0 * inv;
-      out[orow + lane + 64] = o1 * inv;
+    inv_l[t] = 1.f / lsum;
+  }
+  __syncthreads();
+  E* out = static_cast<E*>(a.out);
+  // one thread per (query, 4 channels)
+  for (int item = t; item < G * (kHeadDim / 4); item += blockDim.x) {
+    const int q = item / (kHeadDim / 4), c4 = (item % (kHeadDim / 4)) * 4;
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+    for (int s = 0; s < nsplit; ++s) {
+      const f32x4 v = *reinterpret_cast<const f32x4*>(
+          po + static_cast<int64_t>(s * G + q) * kHeadDim + c4);
+      acc += v * sm[s * G + q];
+    }
+    acc *= inv_l[q];
+    const int64_t orow = (static_cast<int64_t>(slot) * Hq + g * G + q) * kHeadDim + c4;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if constexpr (sizeof(E) == 2) out[orow + j] = f32_to_bf16(acc[j]);
+      else out[orow + j] = acc[j];
     }
   }
-  if (lane == 0) a.counters[head] = 0;
 }
 
 // ---------------------------------------------------------------------------
@@ -168,7 +187,7 @@ struct BlockRegs {
 // Offsets (in elements) of this lane's operand loads within a 32-key block.
 struct LaneMap {
   int krow[2];   // key row within the block for S tile 0 / 1
-  int kcol;      // first channel of the lane's 64-byte key slice
+  int kcol;      // first channel of the lane's 16-byte chunk at k-step 0
   int vrow;      // first key row of the lane's value tile
   int vch;       // channel within each 16-channel tile
 };
@@ -178,7 +197,7 @@ __device__ __forceinline__ LaneMap lane_map() {
   LaneMap m;
   m.krow[0] = 8 * (r >> 2) + (r & 3);
   m.krow[1] = 8 * (r >> 2) + 4 + (r & 3);
-  m.kcol = 32 * grp;
+  m.kcol = 8 * grp;
   m.vrow = 8 * grp;
   m.vch = r;
   return m;
@@ -191,7 +210,7 @@ __device__ __forceinline__ void load_block(BlockRegs& b, const uint16_t* Kr,
   for (int t = 0; t < 2; ++t) {
     const uint16_t* row = Kr + static_cast<int64_t>(kb + lm.krow[t]) * kHeadDim + lm.kcol;
 #pragma unroll
-    for (int s = 0; s < 4; ++s) b.k[t][s] = ld16(row + 8 * s);
+    for (int s = 0; s < 4; ++s) b.k[t][s] = ld16(row + 32 * s);
   }
   const uint16_t* vt = Vr + static_cast<int64_t>(kb + lm.vrow) * kHeadDim + lm.vch * 8;
 #pragma unroll
@@ -251,7 +270,7 @@ __device__ __forceinline__ void compute_block(Softmax& st, const BlockRegs& b,
   }
 }
 
-__global__ __launch_bounds__(64) void attn_bf16_kernel(AttnLaunch a, int G,
+__global__ __launch_bounds__(64, 2) void attn_bf16_kernel(AttnLaunch a, int G,
                                                        int Hq, int Hkv,
                                                        float scale_log2) {
   const Work w = locate(a.meta, a.layer, Hkv, a.split_keys);
@@ -265,15 +284,17 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnLaunch a, int G,
   const uint16_t* vn = static_cast<const uint16_t*>(a.v_new) +
                        (static_cast<int64_t>(w.slot) * Hkv + w.g) * kHeadDim;
 
-  // Q^T operand: query qi of the group, channels 32*grp + 8*s + [0, 8)
+  // Q^T operand: query qi of the group, channels 32*s + 8*grp + [0, 8) at
+  // k-step s (the key operand uses the same channel order, so a row's four
+  // lane groups read 64 contiguous bytes per load)
   bf16x8 qop[4];
   {
     const uint16_t* qrow = static_cast<const uint16_t*>(a.q) +
-        (static_cast<int64_t>(w.slot) * Hq + w.g * G + qi) * kHeadDim + 32 * grp;
+        (static_cast<int64_t>(w.slot) * Hq + w.g * G + qi) * kHeadDim + 8 * grp;
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       const u32x4 z = {0u, 0u, 0u, 0u};
-      qop[s] = as_bf16x8(qi < G ? ld16(qrow + 8 * s) : z);
+      qop[s] = as_bf16x8(qi < G ? ld16(qrow + 32 * s) : z);
     }
   }
 
@@ -286,15 +307,22 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnLaunch a, int G,
   const bool owns_last = (w.k1 == w.n_keys);
   // full blocks: every key a cached row
   const int nfull = owns_last ? (w.len - w.k0) / 32 : (w.k1 - w.k0) / 32;
-  {
+  if (nfull > 0) {
+    // Two register buffers; every prefetch is unconditional (clamped to the
+    // last block, whose repeated loads hit in cache) so that no branch makes
+    // the wait before a block's compute also wait for the next block's loads.
+    // The loop body has no conditional code at all: the loads it issues are
+    // consumed by the next iteration, so the compiler cannot sink them.
+    const int last = nfull - 1;
     BlockRegs A, B;
+    load_block(A, Kr, Vr, w.k0, lm);
+    load_block(B, Kr, Vr, w.k0 + 32 * min(1, last), lm);
     int i = 0;
-    if (nfull > 0) load_block(A, Kr, Vr, w.k0, lm);
     for (; i + 1 < nfull; i += 2) {
-      load_block(B, Kr, Vr, w.k0 + 32 * (i + 1), lm);
       compute_block(st, A, qop, scale_log2, 32);
-      if (i + 2 < nfull) load_block(A, Kr, Vr, w.k0 + 32 * (i + 2), lm);
+      load_block(A, Kr, Vr, w.k0 + 32 * min(i + 2, last), lm);
       compute_block(st, B, qop, scale_log2, 32);
+      load_block(B, Kr, Vr, w.k0 + 32 * min(i + 3, last), lm);
     }
     if (i < nfull) compute_block(st, A, qop, scale_log2, 32);
   }
@@ -310,7 +338,7 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnLaunch a, int G,
       const uint16_t* row = key < w.len ? Kr + static_cast<int64_t>(key) * kHeadDim : kn;
 #pragma unroll
       for (int s = 0; s < 4; ++s)
-        b.k[t][s] = key <= w.len ? ld16(row + lm.kcol + 8 * s) : z;
+        b.k[t][s] = key <= w.len ? ld16(row + lm.kcol + 32 * s) : z;
     }
     const int key0 = kb + lm.vrow;         // first key of this lane's tile
 #pragma unroll
@@ -352,7 +380,6 @@ __global__ __launch_bounds__(64) void attn_bf16_kernel(AttnLaunch a, int G,
       a.ws_ml[(item * G + qi) * 2 + 1] = st.l;
     }
   }
-  finish_head<uint16_t>(w, a, G, Hq, Hkv);
 }
 
 // ---------------------------------------------------------------------------
@@ -461,7 +488,6 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G,
       }
     }
   }
-  finish_head<float>(w, a, G, Hq, Hkv);
 }
 
 }  // namespace
@@ -470,12 +496,17 @@ hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s)
   const dim3 grid(a.max_splits, sh.Hkv, a.max_seqs);
   // scores in log2 units: q.k / sqrt(d) * log2(e)
   const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(kHeadDim));
+  const dim3 cgrid(sh.Hkv, a.max_seqs);
   if (sh.dtype == 1) {
     hipLaunchKernelGGL(attn_bf16_kernel, grid, dim3(64), 0, s, a, sh.G, sh.Hq,
                        sh.Hkv, scale_log2);
+    hipLaunchKernelGGL(combine_kernel<uint16_t>, cgrid, dim3(256), 0, s, a, sh.G,
+                       sh.Hq, sh.Hkv);
   } else {
     hipLaunchKernelGGL(attn_f32_kernel, grid, dim3(64), 0, s, a, sh.G, sh.Hq,
                        sh.Hkv, scale_log2);
+    hipLaunchKernelGGL(combine_kernel<float>, cgrid, dim3(256), 0, s, a, sh.G,
+                       sh.Hq, sh.Hkv);
   }
   return hipGetLastError();
 }

@@ -82,7 +82,6 @@ struct AttnLaunch {
   void* out;
   float* ws_o;         // [heads][kMaxSplits][G][128] partial numerators
   float* ws_ml;        // [heads][kMaxSplits][G][2]  running max (log2), sum
-  int32_t* counters;   // [heads] completed work items of this launch
   int layer;
   int max_seqs;
   int split_keys;
