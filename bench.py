@@ -138,6 +138,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-steps", type=int, default=96)
     ap.add_argument("--attn-split", type=int, default=0)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a 1 GiB device-to-device copy three times (the "
+                         "known-size reference for the HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -148,6 +151,15 @@ def main():
     import torch
     from paper_2609_03430_amd import binding as B
     from paper_2609_03430_amd.synth import Workload
+
+    if args.calibrate_copy:
+        src = torch.ones(1 << 28, dtype=torch.float32, device="cuda:0")  # 1 GiB
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes": src.numel() * 4}))
+        return
 
     w = WORKLOADS[args.workload]
     L, Hq, Hkv, Bsz, lp, T, K = (w[k] for k in ("L", "Hq", "Hkv", "B", "lp", "T", "K"))
