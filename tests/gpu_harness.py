@@ -146,6 +146,17 @@ class OracleSeq:
         v = self.wl.v_rows(self.rid, layer, g, torch.as_tensor(P), self.lp)
         return k, v
 
+    def attend_group(self, layer, g, step0):
+        """Outputs [G, d] float64 of the query heads of KV head g."""
+        run = self.run
+        G = run.G
+        q = self.wl.q_rows(self.rid, layer, torch.arange(g * G, (g + 1) * G), step0)
+        k, v = self.rows(layer, g, self.rep.P[(layer, g)])
+        from oracle.attention import softmax_attention
+        qd = q.double().numpy()
+        kd, vd = k.double().numpy(), v.double().numpy()
+        return np.stack([softmax_attention(qd[i], kd, vd) for i in range(G)])
+
     def attend(self, layer, step0):
         """Outputs [Hq, d] float64 of `layer` at 0-based step ``step0``; the
         replay must hold the cache after that step's append."""

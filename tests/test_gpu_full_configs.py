@@ -1,0 +1,76 @@
+"""Parity at the full sizes of the measured workloads, in the launch
+configuration bench.py times (all sequences, all layers, the library's own
+split choice).
+
+Each case fast-forwards every sequence (positions only) to shortly before
+step 32768 of a 32k-token generation, materialises the kept rows from the
+seeded generator, then decodes the last steps, which include an eviction
+event.  Sampled (sequence, layer, KV head) sites are replayed by the oracle
+from the seeds alone: their kept positions must match bit-exactly after the
+event, and the sampled outputs of their query heads must be within 2e-2 of
+the fp64 oracle.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_harness import OracleSeq, Run, log, max_abs
+from paper_2609_03430_amd import binding as B
+
+pytestmark = pytest.mark.gpu
+
+# (layers, q heads, kv heads, batch, prompt, K, seed)
+SHAPES = {
+    "qwen3-4b": (36, 32, 8, 16, 512, 8192, 1001),
+    "qwen3-14b": (40, 40, 8, 32, 1024, 8192, 1002),
+    "qwen3-32b": (64, 64, 8, 16, 4096, 4096, 1003),
+}
+T = 32768
+WINDOW = 72          # steps decoded on the GPU (events at 32704 and 32768)
+
+
+@pytest.mark.parametrize("name", sorted(SHAPES))
+def test_full_size(name):
+    L, Hq, Hkv, Bsz, lp, K, seed = SHAPES[name]
+    log("full size %s: L=%d Hq=%d Hkv=%d B=%d lp=%d K=%d" % (name, L, Hq, Hkv, Bsz, lp, K))
+    run = Run(L=L, Hq=Hq, Hkv=Hkv, K=K, lps=[lp] * Bsz, r=64, every=64,
+              seeds=[seed * 1000003 + b for b in range(Bsz)], rids=list(range(Bsz)),
+              wl_seed=seed, ring=64, write_prompt=False)
+    t0 = T - WINDOW
+    run.fast_forward(t0)
+    for b in range(Bsz):
+        run.materialise(b)
+    log("  state at step %d materialised" % t0)
+    sites = [(0, 0, 0), (Bsz - 1, L - 1, Hkv - 1), (Bsz // 2, L // 2, 1)]
+    heads = {}
+    for b, l, g in sites:
+        heads.setdefault(b, []).append((l, g))
+    oracles = {b: OracleSeq(run, b, heads=h) for b, h in heads.items()}
+    for o in oracles.values():
+        o.advance(t0)
+    log("  oracle replay done")
+    check_steps = {0, 31, 32, 33, WINDOW - 1}
+    worst = 0.0
+    for i in range(WINDOW):
+        outs, ev = run.step()
+        for o in oracles.values():
+            o.rep.append()
+        if i in check_steps:
+            for b, l, g in sites:
+                o = oracles[b]
+                want = o.attend_group(l, g, t0 + i)
+                got = outs[l, b, g * run.G:(g + 1) * run.G].float().cpu()
+                err = max_abs(got, want)
+                worst = max(worst, err)
+                assert err <= 2e-2, (name, i, b, l, g, err)
+        for o in oracles.values():
+            o.rep.end_step()
+    for b, l, g in sites:
+        got = run.positions(b, l, g)
+        want = oracles[b].rep.P[(l, g)]
+        assert np.array_equal(got, want), (name, b, l, g)
+    assert oracles[0].rep.event >= 2
+    log("  %s ok: worst %.3g, events %d" % (name, worst, oracles[0].rep.event))
+    run.close()
+    torch.cuda.empty_cache()
