@@ -18,7 +18,8 @@
 //                               the group's G queries on the N side (padded
 //                               to 16 with zeros);
 //   O^T[ch][query] += V^T . P^T A = 16 channels x 32 keys from the
-//                               transposed value tiles, B = P^T.
+//                               transposed value tiles, B = P^T split into
+//                               two bf16 parts (hi + lo) for precision.
 // A lane's 8 operand elements come from one 16-byte global load: key rows
 // are row-major and value rows are stored as transposed 8-row tiles.  The
 // key rows are assigned to the two 16-row S tiles so that each lane's
@@ -253,20 +254,25 @@ __device__ __forceinline__ void compute_block(Softmax& st, const BlockRegs& b,
   bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
   const float mn = fmaxf(st.m, bm);
   const float alpha = exp2f(st.m - mn);
-  bf16x8 p;
+  // P = hi + lo, both bf16, so the weights keep ~16 significant bits through
+  // the bf16 MFMA (the remainder of a bf16 rounding is exact in fp32)
+  bf16x8 p_hi, p_lo;
   float psum = 0.f;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    const __bf16 pb = static_cast<__bf16>(exp2f(x[e] - mn));
-    p[e] = pb;
-    psum += static_cast<float>(pb);
+    const float pf = exp2f(x[e] - mn);
+    const __bf16 hi = static_cast<__bf16>(pf);
+    p_hi[e] = hi;
+    p_lo[e] = static_cast<__bf16>(pf - static_cast<float>(hi));
+    psum += pf;
   }
   st.l = st.l * alpha + psum;
   st.m = mn;
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
     st.acc[u] *= alpha;
-    st.acc[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(b.v[u]), p, st.acc[u], 0, 0, 0);
+    st.acc[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(b.v[u]), p_hi, st.acc[u], 0, 0, 0);
+    st.acc[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(b.v[u]), p_lo, st.acc[u], 0, 0, 0);
   }
 }
 
