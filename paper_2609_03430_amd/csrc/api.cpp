@@ -111,8 +111,9 @@ void attention_plan(const ra_cache* c, int* split_keys, int* max_splits) {
   if (c->cfg.attn_split > 0) {
     sk = c->cfg.attn_split;
   } else {
-    // about 2048 wavefronts per launch (8 per CU on 256 CUs)
-    const int target = 2048;
+    // about 1024 wavefronts per launch: one per SIMD on 256 CUs (measured
+    // best on the 40-layer, 256-head workload against 512..4096)
+    const int target = 1024;
     const int splits = std::min(ra::kMaxSplits, std::max(1, (target + heads - 1) / heads));
     sk = static_cast<int>(round_up((cap_max + splits - 1) / splits, 32));
   }

@@ -276,7 +276,8 @@ __device__ __forceinline__ void compute_block(Softmax& st, const BlockRegs& b,
   }
 }
 
-__global__ __launch_bounds__(64, 2) void attn_bf16_kernel(AttnLaunch a, int G,
+template <int NBUF>
+__global__ __launch_bounds__(64, NBUF <= 2 ? 2 : 1) void attn_bf16_kernel(AttnLaunch a, int G,
                                                        int Hq, int Hkv,
                                                        float scale_log2) {
   const Work w = locate(a.meta, a.layer, Hkv, a.split_keys);
@@ -314,23 +315,26 @@ __global__ __launch_bounds__(64, 2) void attn_bf16_kernel(AttnLaunch a, int G,
   // full blocks: every key a cached row
   const int nfull = owns_last ? (w.len - w.k0) / 32 : (w.k1 - w.k0) / 32;
   if (nfull > 0) {
-    // Two register buffers; every prefetch is unconditional (clamped to the
-    // last block, whose repeated loads hit in cache) so that no branch makes
-    // the wait before a block's compute also wait for the next block's loads.
-    // The loop body has no conditional code at all: the loads it issues are
-    // consumed by the next iteration, so the compiler cannot sink them.
+    // NBUF register buffers in rotation; every prefetch is unconditional
+    // (clamped to the last block, whose repeated loads hit in cache) and the
+    // loop body has no conditional code, so the loads it issues are consumed
+    // by the next iteration and the compiler can neither sink them nor make
+    // the wait before a block's compute also wait for later blocks' loads.
     const int last = nfull - 1;
-    BlockRegs A, B;
-    load_block(A, Kr, Vr, w.k0, lm);
-    load_block(B, Kr, Vr, w.k0 + 32 * min(1, last), lm);
+    BlockRegs buf[NBUF];
+#pragma unroll
+    for (int j = 0; j < NBUF; ++j) load_block(buf[j], Kr, Vr, w.k0 + 32 * min(j, last), lm);
     int i = 0;
-    for (; i + 1 < nfull; i += 2) {
-      compute_block(st, A, qop, scale_log2, 32);
-      load_block(A, Kr, Vr, w.k0 + 32 * min(i + 2, last), lm);
-      compute_block(st, B, qop, scale_log2, 32);
-      load_block(B, Kr, Vr, w.k0 + 32 * min(i + 3, last), lm);
+    for (; i + NBUF - 1 < nfull; i += NBUF) {
+#pragma unroll
+      for (int j = 0; j < NBUF; ++j) {
+        compute_block(st, buf[j], qop, scale_log2, 32);
+        load_block(buf[j], Kr, Vr, w.k0 + 32 * min(i + NBUF + j, last), lm);
+      }
     }
-    if (i < nfull) compute_block(st, A, qop, scale_log2, 32);
+#pragma unroll
+    for (int j = 0; j < NBUF - 1; ++j)
+      if (i + j < nfull) compute_block(st, buf[j], qop, scale_log2, 32);
   }
   if (owns_last) {
     // tail block: cached rows below len, the new pair at len, masked above
@@ -504,7 +508,9 @@ hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s)
   const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(kHeadDim));
   const dim3 cgrid(sh.Hkv, a.max_seqs);
   if (sh.dtype == 1) {
-    hipLaunchKernelGGL(attn_bf16_kernel, grid, dim3(64), 0, s, a, sh.G, sh.Hq,
+    // two register buffers: measured best; deeper pipelines (3, 4 buffers at
+    // one wavefront per SIMD) were not faster
+    hipLaunchKernelGGL(attn_bf16_kernel<2>, grid, dim3(64), 0, s, a, sh.G, sh.Hq,
                        sh.Hkv, scale_log2);
     hipLaunchKernelGGL(combine_kernel<uint16_t>, cgrid, dim3(256), 0, s, a, sh.G,
                        sh.Hq, sh.Hkv);
