@@ -26,7 +26,7 @@ class Run:
     def __init__(self, L, Hq, Hkv, K, lps, r=64, every=64, dtype=B.RA_BF16,
                  mode=B.RA_BUDGET_EVICTABLE, seeds=None, rids=None,
                  scaled=True, wl_seed=1000, ring=None, attn_split=0,
-                 max_seqs=None, write_prompt=True):
+                 max_seqs=None, write_prompt=True, begin=True):
         self.L, self.Hq, self.Hkv, self.K, self.r, self.every = L, Hq, Hkv, K, r, every
         self.G = Hq // Hkv
         self.lps = list(lps)
@@ -46,11 +46,19 @@ class Run:
                            device=DEV)
         self.slots = list(range(n))
         self.steps = [0] * n
-        for slot, lp in enumerate(self.lps):
-            kp = vp = None
-            if write_prompt and lp > 0:
-                kp, vp = self.prompt_rows(slot, lp)
-            B.ra_seq_begin(self.h, slot, lp, self.seeds[slot], self.rids[slot], kp, vp)
+        self.write_prompt = write_prompt
+        if begin:
+            for slot in range(n):
+                self.begin(slot)
+
+    def begin(self, slot):
+        lp = self.lps[slot]
+        kp = vp = None
+        if self.write_prompt and lp > 0:
+            kp, vp = self.prompt_rows(slot, lp)
+        B.ra_seq_begin(self.h, slot, lp, self.seeds[slot], self.rids[slot], kp, vp)
+        self.steps[slot] = 0
+        self.active = getattr(self, "active", set()) | {slot}
 
     def k_keep(self, slot):
         return keep_count(self.K, self.lps[slot], self.mode)
@@ -89,25 +97,30 @@ class Run:
         return outs, evicted
 
     def fast_forward(self, n):
+        """Positions-only advance of every begun sequence."""
         B.ra_fast_forward(self.h, n)
-        self.steps = [s + n for s in self.steps]
+        self.steps = [s + n if slot in self.active else s
+                      for slot, s in enumerate(self.steps)]
 
     def materialise(self, slot):
         """Write the rows of the currently cached positions (after a fast
-        forward) from the workload generator."""
+        forward) from the workload generator, one layer at a time."""
         info = B.ra_get_seq_info(self.h, slot)
         n = info.len
         pos = torch.empty(self.L * self.Hkv * n, dtype=torch.int32, device=DEV)
         B.ra_export_positions(self.h, slot, pos)
         pos = pos.view(self.L, self.Hkv, n).long()
-        l = torch.arange(self.L, device=DEV).view(-1, 1, 1)
-        g = torch.arange(self.Hkv, device=DEV).view(1, -1, 1)
+        g = torch.arange(self.Hkv, device=DEV).view(-1, 1)
         rid = self.rids[slot]
         lp = self.lps[slot]
-        k = self.wl.k_rows(rid, l, g, pos, lp).contiguous()
-        v = self.wl.v_rows(rid, l, g, pos, lp).contiguous()
+        k = torch.empty(self.L, self.Hkv, n, 128, dtype=self.tdtype, device=DEV)
+        v = torch.empty_like(k)
+        for l in range(self.L):
+            k[l] = self.wl.k_rows(rid, l, g, pos[l], lp)
+            v[l] = self.wl.v_rows(rid, l, g, pos[l], lp)
         B.ra_write_rows(self.h, slot, k, v)
         torch.cuda.synchronize()
+        del k, v, pos
 
     def positions(self, slot, layer, g):
         info = B.ra_get_seq_info(self.h, slot)

@@ -74,3 +74,64 @@ def test_full_size(name):
     log("  %s ok: worst %.3g, events %d" % (name, worst, oracles[0].rep.event))
     run.close()
     torch.cuda.empty_cache()
+
+
+def test_full_size_phi4_ragged():
+    """Phi-4-reasoning-shaped ragged batch: 40 layers, 40 Q / 10 KV heads,
+    128 sequences with prompts ~U[64, 2048] and generated lengths
+    ~U[4096, 32768] (seeded), K=8192, r=64.  Sequences are begun longest
+    first and fast-forwarded between begins, so each reaches its own step
+    count through the real sampler; the decoded window then evicts every
+    sequence on its own phase."""
+    L, Hq, Hkv, Bsz, K, seed = 40, 40, 10, 128, 8192, 1004
+    rng = np.random.default_rng(seed)
+    lps = rng.integers(64, 2049, Bsz).tolist()
+    gens = sorted(rng.integers(4096, 32769, Bsz).tolist(), reverse=True)
+    log("phi4 ragged: prompts %d..%d, generated %d..%d" % (min(lps), max(lps), gens[-1], gens[0]))
+    run = Run(L=L, Hq=Hq, Hkv=Hkv, K=K, lps=lps, r=64, every=64,
+              seeds=[seed * 1000003 + b for b in range(Bsz)], rids=list(range(Bsz)),
+              wl_seed=seed, ring=64, write_prompt=False, begin=False)
+    for b in range(Bsz):
+        run.begin(b)
+        nxt = gens[b + 1] if b + 1 < Bsz else 0
+        if gens[b] - nxt > 0:
+            run.fast_forward(gens[b] - nxt)
+    assert run.steps == gens
+    for b in range(Bsz):
+        run.materialise(b)
+    log("  snapshot materialised")
+    sites = [(0, 0, 0), (Bsz - 1, L - 1, Hkv - 1), (Bsz // 2, 7, 5), (31, L - 1, 0)]
+    heads = {}
+    for b, l, g in sites:
+        heads.setdefault(b, []).append((l, g))
+    oracles = {b: OracleSeq(run, b, heads=h) for b, h in heads.items()}
+    for b, o in oracles.items():
+        o.advance(gens[b])
+    log("  oracle replay done")
+    window = 72
+    check_steps = {0, 40, window - 1}
+    events = 0
+    for i in range(window):
+        outs, ev = run.step()
+        events += ev
+        for o in oracles.values():
+            o.rep.append()
+        if i in check_steps:
+            for b, l, g in sites:
+                want = oracles[b].attend_group(l, g, gens[b] + i)
+                got = outs[l, b, g * run.G:(g + 1) * run.G].float().cpu()
+                err = max_abs(got, want)
+                assert err <= 2e-2, ("phi4", i, b, l, g, err)
+        for o in oracles.values():
+            o.rep.end_step()
+    for b, l, g in sites:
+        assert np.array_equal(run.positions(b, l, g), oracles[b].rep.P[(l, g)]), (b, l, g)
+    # a sequence is evicted at step t iff t is a multiple of 64 and its
+    # evictable rows (t - r during growth, k_keep + 64 in steady state)
+    # exceed k_keep, i.e. t > k_keep + r
+    expected = sum(1 for g0 in gens for t in range(g0 + 1, g0 + window + 1)
+                   if t % 64 == 0 and t > K + 64)
+    assert events == expected, (events, expected)
+    log("  phi4 ok: %d sequence-events in the window" % events)
+    run.close()
+    torch.cuda.empty_cache()
