@@ -10,11 +10,13 @@ and MLPs are not part of the path and are not run.
 Default workload: the Qwen3-14B-shaped headline case (40 layers, 40 query /
 8 KV heads, head_dim 128, bf16, batch 32, prompt 1024, K=8192, r=64,
 eviction every 64 steps) in its steady state at the end of a 32k-token
-generation: the state at step T - warmup - steps is reached with the
+generation: the state at step 32768 - warmup - steps is reached with the
 positions-only fast forward (the same sampler and trigger), the kept rows
 are materialised from the seeded generator, then `warmup` untimed and
 `steps` timed decode steps run up to step 32768.  Inputs (a 64-step ring of
 q, k_new, v_new for every layer) are resident in HBM before timing.
+--workload selects the other shapes (Qwen3-4B, Qwen3-32B, and the ragged
+Phi-4 batch whose sequences start from their own generated lengths).
 
 Prints one JSON line.  `value` is tokens/s = batch * steps / wall time.
 """
@@ -46,7 +48,24 @@ WORKLOADS = {
                       desc="Qwen3-32B-shaped attention stack: 64 layers, 64 Q / 8 KV "
                            "heads, head_dim 128, bf16, batch 16, prompt 4096, 32768 "
                            "generated tokens, K=4096, r=64, evict every 64 steps"),
+    "phi4-ragged": dict(L=40, Hq=40, Hkv=10, B=128, lp=None, T=None, K=8192,
+                        desc="Phi-4-reasoning-shaped ragged batch: 40 layers, 40 Q / 10 KV "
+                             "heads, head_dim 128, bf16, 128 sequences, prompts ~U[64,2048], "
+                             "generated lengths ~U[4096,32768] at the window start, K=8192, "
+                             "r=64, evict every 64 steps (each sequence on its own phase)"),
 }
+SEEDS = {"qwen3-4b": 1001, "qwen3-14b": 1002, "qwen3-32b": 1003, "phi4-ragged": 1004}
+
+
+def sequence_plan(name, w, total):
+    """Per-sequence (prompt length, step at the start of the warm-up)."""
+    import numpy as np
+    if name == "phi4-ragged":
+        rng = np.random.default_rng(SEEDS[name])
+        lps = rng.integers(64, 2049, w["B"]).tolist()
+        gens = sorted(rng.integers(4096, 32769, w["B"]).tolist(), reverse=True)
+        return lps, gens
+    return [w["lp"]] * w["B"], [w["T"] - total] * w["B"]
 R = 64
 EVERY = 64
 RING = 64
@@ -73,7 +92,7 @@ def read_traffic(workload):
     return d.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(w, seed, t0, steps):
+def cpu_baseline(w, seed, lp, t0, steps):
     """The CPU oracle, untuned, on one sequence x one layer x all KV heads for
     `steps` steady-state decode steps (one eviction event included)."""
     import numpy as np
@@ -87,7 +106,7 @@ def cpu_baseline(w, seed, t0, steps):
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
         threads = 1
-    L, Hq, Hkv, lp, K = w["L"], w["Hq"], w["Hkv"], w["lp"], w["K"]
+    L, Hq, Hkv, K = w["L"], w["Hq"], w["Hkv"], w["K"]
     wl = Workload(seed, L, Hq, Hkv, 128, torch.bfloat16, True, ring=RING)
     layer, rid = 0, 0
     heads = [(layer, g) for g in range(Hkv)]
@@ -162,8 +181,8 @@ def main():
         return
 
     w = WORKLOADS[args.workload]
-    L, Hq, Hkv, Bsz, lp, T, K = (w[k] for k in ("L", "Hq", "Hkv", "B", "lp", "T", "K"))
-    seed = 1000 + {"qwen3-4b": 1, "qwen3-14b": 2, "qwen3-32b": 3}[args.workload]
+    L, Hq, Hkv, Bsz, K = (w[k] for k in ("L", "Hq", "Hkv", "B", "K"))
+    seed = SEEDS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
@@ -172,44 +191,55 @@ def main():
         print("[bench] " + msg, file=sys.stderr, flush=True)
 
     total = args.warmup + args.steps
-    t0 = T - total
-    assert t0 >= 0
+    lps, starts = sequence_plan(args.workload, w, total)
+    assert min(starts) >= 0
     cfg = B.make_config(L, Hq, Hkv, K, R, EVERY, B.RA_BUDGET_EVICTABLE, B.RA_BF16, Bsz,
                         attn_split=args.attn_split)
-    rows = B.ra_seq_rows(cfg, lp) * Bsz
-    log("workload %s: pools %.1f GB" % (args.workload, rows * 128 * 2 * 2 / 1e9))
+    rows = sum(B.ra_seq_rows(cfg, lp) for lp in lps)
+    log("workload %s: pools %.1f GB" % (args.workload, rows * (128 * 2 * 2 + 4) / 1e9))
     cache = B.Cache(cfg, rows, device=dev)
     h = cache.handle
     wl = Workload(seed, L, Hq, Hkv, 128, torch.bfloat16, True, ring=RING, device=dev)
-    for b in range(Bsz):
-        B.ra_seq_begin(h, b, lp, seed * 1000003 + b, b)
     t_ff = time.time()
-    B.ra_fast_forward(h, t0)
+    # begin the longest generations first and fast-forward between begins, so
+    # that every sequence reaches its own step through the real sampler
+    order = sorted(range(Bsz), key=lambda b: -starts[b])
+    for i, b in enumerate(order):
+        B.ra_seq_begin(h, b, lps[b], seed * 1000003 + b, b)
+        nxt = starts[order[i + 1]] if i + 1 < Bsz else 0
+        if starts[b] > nxt:
+            B.ra_fast_forward(h, starts[b] - nxt)
     torch.cuda.synchronize()
-    log("fast forward to step %d: %.2fs" % (t0, time.time() - t_ff))
-    ls = torch.arange(L, device=dev).view(-1, 1, 1)
-    gs = torch.arange(Hkv, device=dev).view(1, -1, 1)
+    log("fast forward to steps %d..%d: %.2fs" % (min(starts), max(starts), time.time() - t_ff))
+    gs = torch.arange(Hkv, device=dev).view(-1, 1)
     for b in range(Bsz):
         n = B.ra_get_seq_info(h, b).len
         pos = torch.empty(L * Hkv * n, dtype=torch.int32, device=dev)
         B.ra_export_positions(h, b, pos)
         pos = pos.view(L, Hkv, n).long()
-        B.ra_write_rows(h, b, wl.k_rows(b, ls, gs, pos, lp).contiguous(),
-                        wl.v_rows(b, ls, gs, pos, lp).contiguous())
-        del pos
+        kr = torch.empty(L, Hkv, n, 128, dtype=torch.bfloat16, device=dev)
+        vr = torch.empty_like(kr)
+        for l in range(L):
+            kr[l] = wl.k_rows(b, l, gs, pos[l], lps[b])
+            vr[l] = wl.v_rows(b, l, gs, pos[l], lps[b])
+        B.ra_write_rows(h, b, kr, vr)
+        del pos, kr, vr
     torch.cuda.synchronize()
     log("rows materialised: %.2fs" % (time.time() - t_ff))
 
-    # 64-step input ring for every layer, resident before timing
+    # 64-step input ring for every layer, resident before timing: slot j holds
+    # each sequence's inputs of its step starts[b] + j; iteration i of the
+    # run uses slot i mod 64 (the generator's rows repeat with period 64)
     bidx = torch.arange(Bsz, device=dev)
+    lp_t = torch.tensor(lps, device=dev)
+    st_t = torch.tensor(starts, device=dev)
     q_ring = torch.empty(RING, L, Bsz, Hq, 128, dtype=torch.bfloat16, device=dev)
     k_ring = torch.empty(RING, L, Bsz, Hkv, 128, dtype=torch.bfloat16, device=dev)
     v_ring = torch.empty_like(k_ring)
     for j in range(RING):
         for l in range(L):
-            q_ring[j, l] = wl.q_step(bidx, l, torch.full((Bsz,), j, device=dev))
-            k, v = wl.kv_step(bidx, l, torch.full((Bsz,), lp + j, device=dev),
-                              torch.full((Bsz,), lp, device=dev))
+            q_ring[j, l] = wl.q_step(bidx, l, st_t + j)
+            k, v = wl.kv_step(bidx, l, lp_t + st_t + j, lp_t)
             k_ring[j, l] = k
             v_ring[j, l] = v
     out = torch.empty(Bsz, Hq, 128, dtype=torch.bfloat16, device=dev)
@@ -219,9 +249,8 @@ def main():
 
     def run_steps(first, n, timed):
         rec = []
-        for i in range(n):
-            s = first + i
-            j = s % RING
+        for i in range(first, first + n):
+            j = i % RING
             lens = [B.ra_get_seq_info(h, b).len for b in range(Bsz)] if timed else None
             evs = []
             for l in range(L):
@@ -244,20 +273,26 @@ def main():
                 rec.append((lens, evs, (x0, x1), nev))
         return rec
 
-    run_steps(t0, args.warmup, False)
+    run_steps(0, args.warmup, False)
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    rec = run_steps(t0 + args.warmup, args.steps, True)
+    rec = run_steps(args.warmup, args.steps, True)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     tokens = Bsz * args.steps
-    assert B.ra_get_seq_info(h, 0).step == T
+    for b in range(Bsz):
+        assert B.ra_get_seq_info(h, b).step == starts[b] + total
 
     # per-launch durations and algorithmic bytes
     s_el = 2
     attn_ms, attn_bytes = [], []
     ev_ms, ev_bytes = [], []
     n_events = 0
+    seq_events = 0
+    C = K + EVERY                      # candidates at every event of these workloads
+    m = EVERY
+    moved = K + R - (C - m) / (m + 1)  # rows from the expected first drop to the end
+    per_head = moved * (2 * 128 * s_el + 4) * 2 + C * 4
     for lens, evs, (x0, x1), nev in rec:
         per_launch = sum(Hkv * ((n + 1) * 2 * 128 * s_el + (2 * 128 * s_el + 4)) +
                          2 * Hq * 128 * s_el for n in lens)
@@ -266,10 +301,7 @@ def main():
             attn_bytes.append(per_launch)
         if nev:
             n_events += 1
-            C = K + EVERY
-            m = EVERY
-            moved = (lp + K + R) - (lp + (C - m) / (m + 1))
-            per_head = moved * (2 * 128 * s_el + 4) * 2 + C * 4
+            seq_events += nev
             ev_ms.append(x0.elapsed_time(x1))
             ev_bytes.append(per_head * nev * L * Hkv)
     attn_avg_ms = sum(attn_ms) / len(attn_ms)
@@ -277,16 +309,25 @@ def main():
     comp = None
     if ev_ms:
         comp = {
-            "events_timed": n_events,
-            "avg_ms_per_event": sum(ev_ms) / len(ev_ms),
+            "end_steps_with_events": n_events,
+            "sequence_events": seq_events,
+            "avg_ms_per_end_step_with_events": sum(ev_ms) / len(ev_ms),
             "achieved_gbs": sum(ev_bytes) / (sum(ev_ms) * 1e-3) / 1e9,
             "peak_gbs": PEAK_HBM_GBS,
             "frac": sum(ev_bytes) / (sum(ev_ms) * 1e-3) / 1e9 / PEAK_HBM_GBS,
-            "bytes_note": "expected rows moved by the order-preserving shift "
-                          "(prompt + first drop onward) x (key + value + position) x 2, "
-                          "plus candidate positions read",
+            "bytes_note": "per (sequence, layer, KV head) event: expected rows moved by "
+                          "the order-preserving shift (from the first drop to the end) x "
+                          "(key + value + position) x 2, plus candidate positions read",
         }
     total_bytes = sum(attn_bytes) + sum(ev_bytes)
+    if len(set(starts)) == 1:
+        window = ("decode steps %d..%d of %d (%d end-of-step eviction events)"
+                  % (starts[0] + args.warmup + 1, starts[0] + total, starts[0] + total,
+                     n_events))
+    else:
+        window = ("%d timed decode steps per sequence, sequence i from step "
+                  "start_i + %d (start_i %d..%d), %d sequence eviction events"
+                  % (args.steps, args.warmup + 1, min(starts), max(starts), seq_events))
     result = {
         "metric": METRIC,
         "value": tokens / wall,
@@ -302,10 +343,9 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": w["desc"],
-            "timed_window": "decode steps %d..%d of %d (steady state, %d eviction events)"
-                            % (t0 + args.warmup + 1, T, T, n_events),
+            "timed_window": window,
             "global_batch": Bsz,
-            "seq_len": lp + T,
+            "seq_len": max(lp + st + total for lp, st in zip(lps, starts)),
             "attn_split_keys": split_keys,
         },
         "roofline": {
@@ -325,11 +365,13 @@ def main():
     }
     cache.close()
     del q_ring, k_ring, v_ring
+    torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
-        # start 32 steps before an eviction step so the sample contains one
-        c0 = T - 256 - 32
-        result["cpu_baseline"] = cpu_baseline(w, seed, c0, args.cpu_steps)
+        # sequence 0, a 96-step sample ending 192 steps before its last step
+        # (96 > 64, so the sample contains an eviction event)
+        c0 = starts[0] + total - 288
+        result["cpu_baseline"] = cpu_baseline(w, seed, lps[0], c0, args.cpu_steps)
     print(json.dumps(result), flush=True)
 
 
