@@ -213,6 +213,55 @@ def evict_cost(B, torch, Workload):
     return res
 
 
+def time_window_scorer(B, torch, h, wl, cfg, Bsz, L, Hq, Hkv, stream, comp, log):
+    """One round of the observation-window scoring pass over every sequence
+    (what a score-based evictor computes before it can evict, and Random
+    Attention does not), timed with HIP events on the current state."""
+    dev = torch.device("cuda:0")
+    infos = [B.ra_get_seq_info(h, b) for b in range(Bsz)]
+    qwin = torch.empty(Bsz, L, Hq, 64, 128, dtype=torch.bfloat16, device=dev)
+    heads = torch.arange(Hq, device=dev).view(-1, 1)
+    for b in range(Bsz):
+        steps = torch.arange(infos[b].step - 64, infos[b].step, device=dev).view(1, -1)
+        for l in range(L):
+            qwin[b, l] = wl.q_rows(b, l, heads, steps)
+    drops = torch.empty(Bsz, L, Hkv, cfg.evict_every, dtype=torch.int32, device=dev)
+    B.ra_window_select(h, 0, Bsz, qwin, None, 0, drops, stream)     # warm-up
+    times = []
+    for _ in range(3):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        B.ra_window_select(h, 0, Bsz, qwin, None, 0, drops, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    ms = min(times)
+    G = Hq // Hkv
+    keys = sum(i.len for i in infos) * L * Hkv
+    flops = 2 * 2 * keys * G * 64 * 128          # two logit passes, 2 flop per MAC
+    kbytes = 2 * keys * 128 * 2                   # every cached key read in both passes
+    rand_ms = None
+    if comp and comp.get("sequence_events"):
+        rand_ms = (comp["avg_ms_per_end_step_with_events"] * comp["end_steps_with_events"]
+                   / comp["sequence_events"])
+    log("window scorer: %.2f ms per round over %d sequences" % (ms, Bsz))
+    out = {
+        "what": "observation-window (last 64 queries x G heads) attention-score pass, "
+                "max-pool 7 and lowest-m selection, every (sequence, layer, KV head)",
+        "ms_per_round_all_sequences": ms,
+        "ms_per_sequence": ms / Bsz,
+        "tflops": flops / (ms * 1e-3) / 1e12,
+        "key_read_gbs": kbytes / (ms * 1e-3) / 1e9,
+        "random_eviction_ms_per_sequence_event": rand_ms,
+    }
+    if rand_ms:
+        out["scorer_over_random_eviction"] = (ms / Bsz) / rand_ms
+    del qwin, drops
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -226,6 +275,9 @@ def main():
                     help="eviction-round cost of one sequence at K=1024 (budget counting "
                          "the prompt, prompt 300) over 4096 decode steps, as in the "
                          "paper's eviction-cost table; prints its own JSON line")
+    ap.add_argument("--window-scorer", action="store_true",
+                    help="also time the observation-window scoring pass (always on for "
+                         "phi4-ragged)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device-to-device copy three times (the "
                          "known-size reference for the HBM byte counters)")
@@ -436,8 +488,13 @@ def main():
         "end_to_end_gbs": total_bytes / wall / 1e9,
         "end_to_end_frac": total_bytes / wall / 1e9 / PEAK_HBM_GBS,
     }
+    if args.workload == "phi4-ragged" or args.window_scorer:
+        del q_ring, k_ring, v_ring
+        torch.cuda.empty_cache()
+        result["window_scorer"] = time_window_scorer(B, torch, h, wl, cfg, Bsz, L, Hq,
+                                                     Hkv, stream, comp, log)
     cache.close()
-    del q_ring, k_ring, v_ring
+    q_ring = k_ring = v_ring = None
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")

@@ -223,6 +223,31 @@ ra_status ra_read_positions(ra_cache* cache, int32_t seq, int32_t layer,
                             int32_t kv_head, int32_t* host_out,
                             int32_t host_cap, int32_t* n_out, void* stream);
 
+/* ---- measurement only --------------------------------------------------------- */
+
+/* NOT PART OF RANDOM ATTENTION.  The scoring pass of a score-based evictor,
+ * provided to measure the cost that Random Attention removes: Section 2
+ * ("Baselines as choices of s") defines SnapKV's score of a cached position
+ * as the sum of the attention weights of the last w queries, max-pooled over
+ * neighbouring positions, and Eq. 1 keeps the top-scoring candidates.  For
+ * every (layer, KV head) of the active slots in [seq_lo, seq_hi):
+ *   score[j] = sum over the G*64 window queries of softmax(q.k/sqrt(d)) at
+ *              cached row j (a query sees the rows at or before its
+ *              position), then max-pooled over 7 rows;
+ *   drops    = the m lowest candidates (cached rows before the r most
+ *              recent; ties by row), m = the number Random Attention would
+ *              drop at this state.
+ * dev_q_window: [max_seqs][L][Hq][64][d] bf16, the queries of each
+ * sequence's last 64 decode steps, oldest first.  dev_scores (optional):
+ * [seq_hi-seq_lo][L][Hkv][scores_stride] float, the un-pooled scores of rows
+ * [0, len).  dev_drops (optional): [seq_hi-seq_lo][L][Hkv][evict_every]
+ * int32, the dropped rows ascending.  The cache is not modified.  bf16 only
+ * (RA_ERR_UNSUPPORTED otherwise); RA_ERR_STATE if a slot has fewer than 64
+ * steps or more than evict_every rows to drop. */
+ra_status ra_window_select(ra_cache* cache, int32_t seq_lo, int32_t seq_hi,
+                           const void* dev_q_window, float* dev_scores,
+                           int32_t scores_stride, int32_t* dev_drops, void* stream);
+
 /* ---- diagnostics ----------------------------------------------------------- */
 
 const char* ra_status_string(int32_t status);

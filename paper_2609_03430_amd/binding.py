@@ -37,7 +37,7 @@ EXPORTS = (
     "ra_seq_begin", "ra_seq_end", "ra_get_seq_info", "ra_decode_attention",
     "ra_end_step", "ra_evict_now", "ra_fast_forward", "ra_export_positions",
     "ra_write_rows", "ra_read_rows", "ra_read_positions", "ra_status_string",
-    "ra_last_hip_error", "ra_attention_plan",
+    "ra_last_hip_error", "ra_attention_plan", "ra_window_select",
 )
 
 
@@ -94,6 +94,7 @@ _SIGS = {
     "ra_status_string": (ctypes.c_char_p, [_I32]),
     "ra_last_hip_error": (_I32, []),
     "ra_attention_plan": (_I32, [_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32)]),
+    "ra_window_select": (_I32, [_P, _I32, _I32, _P, _P, _I32, _P, _P]),
 }
 
 _handle = None
@@ -263,6 +264,14 @@ def ra_read_positions(handle, seq, layer, kv_head, cap, stream=None):
                                     ctypes.byref(n), _stream(stream)),
            "ra_read_positions")
     return np.frombuffer(buf, dtype=np.int32, count=n.value).copy()
+
+
+def ra_window_select(handle, seq_lo, seq_hi, q_window, scores=None, scores_stride=0,
+                     drops=None, stream=None):
+    """Measurement only: the observation-window scoring pass (see the header)."""
+    _check(_lib().ra_window_select(handle, int(seq_lo), int(seq_hi), _ptr(q_window),
+                                   _ptr(scores), int(scores_stride), _ptr(drops),
+                                   _stream(stream)), "ra_window_select")
 
 
 def ra_attention_plan(handle):

@@ -489,6 +489,31 @@ ra_status ra_read_rows(ra_cache* c, int32_t seq, int32_t layer, int32_t kv_head,
   return RA_OK;
 }
 
+ra_status ra_window_select(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
+                           const void* dev_q_window, float* dev_scores,
+                           int32_t scores_stride, int32_t* dev_drops, void* stream) {
+  if (!c || seq_lo < 0 || seq_hi > c->cfg.max_seqs || seq_lo >= seq_hi || !dev_q_window)
+    return RA_ERR_INVALID_ARG;
+  if (c->cfg.dtype != RA_BF16) return RA_ERR_UNSUPPORTED;
+  if (c->step_open()) return RA_ERR_STATE;
+  int max_len = 0;
+  for (int s = seq_lo; s < seq_hi; ++s) {
+    const SeqMeta& M = c->mirror[s];
+    if (!M.active) continue;
+    if (M.step < 64) return RA_ERR_STATE;           // a full 64-query window
+    if (M.len - M.prompt_len - c->cfg.recent_r - M.k_keep > c->cfg.evict_every)
+      return RA_ERR_STATE;
+    max_len = std::max(max_len, M.len);
+  }
+  if (max_len == 0) return RA_OK;
+  if (dev_scores && scores_stride < max_len) return RA_ERR_INVALID_ARG;
+  if (max_len - c->cfg.recent_r > 512 * 32) return RA_ERR_UNSUPPORTED;
+  RA_LAUNCH(ra::launch_window_score(c->shape(), c->meta, c->kpool, c->pos, dev_q_window,
+                                    dev_scores, dev_drops, scores_stride, seq_lo, seq_hi,
+                                    max_len, static_cast<hipStream_t>(stream)));
+  return RA_OK;
+}
+
 ra_status ra_read_positions(ra_cache* c, int32_t seq, int32_t layer, int32_t kv_head,
                             int32_t* host_out, int32_t host_cap, int32_t* n_out,
                             void* stream) {

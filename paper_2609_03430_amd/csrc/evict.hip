@@ -8,8 +8,7 @@
 //      gets its 64-bit Philox score, held in registers (KPT per thread, in
 //      slot order);
 //   2. an MSB-first radix select over the composite (score, candidate index)
-//      finds the m = |C| - k_keep smallest, 8 bits per pass in an LDS
-//      histogram (usually 2 passes: after 16 bits the bucket is exact);
+//      finds the m = |C| - k_keep smallest (select.h);
 //   3. a block scan turns the drop flags into the sorted drop list, stored as
 //      f[k] = d_k - k, so that destination row j receives source row
 //      j + #{k : f[k] <= j};
@@ -20,6 +19,7 @@
 //      the next chunk's sources, so the in-place move is race-free.
 #include "philox.h"
 #include "ra_internal.h"
+#include "select.h"
 
 namespace ra {
 namespace {
@@ -27,21 +27,6 @@ namespace {
 using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
 
 constexpr int kChunk = 64;
-
-__device__ __forceinline__ int score_digit(int level, uint64_t score, int c) {
-  if (level < 8) return static_cast<int>((score >> (56 - 8 * level)) & 0xFF);
-  return level == 8 ? ((c >> 8) & 0xFF) : (c & 0xFF);
-}
-
-__device__ __forceinline__ int wave_inclusive_scan(int x) {
-  const int lane = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
-  return x;
-}
 
 // Number of f[k] <= x for the non-decreasing list f[0..m).
 __device__ __forceinline__ int count_le(const int* f, int m, int x) {
@@ -64,7 +49,6 @@ __global__ __launch_bounds__(NT) void evict_kernel(
     E* __restrict__ vpool, int32_t* __restrict__ pos, int L, int Hkv, int r,
     int slot_lo) {
   static_assert(KPT <= 32, "drop flags live in one 32-bit mask");
-  constexpr int kWaves = NT / 64;
   constexpr int kEpu = 16 / sizeof(E);            // elements per 16-byte unit
   constexpr int kKUnitsRow = kHeadDim / kEpu;     // 16-byte units per key row
   constexpr int kVUnitsCh = 8 / kEpu;             // units per (tile, channel)
@@ -73,11 +57,9 @@ __global__ __launch_bounds__(NT) void evict_kernel(
   constexpr int kKPer = (kKUnits + NT - 1) / NT;
   constexpr int kVPer = (kVUnits + NT - 1) / NT;
 
-  __shared__ int hist[256];
+  __shared__ SelectShared sel_sh;
   __shared__ int f[kMaxEvery];
   __shared__ int src_of[kChunk];
-  __shared__ int wave_tot[kWaves];
-  __shared__ int sel[3];
 
   const int per_seq = L * Hkv;
   const int slot = slot_lo + static_cast<int>(blockIdx.x) / per_seq;
@@ -98,7 +80,7 @@ __global__ __launch_bounds__(NT) void evict_kernel(
 
   // 1. scores of this thread's KPT consecutive candidates
   uint64_t score[KPT];
-  uint32_t undecided = 0, drop = 0;
+  uint32_t valid = 0;
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
     const int c = t * KPT + i;
@@ -108,74 +90,13 @@ __global__ __launch_bounds__(NT) void evict_kernel(
                               static_cast<uint64_t>(event),
                               static_cast<uint64_t>(layer),
                               static_cast<uint64_t>(g), seed, rid);
-      undecided |= 1u << i;
+      valid |= 1u << i;
     }
   }
 
-  // 2. radix select of the m smallest (score, index)
-  int remaining = m;
-  for (int level = 0; level < 10; ++level) {
-    for (int i = t; i < 256; i += NT) hist[i] = 0;
-    __syncthreads();
-#pragma unroll
-    for (int i = 0; i < KPT; ++i)
-      if ((undecided >> i) & 1)
-        atomicAdd(&hist[score_digit(level, score[i], t * KPT + i)], 1);
-    __syncthreads();
-    if (t < 64) {
-      const int h0 = hist[4 * t], h1 = hist[4 * t + 1];
-      const int h2 = hist[4 * t + 2], h3 = hist[4 * t + 3];
-      const int s = h0 + h1 + h2 + h3;
-      int cum = wave_inclusive_scan(s) - s;
-      const int hs[4] = {h0, h1, h2, h3};
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        if (cum < remaining && remaining <= cum + hs[j]) {
-          sel[0] = 4 * t + j;
-          sel[1] = cum;
-          sel[2] = hs[j];
-        }
-        cum += hs[j];
-      }
-    }
-    __syncthreads();
-    const int v = sel[0], below = sel[1], cnt = sel[2];
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      if ((undecided >> i) & 1) {
-        const int dg = score_digit(level, score[i], t * KPT + i);
-        if (dg < v) {
-          drop |= 1u << i;
-          undecided &= ~(1u << i);
-        } else if (dg > v) {
-          undecided &= ~(1u << i);
-        }
-      }
-    }
-    remaining -= below;
-    if (cnt == remaining) {       // the whole bucket goes: selection complete
-      drop |= undecided;
-      undecided = 0;
-      break;
-    }
-    __syncthreads();
-  }
-
-  // 3. sorted drop list as f[k] = d_k - k
-  const int mine = __popc(drop);
-  const int incl = wave_inclusive_scan(mine);
-  if ((t & 63) == 63) wave_tot[t >> 6] = incl;
-  __syncthreads();
-  int k = incl - mine;
-  for (int w = 0; w < (t >> 6); ++w) k += wave_tot[w];
-#pragma unroll
-  for (int i = 0; i < KPT; ++i) {
-    if ((drop >> i) & 1) {
-      f[k] = lp + t * KPT + i - k;
-      ++k;
-    }
-  }
-  __syncthreads();
+  // 2. radix select of the m smallest (score, index); 3. sorted drop list
+  const uint32_t drop = select_smallest<NT, KPT, 64>(score, valid, m, sel_sh);
+  drop_list<NT, KPT>(drop, lp, f, sel_sh);
   const int d0 = f[0];
 
   // 4. order-preserving in-place compaction of positions, keys and values

@@ -89,4 +89,10 @@ struct AttnLaunch {
 };
 hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s);
 
+// Observation-window scorer (measurement only, window_score.hip).
+hipError_t launch_window_score(const Shape& sh, const SeqMeta* meta, const void* kpool,
+                               const int32_t* pos, const void* qwin, float* scores_out,
+                               int32_t* drops_out, int scores_stride, int slot_lo,
+                               int slot_hi, int max_len, hipStream_t s);
+
 }  // namespace ra
