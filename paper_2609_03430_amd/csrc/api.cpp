@@ -99,7 +99,16 @@ void mirror_plan(SeqMeta& M, int r, bool at_trigger) {
   }
 }
 
-void attention_plan(const ra_cache* c, int* split_keys, int* max_splits) {
+// Work decomposition of one attention launch, from the host mirror:
+//  - bf16: about 1024 wavefronts (one per SIMD on 256 CUs, measured best on
+//    the 40-layer workloads against 512..4096); with at least 1024 KV heads,
+//    one wavefront per head and no split; otherwise workgroups of 4
+//    wavefronts per (head, split), as few splits as reach ~1024 wavefronts
+//    (one split per head, so no merge kernel, from 256 heads up);
+//  - fp32: one wavefront per (head, split), ~1024 work items.
+// cfg.attn_split > 0 fixes the keys per work item (rounded up to a multiple
+// of 32 per wavefront).
+void attention_plan(const ra_cache* c, int* split_keys, int* max_splits, int* waves) {
   int cap_max = 32, n_active = 0;
   for (int s = c->slot_lo; s < c->slot_hi; ++s) {
     if (!c->mirror[s].active) continue;
@@ -107,19 +116,22 @@ void attention_plan(const ra_cache* c, int* split_keys, int* max_splits) {
     ++n_active;
   }
   const int heads = std::max(1, n_active * c->cfg.num_kv_heads);
+  const int target = 1024;
+  int w = 1;
+  if (c->cfg.dtype == RA_BF16 && heads < target) w = 4;
+  const int unit = 32 * w;
   int sk;
   if (c->cfg.attn_split > 0) {
-    sk = c->cfg.attn_split;
+    sk = static_cast<int>(round_up(c->cfg.attn_split, unit));
   } else {
-    // about 1024 wavefronts per launch: one per SIMD on 256 CUs (measured
-    // best on the 40-layer, 256-head workload against 512..4096)
-    const int target = 1024;
-    const int splits = std::min(ra::kMaxSplits, std::max(1, (target + heads - 1) / heads));
-    sk = static_cast<int>(round_up((cap_max + splits - 1) / splits, 32));
+    const int per_head = (target + heads - 1) / heads;          // wavefronts per head
+    const int splits = std::min(ra::kMaxSplits, std::max(1, (per_head + w - 1) / w));
+    sk = static_cast<int>(round_up((cap_max + splits - 1) / splits, unit));
   }
-  sk = std::max<int>(sk, static_cast<int>(round_up((cap_max + ra::kMaxSplits - 1) / ra::kMaxSplits, 32)));
+  sk = std::max<int>(sk, static_cast<int>(round_up((cap_max + ra::kMaxSplits - 1) / ra::kMaxSplits, unit)));
   *split_keys = sk;
   *max_splits = (cap_max + sk - 1) / sk;
+  *waves = w;
 }
 
 }  // namespace
@@ -252,8 +264,8 @@ ra_status ra_get_seq_info(const ra_cache* c, int32_t seq, ra_seq_info* out) {
 
 ra_status ra_attention_plan(const ra_cache* c, int32_t* split_keys, int32_t* max_splits) {
   if (!c || !split_keys || !max_splits) return RA_ERR_INVALID_ARG;
-  int sk, ms;
-  attention_plan(c, &sk, &ms);
+  int sk, ms, w;
+  attention_plan(c, &sk, &ms, &w);
   *split_keys = sk;
   *max_splits = ms;
   return RA_OK;
@@ -340,8 +352,8 @@ ra_status ra_decode_attention(ra_cache* c, int32_t layer, const void* q,
   c->appended[layer] = 1;
   ++c->n_appended;
   if (c->slot_hi <= c->slot_lo) return RA_OK;
-  int sk, ms;
-  attention_plan(c, &sk, &ms);
+  int sk, ms, waves;
+  attention_plan(c, &sk, &ms, &waves);
   const size_t G = static_cast<size_t>(c->G);
   const size_t items = static_cast<size_t>(c->cfg.max_seqs) * c->cfg.num_kv_heads * ra::kMaxSplits;
   float* ws = static_cast<float*>(workspace);
@@ -360,6 +372,7 @@ ra_status ra_decode_attention(ra_cache* c, int32_t layer, const void* q,
   a.max_seqs = c->slot_hi;
   a.split_keys = sk;
   a.max_splits = ms;
+  a.waves = waves;
   const hipError_t e = ra::launch_attention(c->shape(), a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) {
     c->appended[layer] = 0;

@@ -104,7 +104,7 @@ __device__ __forceinline__ void append_row(const Work& w, const SeqMeta* meta,
                                            int Hkv, const E* k_new,
                                            const E* v_new, E* kpool, E* vpool,
                                            int32_t* pos) {
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;   // called by one whole wavefront
   const int64_t src = (static_cast<int64_t>(w.slot) * Hkv + w.g) * kHeadDim;
   const int64_t row = w.region + w.len;
   for (int c = lane; c < kHeadDim; c += 64) {
@@ -124,7 +124,7 @@ __device__ __forceinline__ void append_row(const Work& w, const SeqMeta* meta,
 // 2^(s - m) over the split's keys.
 template <typename E>
 __global__ __launch_bounds__(256) void combine_kernel(AttnLaunch a, int G, int Hq,
-                                                      int Hkv) {
+                                                      int Hkv, bool skip_single) {
   __shared__ float sm[kMaxSplits * kMaxGroup];   // split maxima, then weights
   __shared__ float sl[kMaxSplits * kMaxGroup];   // split sums
   __shared__ float inv_l[kMaxGroup];
@@ -134,6 +134,8 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnLaunch a, int G, int H
   const int t = threadIdx.x;
   const int n_keys = M.len + 1;
   const int nsplit = (n_keys + a.split_keys - 1) / a.split_keys;
+  // a head with one split was written directly by the attention kernel
+  if (skip_single && nsplit == 1) return;
   const int head = slot * Hkv + g;
   const float* ml = a.ws_ml + static_cast<int64_t>(head) * kMaxSplits * G * 2;
   const float* po = a.ws_o + static_cast<int64_t>(head) * kMaxSplits * G * kHeadDim;
@@ -194,7 +196,7 @@ struct LaneMap {
 };
 
 __device__ __forceinline__ LaneMap lane_map() {
-  const int lane = threadIdx.x, r = lane & 15, grp = lane >> 4;
+  const int lane = threadIdx.x & 63, r = lane & 15, grp = lane >> 4;
   LaneMap m;
   m.krow[0] = 8 * (r >> 2) + (r & 3);
   m.krow[1] = 8 * (r >> 2) + 4 + (r & 3);
@@ -235,7 +237,7 @@ __device__ __forceinline__ void compute_block(Softmax& st, const BlockRegs& b,
     s0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(b.k[0][s]), qop[s], s0, 0, 0, 0);
     s1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(b.k[1][s]), qop[s], s1, 0, 0, 0);
   }
-  const int grp = threadIdx.x >> 4;
+  const int grp = (threadIdx.x & 63) >> 4;
   float x[8];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -276,13 +278,22 @@ __device__ __forceinline__ void compute_block(Softmax& st, const BlockRegs& b,
   }
 }
 
-template <int NBUF>
-__global__ __launch_bounds__(64, NBUF <= 2 ? 2 : 1) void attn_bf16_kernel(AttnLaunch a, int G,
-                                                       int Hq, int Hkv,
-                                                       float scale_log2) {
+// W wavefronts per workgroup share one (sequence, KV head, split) work item:
+// wavefront v takes the v-th quarter (for W = 4) of the split's keys, and the
+// wavefronts merge their online-softmax states in LDS at the end.  When the
+// head needs a single split, the workgroup writes the normalised output
+// itself and no merge kernel runs.
+template <int W>
+__global__ __launch_bounds__(64 * W, W == 1 ? 2 : 1) void attn_bf16_kernel(
+    AttnLaunch a, int G, int Hq, int Hkv, float scale_log2) {
+  constexpr int kNBuf = 2;   // register buffers (3 or 4 measured no faster)
+  __shared__ float s_m[W][kMaxGroup];
+  __shared__ float s_l[W][kMaxGroup];
+  __shared__ float s_o[W > 1 ? W : 1][kMaxGroup][kHeadDim];
   const Work w = locate(a.meta, a.layer, Hkv, a.split_keys);
   if (!w.valid) return;
-  const int lane = threadIdx.x, qi = lane & 15, grp = lane >> 4;
+  const int wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, qi = lane & 15, grp = lane >> 4;
   const LaneMap lm = lane_map();
   const uint16_t* Kr = static_cast<const uint16_t*>(a.kpool) + w.region * kHeadDim;
   const uint16_t* Vr = static_cast<const uint16_t*>(a.vpool) + w.region * kHeadDim;
@@ -311,34 +322,39 @@ __global__ __launch_bounds__(64, NBUF <= 2 ? 2 : 1) void attn_bf16_kernel(AttnLa
 #pragma unroll
   for (int u = 0; u < 8; ++u) st.acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  const bool owns_last = (w.k1 == w.n_keys);
-  // full blocks: every key a cached row
-  const int nfull = owns_last ? (w.len - w.k0) / 32 : (w.k1 - w.k0) / 32;
+  // this wavefront's keys: [k0, k1) within the split (a multiple of 32 long
+  // except where it ends at the new key)
+  const int kpw = a.split_keys / W;
+  const int k0 = w.k0 + wave * kpw;
+  const int k1 = min(k0 + kpw, w.k1);
+  const bool has = k0 < k1;
+  const bool owns_last = has && k1 == w.n_keys;
+  const int nfull = !has ? 0 : (owns_last ? (w.len - k0) / 32 : (k1 - k0) / 32);
   if (nfull > 0) {
-    // NBUF register buffers in rotation; every prefetch is unconditional
-    // (clamped to the last block, whose repeated loads hit in cache) and the
-    // loop body has no conditional code, so the loads it issues are consumed
-    // by the next iteration and the compiler can neither sink them nor make
-    // the wait before a block's compute also wait for later blocks' loads.
+    // register buffers in rotation; every prefetch is unconditional (clamped
+    // to the last block, whose repeated loads hit in cache) and the loop body
+    // has no conditional code, so the loads it issues are consumed by the
+    // next iteration and the compiler can neither sink them nor make the wait
+    // before a block's compute also wait for later blocks' loads
     const int last = nfull - 1;
-    BlockRegs buf[NBUF];
+    BlockRegs buf[kNBuf];
 #pragma unroll
-    for (int j = 0; j < NBUF; ++j) load_block(buf[j], Kr, Vr, w.k0 + 32 * min(j, last), lm);
+    for (int j = 0; j < kNBuf; ++j) load_block(buf[j], Kr, Vr, k0 + 32 * min(j, last), lm);
     int i = 0;
-    for (; i + NBUF - 1 < nfull; i += NBUF) {
+    for (; i + kNBuf - 1 < nfull; i += kNBuf) {
 #pragma unroll
-      for (int j = 0; j < NBUF; ++j) {
+      for (int j = 0; j < kNBuf; ++j) {
         compute_block(st, buf[j], qop, scale_log2, 32);
-        load_block(buf[j], Kr, Vr, w.k0 + 32 * min(i + NBUF + j, last), lm);
+        load_block(buf[j], Kr, Vr, k0 + 32 * min(i + kNBuf + j, last), lm);
       }
     }
 #pragma unroll
-    for (int j = 0; j < NBUF - 1; ++j)
+    for (int j = 0; j < kNBuf - 1; ++j)
       if (i + j < nfull) compute_block(st, buf[j], qop, scale_log2, 32);
   }
   if (owns_last) {
     // tail block: cached rows below len, the new pair at len, masked above
-    const int kb = w.k0 + 32 * nfull;
+    const int kb = k0 + 32 * nfull;
     const int limit = w.n_keys - kb;       // 1..32 valid keys
     BlockRegs b;
     const u32x4 z = {0u, 0u, 0u, 0u};
@@ -368,7 +384,7 @@ __global__ __launch_bounds__(64, NBUF <= 2 ? 2 : 1) void attn_bf16_kernel(AttnLa
     compute_block(st, b, qop, scale_log2, limit);
   }
 
-  // lane sums of the same query -> full sum
+  // lane sums of the same query -> the wavefront's sum
   st.l += __shfl_xor(st.l, 16, 64);
   st.l += __shfl_xor(st.l, 32, 64);
 
@@ -380,14 +396,62 @@ __global__ __launch_bounds__(64, NBUF <= 2 ? 2 : 1) void attn_bf16_kernel(AttnLa
 
   const int head = w.slot * Hkv + w.g;
   const int64_t item = static_cast<int64_t>(head) * kMaxSplits + w.split;
-  if (qi < G) {
-    float* po = a.ws_o + (item * G + qi) * kHeadDim;
+  uint16_t* out = static_cast<uint16_t*>(a.out);
+  if constexpr (W == 1) {
+    if (qi < G) {
+      if (w.nsplit == 1) {
+        const float inv = 1.f / st.l;
+        const int64_t orow = (static_cast<int64_t>(w.slot) * Hq + w.g * G + qi) * kHeadDim;
 #pragma unroll
-    for (int u = 0; u < 8; ++u)
-      *reinterpret_cast<f32x4*>(po + 16 * u + 4 * grp) = st.acc[u];
-    if (grp == 0) {
-      a.ws_ml[(item * G + qi) * 2] = st.m;
-      a.ws_ml[(item * G + qi) * 2 + 1] = st.l;
+        for (int u = 0; u < 8; ++u)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            out[orow + 16 * u + 4 * grp + i] = f32_to_bf16(st.acc[u][i] * inv);
+      } else {
+        float* po = a.ws_o + (item * G + qi) * kHeadDim;
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          *reinterpret_cast<f32x4*>(po + 16 * u + 4 * grp) = st.acc[u];
+        if (grp == 0) {
+          a.ws_ml[(item * G + qi) * 2] = st.m;
+          a.ws_ml[(item * G + qi) * 2 + 1] = st.l;
+        }
+      }
+    }
+  } else {
+    // merge the W wavefronts in LDS
+    if (qi < G) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        *reinterpret_cast<f32x4*>(&s_o[wave][qi][16 * u + 4 * grp]) = st.acc[u];
+      if (grp == 0) {
+        s_m[wave][qi] = st.m;
+        s_l[wave][qi] = st.l;
+      }
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < G * kHeadDim; idx += 64 * W) {
+      const int q = idx / kHeadDim, c = idx % kHeadDim;
+      float mx = kNegInf;
+#pragma unroll
+      for (int v = 0; v < W; ++v) mx = fmaxf(mx, s_m[v][q]);
+      float lsum = 0.f, o = 0.f;
+#pragma unroll
+      for (int v = 0; v < W; ++v) {
+        const float sc = s_m[v][q] == kNegInf ? 0.f : exp2f(s_m[v][q] - mx);
+        lsum += s_l[v][q] * sc;
+        o += s_o[v][q][c] * sc;
+      }
+      if (w.nsplit == 1) {
+        out[(static_cast<int64_t>(w.slot) * Hq + w.g * G + q) * kHeadDim + c] =
+            f32_to_bf16(o / lsum);
+      } else {
+        a.ws_o[(item * G + q) * kHeadDim + c] = o;
+        if (c == 0) {
+          a.ws_ml[(item * G + q) * 2] = mx;
+          a.ws_ml[(item * G + q) * 2 + 1] = lsum;
+        }
+      }
     }
   }
 }
@@ -508,17 +572,20 @@ hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s)
   const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(kHeadDim));
   const dim3 cgrid(sh.Hkv, a.max_seqs);
   if (sh.dtype == 1) {
-    // two register buffers: measured best; deeper pipelines (3, 4 buffers at
-    // one wavefront per SIMD) were not faster
-    hipLaunchKernelGGL(attn_bf16_kernel<2>, grid, dim3(64), 0, s, a, sh.G, sh.Hq,
-                       sh.Hkv, scale_log2);
-    hipLaunchKernelGGL(combine_kernel<uint16_t>, cgrid, dim3(256), 0, s, a, sh.G,
-                       sh.Hq, sh.Hkv);
+    if (a.waves == 4)
+      hipLaunchKernelGGL(attn_bf16_kernel<4>, grid, dim3(256), 0, s, a, sh.G, sh.Hq,
+                         sh.Hkv, scale_log2);
+    else
+      hipLaunchKernelGGL(attn_bf16_kernel<1>, grid, dim3(64), 0, s, a, sh.G, sh.Hq,
+                         sh.Hkv, scale_log2);
+    if (a.max_splits > 1)
+      hipLaunchKernelGGL(combine_kernel<uint16_t>, cgrid, dim3(256), 0, s, a, sh.G,
+                         sh.Hq, sh.Hkv, true);
   } else {
     hipLaunchKernelGGL(attn_f32_kernel, grid, dim3(64), 0, s, a, sh.G, sh.Hq,
                        sh.Hkv, scale_log2);
     hipLaunchKernelGGL(combine_kernel<float>, cgrid, dim3(256), 0, s, a, sh.G,
-                       sh.Hq, sh.Hkv);
+                       sh.Hq, sh.Hkv, false);
   }
   return hipGetLastError();
 }

@@ -86,6 +86,7 @@ struct AttnLaunch {
   int max_seqs;
   int split_keys;
   int max_splits;
+  int waves;           // wavefronts per work item (bf16 path: 1 or 4)
 };
 hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s);
 
