@@ -26,7 +26,7 @@ namespace {
 
 using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
 
-constexpr int kChunk = 64;
+constexpr int kChunk = 128;   // destination rows moved per barrier round
 
 // Number of f[k] <= x for the non-decreasing list f[0..m).
 __device__ __forceinline__ int count_le(const int* f, int m, int x) {
@@ -41,6 +41,40 @@ __device__ __forceinline__ int count_le(const int* f, int m, int x) {
 __device__ __forceinline__ int64_t vt_index(int64_t row, int ch) {
   // element index of (row, channel) in the transposed 8-row value tiles
   return (row & ~int64_t(7)) * kHeadDim + ch * 8 + (row & 7);
+}
+
+// Eight consecutive bf16 elements starting at element `off` of the 16
+// elements a:b (two adjacent 8-row value tiles of one channel).
+template <int OFF>
+__device__ __forceinline__ u32x4 funnel_at(const uint32_t (&w)[8]) {
+  u32x4 r;
+  if constexpr (OFF % 2 == 0) {
+    r.x = w[OFF / 2];
+    r.y = w[OFF / 2 + 1];
+    r.z = w[OFF / 2 + 2];
+    r.w = w[OFF / 2 + 3];
+  } else {
+    constexpr int i = OFF / 2;
+    r.x = __builtin_amdgcn_alignbyte(w[i + 1], w[i], 2);
+    r.y = __builtin_amdgcn_alignbyte(w[i + 2], w[i + 1], 2);
+    r.z = __builtin_amdgcn_alignbyte(w[i + 3], w[i + 2], 2);
+    r.w = __builtin_amdgcn_alignbyte(w[i + 4], w[i + 3], 2);
+  }
+  return r;
+}
+
+__device__ __forceinline__ u32x4 funnel8(u32x4 a, u32x4 b, int off) {
+  const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+  switch (off) {
+    case 0: return a;
+    case 1: return funnel_at<1>(w);
+    case 2: return funnel_at<2>(w);
+    case 3: return funnel_at<3>(w);
+    case 4: return funnel_at<4>(w);
+    case 5: return funnel_at<5>(w);
+    case 6: return funnel_at<6>(w);
+    default: return funnel_at<7>(w);
+  }
 }
 
 template <int NT, int KPT, typename E, bool POS_ONLY>
@@ -129,10 +163,25 @@ __global__ __launch_bounds__(NT) void evict_kernel(
         const int ch = rem / kVUnitsCh, part = rem % kVUnitsCh;
         const int jt = j0 + tile * 8 + part * kEpu;
         if (u < kVUnits && j0 + tile * 8 < new_len) {
+          const int s0 = src_of[jt - j0], s_last = src_of[jt + kEpu - 1 - j0];
+          if (sizeof(E) == 2 && s_last - s0 == kEpu - 1 && s_last < old_len) {
+            // no drop inside this destination tile: its 8 sources are
+            // consecutive rows, i.e. one or two adjacent source tiles (the
+            // offset is the same for the whole wavefront, so the branch and
+            // the switch in funnel8 do not diverge)
+            const E* a = vpool + vt_index(region + (s0 & ~7), ch);
+            const u32x4 va = *reinterpret_cast<const u32x4*>(a);
+            const int off = s0 & 7;
+            u32x4 vb = va;
+            if (off) vb = *reinterpret_cast<const u32x4*>(a + 8 * kHeadDim);
+            const u32x4 r = funnel8(va, vb, off);
+            __builtin_memcpy(vbuf[q], &r, 16);
+          } else {
 #pragma unroll
-          for (int e = 0; e < kEpu; ++e) {
-            const int sj = src_of[jt + e - j0];
-            vbuf[q][e] = sj < old_len ? vpool[vt_index(region + sj, ch)] : zero_e;
+            for (int e = 0; e < kEpu; ++e) {
+              const int sj = src_of[jt + e - j0];
+              vbuf[q][e] = sj < old_len ? vpool[vt_index(region + sj, ch)] : zero_e;
+            }
           }
         }
       }
@@ -203,8 +252,11 @@ hipError_t launch_mode(const Shape& sh, const SeqMeta* meta, void* kpool,
     return launch_kpt<512, 8, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
   if (max_candidates <= 512 * 16)
     return launch_kpt<512, 16, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
-  if (max_candidates <= 512 * 32)
-    return launch_kpt<512, 32, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+  // more than 16 scores per thread is kept for the largest budgets only: 32
+  // unrolled Philox evaluations exceed the compiler's unroll budget and the
+  // score array then lives in scratch memory
+  if (max_candidates <= 1024 * 16)
+    return launch_kpt<1024, 16, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
   if (max_candidates <= kMaxCandidates)
     return launch_kpt<1024, 32, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
   return hipErrorInvalidValue;

@@ -41,7 +41,7 @@ __device__ __forceinline__ int select_digit(int level, uint64_t key, int c) {
 // the m smallest).  `valid` marks the thread's real candidates; candidate
 // indices must be < 65536.  All threads of the block must call it.
 template <int NT, int KPT, int KEY_BITS>
-__device__ uint32_t select_smallest(const uint64_t (&key)[KPT], uint32_t valid,
+__device__ __forceinline__ uint32_t select_smallest(const uint64_t (&key)[KPT], uint32_t valid,
                                     int m, SelectShared& sh) {
   static_assert(KPT <= 32, "one 32-bit mask per thread");
   const int t = threadIdx.x;
@@ -99,7 +99,7 @@ __device__ uint32_t select_smallest(const uint64_t (&key)[KPT], uint32_t valid,
 // Writes the dropped candidates' slots, ascending, as f[k] = slot_k - k
 // (slot = slot0 + candidate index).  Ends with a barrier.
 template <int NT, int KPT>
-__device__ void drop_list(uint32_t drop, int slot0, int* f, SelectShared& sh) {
+__device__ __forceinline__ void drop_list(uint32_t drop, int slot0, int* f, SelectShared& sh) {
   const int t = threadIdx.x;
   const int mine = __popc(drop);
   const int incl = wave_inclusive_scan(mine);
