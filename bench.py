@@ -373,21 +373,24 @@ def main():
     log("inputs ready; attention split %d keys x %d" % (split_keys, max_splits))
 
     def run_steps(first, n, timed):
+        # HIP events bracket each step's L attention launches (one pair per
+        # step: an event between every launch would add its own gap to the
+        # timed region) and each end-of-step call
         rec = []
         for i in range(first, first + n):
             j = i % RING
             lens = [B.ra_get_seq_info(h, b).len for b in range(Bsz)] if timed else None
             evs = []
+            if timed:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
             for l in range(L):
-                if timed:
-                    e0 = torch.cuda.Event(enable_timing=True)
-                    e1 = torch.cuda.Event(enable_timing=True)
-                    e0.record(stream)
                 B.ra_decode_attention(h, l, q_ring[j, l], k_ring[j, l], v_ring[j, l], out,
                                       cache.workspace, stream)
-                if timed:
-                    e1.record(stream)
-                    evs.append((e0, e1))
+            if timed:
+                e1.record(stream)
+                evs.append((e0, e1))
             if timed:
                 x0 = torch.cuda.Event(enable_timing=True)
                 x1 = torch.cuda.Event(enable_timing=True)
@@ -421,15 +424,15 @@ def main():
     for lens, evs, (x0, x1), nev in rec:
         per_launch = sum(Hkv * ((n + 1) * 2 * 128 * s_el + (2 * 128 * s_el + 4)) +
                          2 * Hq * 128 * s_el for n in lens)
-        for e0, e1 in evs:
+        for e0, e1 in evs:            # one span = L launches
             attn_ms.append(e0.elapsed_time(e1))
-            attn_bytes.append(per_launch)
+            attn_bytes.append(per_launch * L)
         if nev:
             n_events += 1
             seq_events += nev
             ev_ms.append(x0.elapsed_time(x1))
             ev_bytes.append(per_head * nev * L * Hkv)
-    attn_avg_ms = sum(attn_ms) / len(attn_ms)
+    attn_avg_ms = sum(attn_ms) / (len(attn_ms) * L)
     attn_gbs = sum(attn_bytes) / (sum(attn_ms) * 1e-3) / 1e9
     comp = None
     if ev_ms:
@@ -482,7 +485,9 @@ def main():
             "frac": attn_gbs / PEAK_HBM_GBS,
             "traffic": read_traffic(args.workload),
             "avg_launch_ms": attn_avg_ms,
-            "bytes_per_launch": sum(attn_bytes) / len(attn_bytes),
+            "avg_launch_note": "HIP events around each step's launches of all layers, "
+                               "divided by the layer count (inter-kernel gaps included)",
+            "bytes_per_launch": sum(attn_bytes) / (len(attn_bytes) * L),
         },
         "compaction": comp,
         "end_to_end_gbs": total_bytes / wall / 1e9,

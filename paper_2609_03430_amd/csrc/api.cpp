@@ -101,10 +101,12 @@ void mirror_plan(SeqMeta& M, int r, bool at_trigger) {
 
 // Work decomposition of one attention launch, from the host mirror:
 //  - bf16: about 1024 wavefronts (one per SIMD on 256 CUs, measured best on
-//    the 40-layer workloads against 512..4096); with at least 1024 KV heads,
-//    one wavefront per head and no split; otherwise workgroups of 4
-//    wavefronts per (head, split), as few splits as reach ~1024 wavefronts
-//    (one split per head, so no merge kernel, from 256 heads up);
+//    the 40-layer workloads against 512..4096) in at least 256 workgroups (a
+//    workgroup runs on one CU; 8-wavefront groups for 128 heads left half
+//    the CUs idle): W = min(4, 1024 / heads) wavefronts per workgroup (a
+//    power of two), one workgroup per (head, split), as few splits as reach
+//    ~1024 wavefronts, so from 256 KV heads up a head is one workgroup that
+//    writes its output and no merge kernel runs;
 //  - fp32: one wavefront per (head, split), ~1024 work items.
 // cfg.attn_split > 0 fixes the keys per work item (rounded up to a multiple
 // of 32 per wavefront).
@@ -118,7 +120,8 @@ void attention_plan(const ra_cache* c, int* split_keys, int* max_splits, int* wa
   const int heads = std::max(1, n_active * c->cfg.num_kv_heads);
   const int target = 1024;
   int w = 1;
-  if (c->cfg.dtype == RA_BF16 && heads < target) w = 4;
+  if (c->cfg.dtype == RA_BF16)
+    while (w < 4 && heads * w * 2 <= target) w *= 2;
   const int unit = 32 * w;
   int sk;
   if (c->cfg.attn_split > 0) {

@@ -279,8 +279,8 @@ __device__ __forceinline__ void compute_block(Softmax& st, const BlockRegs& b,
 }
 
 // W wavefronts per workgroup share one (sequence, KV head, split) work item:
-// wavefront v takes the v-th quarter (for W = 4) of the split's keys, and the
-// wavefronts merge their online-softmax states in LDS at the end.  When the
+// wavefront v takes the v-th W-th of the split's keys, and the wavefronts
+// merge their online-softmax states in LDS at the end.  When the
 // head needs a single split, the workgroup writes the normalised output
 // itself and no merge kernel runs.
 template <int W>
@@ -574,6 +574,9 @@ hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s)
   if (sh.dtype == 1) {
     if (a.waves == 4)
       hipLaunchKernelGGL(attn_bf16_kernel<4>, grid, dim3(256), 0, s, a, sh.G, sh.Hq,
+                         sh.Hkv, scale_log2);
+    else if (a.waves == 2)
+      hipLaunchKernelGGL(attn_bf16_kernel<2>, grid, dim3(128), 0, s, a, sh.G, sh.Hq,
                          sh.Hkv, scale_log2);
     else
       hipLaunchKernelGGL(attn_bf16_kernel<1>, grid, dim3(64), 0, s, a, sh.G, sh.Hq,
