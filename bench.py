@@ -271,6 +271,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-steps", type=int, default=96)
     ap.add_argument("--attn-split", type=int, default=0)
+    ap.add_argument("--layout", default="chronological",
+                    choices=["chronological", "holefill"],
+                    help="row order kept by eviction (chronological: the paper's)")
     ap.add_argument("--evict-cost", action="store_true",
                     help="eviction-round cost of one sequence at K=1024 (budget counting "
                          "the prompt, prompt 300) over 4096 decode steps, as in the "
@@ -318,8 +321,9 @@ def main():
     total = args.warmup + args.steps
     lps, starts = sequence_plan(args.workload, w, total)
     assert min(starts) >= 0
+    layout = B.RA_LAYOUT_HOLE_FILL if args.layout == "holefill" else B.RA_LAYOUT_CHRONOLOGICAL
     cfg = B.make_config(L, Hq, Hkv, K, R, EVERY, B.RA_BUDGET_EVICTABLE, B.RA_BF16, Bsz,
-                        attn_split=args.attn_split)
+                        attn_split=args.attn_split, layout=layout)
     rows = sum(B.ra_seq_rows(cfg, lp) for lp in lps)
     log("workload %s: pools %.1f GB" % (args.workload, rows * (128 * 2 * 2 + 4) / 1e9))
     cache = B.Cache(cfg, rows, device=dev)
@@ -419,8 +423,15 @@ def main():
     seq_events = 0
     C = K + EVERY                      # candidates at every event of these workloads
     m = EVERY
-    moved = K + R - (C - m) / (m + 1)  # rows from the expected first drop to the end
-    per_head = moved * (2 * 128 * s_el + 4) * 2 + C * 4
+    if layout == B.RA_LAYOUT_HOLE_FILL:
+        # the surviving rows among the last m slots fill the holes below the
+        # new length: expected h = m * (C - m) / C of them... plus all slots'
+        # positions read by the selection
+        moved = m * (1.0 - m / C)
+        per_head = moved * (2 * 128 * s_el + 4) * 2 + (C + R) * 4
+    else:
+        moved = K + R - (C - m) / (m + 1)  # rows from the expected first drop to the end
+        per_head = moved * (2 * 128 * s_el + 4) * 2 + C * 4
     for lens, evs, (x0, x1), nev in rec:
         per_launch = sum(Hkv * ((n + 1) * 2 * 128 * s_el + (2 * 128 * s_el + 4)) +
                          2 * Hq * 128 * s_el for n in lens)
@@ -471,6 +482,7 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": w["desc"],
+            "layout": args.layout,
             "timed_window": window,
             "global_batch": Bsz,
             "seq_len": max(lp + st + total for lp, st in zip(lps, starts)),

@@ -87,7 +87,17 @@ typedef struct {
   int32_t max_seqs;       /* sequence slots, [1, 65536] */
   int32_t attn_split;     /* keys per attention work item (multiple of 32),
                              0 = chosen by the library */
+  int32_t layout;         /* ra_layout: row order kept in each region */
 } ra_config;
+
+typedef enum {
+  RA_LAYOUT_CHRONOLOGICAL = 0, /* rows in position order; an eviction shifts every
+                                  survivor after the first drop (Appendix F: keep
+                                  sets sorted chronologically, gather compaction) */
+  RA_LAYOUT_HOLE_FILL = 1      /* an eviction moves only the surviving rows of the
+                                  last m slots into the holes; rows are unordered
+                                  (positions travel with them); the same kept sets */
+} ra_layout;
 
 typedef struct ra_cache ra_cache;   /* host-side descriptor + host mirror */
 
@@ -216,8 +226,8 @@ ra_status ra_read_rows(ra_cache* cache, int32_t seq, int32_t layer,
                        int32_t kv_head, void* dev_k_out, void* dev_v_out,
                        void* stream);
 
-/* SYNCHRONOUS: copy one head's cached positions (ascending) to host
- * memory; *n_out receives len.  RA_ERR_CAPACITY if host_cap < len (nothing
+/* SYNCHRONOUS: copy one head's cached positions, in row order (ascending in
+ * the chronological layout), to host memory; *n_out receives len.  RA_ERR_CAPACITY if host_cap < len (nothing
  * copied).  Synchronizes `stream`. */
 ra_status ra_read_positions(ra_cache* cache, int32_t seq, int32_t layer,
                             int32_t kv_head, int32_t* host_out,
@@ -241,9 +251,9 @@ ra_status ra_read_positions(ra_cache* cache, int32_t seq, int32_t layer,
  * sequence's last 64 decode steps, oldest first.  dev_scores (optional):
  * [seq_hi-seq_lo][L][Hkv][scores_stride] float, the un-pooled scores of rows
  * [0, len).  dev_drops (optional): [seq_hi-seq_lo][L][Hkv][evict_every]
- * int32, the dropped rows ascending.  The cache is not modified.  bf16 only
- * (RA_ERR_UNSUPPORTED otherwise); RA_ERR_STATE if a slot has fewer than 64
- * steps or more than evict_every rows to drop. */
+ * int32, the dropped rows ascending.  The cache is not modified.  bf16 and
+ * the chronological layout only (RA_ERR_UNSUPPORTED otherwise); RA_ERR_STATE
+ * if a slot has fewer than 64 steps or more than evict_every rows to drop. */
 ra_status ra_window_select(ra_cache* cache, int32_t seq_lo, int32_t seq_hi,
                            const void* dev_q_window, float* dev_scores,
                            int32_t scores_stride, int32_t* dev_drops, void* stream);

@@ -62,7 +62,7 @@ struct ra_cache {
 
   ra::Shape shape() const {
     return ra::Shape{cfg.num_layers, cfg.num_q_heads, cfg.num_kv_heads, G,
-                     cfg.recent_r, cfg.evict_every, cfg.dtype};
+                     cfg.recent_r, cfg.evict_every, cfg.dtype, cfg.layout};
   }
   bool step_open() const { return n_appended != 0; }
   void update_range() {
@@ -76,11 +76,14 @@ struct ra_cache {
       any = true;
     }
   }
+  // slots the selection examines per head (see evict.hip)
+  int span(const SeqMeta& M) const {
+    return M.plan_len - M.prompt_len - (cfg.layout == RA_LAYOUT_HOLE_FILL ? 0 : cfg.recent_r);
+  }
   int max_candidates_due() const {
     int mx = 0;
     for (int s = slot_lo; s < slot_hi; ++s)
-      if (mirror[s].active && mirror[s].due)
-        mx = std::max(mx, mirror[s].plan_len - mirror[s].prompt_len - cfg.recent_r);
+      if (mirror[s].active && mirror[s].due) mx = std::max(mx, span(mirror[s]));
     return mx;
   }
 };
@@ -164,13 +167,16 @@ ra_status ra_config_check(const ra_config* c) {
       c->max_seqs > 65536 || c->attn_split < 0 || c->attn_split % 32 != 0 ||
       (c->budget_mode != RA_BUDGET_EVICTABLE && c->budget_mode != RA_BUDGET_TOTAL) ||
       (c->dtype != RA_F32 && c->dtype != RA_BF16) || c->num_layers > 4096 ||
+      (c->layout != RA_LAYOUT_CHRONOLOGICAL && c->layout != RA_LAYOUT_HOLE_FILL) ||
       c->num_kv_heads > 4096)
     return RA_ERR_INVALID_ARG;
   if (c->head_dim != ra::kHeadDim) return RA_ERR_UNSUPPORTED;
   if (c->num_q_heads / c->num_kv_heads > ra::kMaxGroup) return RA_ERR_UNSUPPORTED;
   if (c->evict_every > ra::kMaxEvery) return RA_ERR_UNSUPPORTED;
-  // the selection holds every candidate's score in registers
-  if (static_cast<int64_t>(c->budget_k) + c->evict_every > ra::kMaxCandidates)
+  // the selection holds every examined slot's score in registers (hole-fill
+  // examines the r most recent slots too)
+  if (static_cast<int64_t>(c->budget_k) + c->evict_every +
+          (c->layout == RA_LAYOUT_HOLE_FILL ? c->recent_r : 0) > ra::kMaxCandidates)
     return RA_ERR_UNSUPPORTED;
   return RA_OK;
 }
@@ -424,8 +430,7 @@ ra_status ra_evict_now(ra_cache* c, int32_t seq, void* stream) {
   mirror_plan(M, c->cfg.recent_r, true);
   if (M.due) {
     RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos, seq,
-                               seq + 1, M.plan_len - M.prompt_len - c->cfg.recent_r,
-                               false, s));
+                               seq + 1, c->span(M), false, s));
   }
   return RA_OK;
 }
@@ -510,7 +515,8 @@ ra_status ra_window_select(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
                            int32_t scores_stride, int32_t* dev_drops, void* stream) {
   if (!c || seq_lo < 0 || seq_hi > c->cfg.max_seqs || seq_lo >= seq_hi || !dev_q_window)
     return RA_ERR_INVALID_ARG;
-  if (c->cfg.dtype != RA_BF16) return RA_ERR_UNSUPPORTED;
+  if (c->cfg.dtype != RA_BF16 || c->cfg.layout != RA_LAYOUT_CHRONOLOGICAL)
+    return RA_ERR_UNSUPPORTED;
   if (c->step_open()) return RA_ERR_STATE;
   int max_len = 0;
   for (int s = seq_lo; s < seq_hi; ++s) {

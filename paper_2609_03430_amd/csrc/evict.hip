@@ -12,11 +12,15 @@
 //   3. a block scan turns the drop flags into the sorted drop list, stored as
 //      f[k] = d_k - k, so that destination row j receives source row
 //      j + #{k : f[k] <= j};
-//   4. the surviving rows are moved down in chunks of 64 destination rows:
+//   4. chronological layout (the paper's): the surviving rows are moved
+//      down in chunks of 128 destination rows:
 //      every thread gathers its part of the chunk into registers, the block
 //      waits until all loads have returned and synchronises, then writes.
 //      Sources are never below destinations and a chunk's writes land below
-//      the next chunk's sources, so the in-place move is race-free.
+//      the next chunk's sources, so the in-place move is race-free;
+//      hole-fill layout: only the surviving rows of the last m slots move,
+//      into the holes below the new length (order no longer chronological;
+//      the positions travel with the rows).
 #include "philox.h"
 #include "ra_internal.h"
 #include "select.h"
@@ -34,6 +38,16 @@ __device__ __forceinline__ int count_le(const int* f, int m, int x) {
   while (lo < hi) {
     const int mid = (lo + hi) >> 1;
     if (f[mid] <= x) lo = mid + 1; else hi = mid;
+  }
+  return lo;
+}
+
+// Number of drops d_k (= f[k] + k, ascending) with d_k <= x.
+__device__ __forceinline__ int count_le_slot(const int* f, int m, int x) {
+  int lo = 0, hi = m;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (f[mid] + mid <= x) lo = mid + 1; else hi = mid;
   }
   return lo;
 }
@@ -77,7 +91,7 @@ __device__ __forceinline__ u32x4 funnel8(u32x4 a, u32x4 b, int off) {
   }
 }
 
-template <int NT, int KPT, typename E, bool POS_ONLY>
+template <int NT, int KPT, typename E, bool POS_ONLY, int LAYOUT>
 __global__ __launch_bounds__(NT) void evict_kernel(
     const SeqMeta* __restrict__ meta, E* __restrict__ kpool,
     E* __restrict__ vpool, int32_t* __restrict__ pos, int L, int Hkv, int r,
@@ -104,34 +118,81 @@ __global__ __launch_bounds__(NT) void evict_kernel(
   const int lp = Mref.prompt_len, old_len = Mref.plan_len;
   const int event = Mref.plan_event;
   const uint64_t seed = Mref.seed, rid = Mref.rid;
-  const int C = old_len - lp - r;
-  const int m = C - Mref.k_keep;
-  if (m <= 0) return;
+  const int C = old_len - lp - r;          // candidates: every cached position
+  const int m = C - Mref.k_keep;           // outside the prompt and the r most
+  if (m <= 0) return;                      // recent ones (positions < thr)
+  const int thr = lp + Mref.step - r;
   const int new_len = old_len - m;
+  // slots that can hold candidates: all of them in the chronological layout
+  // are [lp, old_len - r); after hole-fill events the recent rows may sit
+  // anywhere above the prompt, so every slot from lp is examined
+  const int span = LAYOUT == 0 ? C : old_len - lp;
   const int64_t region = Mref.base + static_cast<int64_t>(lg) * Mref.cap;
   int32_t* P = pos + region;
   const int t = threadIdx.x;
 
-  // 1. scores of this thread's KPT consecutive candidates
+  // 1. scores of this thread's KPT consecutive slots; ties by position
   uint64_t score[KPT];
+  uint32_t tie[KPT];
   uint32_t valid = 0;
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
     const int c = t * KPT + i;
     score[i] = 0;
-    if (c < C) {
-      score[i] = philox_score(static_cast<uint64_t>(P[lp + c]),
-                              static_cast<uint64_t>(event),
-                              static_cast<uint64_t>(layer),
-                              static_cast<uint64_t>(g), seed, rid);
-      valid |= 1u << i;
+    tie[i] = 0;
+    if (c < span) {
+      const int p = P[lp + c];
+      if (p < thr) {
+        score[i] = philox_score(static_cast<uint64_t>(p), static_cast<uint64_t>(event),
+                                static_cast<uint64_t>(layer), static_cast<uint64_t>(g),
+                                seed, rid);
+        tie[i] = static_cast<uint32_t>(p);
+        valid |= 1u << i;
+      }
     }
   }
 
-  // 2. radix select of the m smallest (score, index); 3. sorted drop list
-  const uint32_t drop = select_smallest<NT, KPT, 64>(score, valid, m, sel_sh);
+  // 2. radix select of the m smallest (score, position); 3. drop list
+  const uint32_t drop = select_smallest<NT, KPT, 64>(score, tie, valid, m, sel_sh);
   drop_list<NT, KPT>(drop, lp, f, sel_sh);
   const int d0 = f[0];
+
+  if constexpr (LAYOUT == 1) {
+    // hole-fill: the h holes below new_len take the h surviving rows of the
+    // tail [new_len, old_len), in ascending order; nothing else moves
+    __shared__ int mv_src[kMaxEvery];
+    __shared__ int mv_dst[kMaxEvery];
+    __shared__ int n_holes;
+    if (t == 0) n_holes = count_le_slot(f, m, new_len - 1);
+    __syncthreads();
+    const int h = n_holes;
+    for (int i = t; i < m; i += NT) {
+      const int s = new_len + i;                 // tail slot
+      const int before = count_le_slot(f, m, s - 1) - h;   // tail drops below s
+      const bool dropped = h + before < m && f[h + before] + h + before == s;
+      if (!dropped) {
+        const int j = i - before;                // rank among tail survivors
+        mv_src[j] = s;
+        mv_dst[j] = f[j] + j;
+      }
+    }
+    __syncthreads();
+    for (int j = t; j < h; j += NT) P[mv_dst[j]] = P[mv_src[j]];
+    if constexpr (!POS_ONLY) {
+      constexpr int kUnitsRow = kHeadDim * sizeof(E) / 16;
+      for (int idx = t; idx < h * kUnitsRow; idx += NT) {
+        const int j = idx / kUnitsRow, col = idx % kUnitsRow;
+        *reinterpret_cast<u32x4*>(kpool + (region + mv_dst[j]) * kHeadDim + col * (16 / sizeof(E))) =
+            *reinterpret_cast<const u32x4*>(kpool + (region + mv_src[j]) * kHeadDim +
+                                            col * (16 / sizeof(E)));
+      }
+      for (int idx = t; idx < h * kHeadDim; idx += NT) {
+        const int j = idx / kHeadDim, ch = idx % kHeadDim;
+        vpool[vt_index(region + mv_dst[j], ch)] = vpool[vt_index(region + mv_src[j], ch)];
+      }
+    }
+    return;
+  }
 
   // 4. order-preserving in-place compaction of positions, keys and values
   const E zero_e = E(0);
@@ -219,23 +280,34 @@ __global__ __launch_bounds__(NT) void evict_kernel(
   }
 }
 
-template <int NT, int KPT, bool POS_ONLY>
-hipError_t launch_kpt(const Shape& sh, const SeqMeta* meta, void* kpool,
-                      void* vpool, int32_t* pos, int slot_lo, int slot_hi,
-                      hipStream_t s) {
+template <int NT, int KPT, bool POS_ONLY, int LAYOUT>
+hipError_t launch_layout(const Shape& sh, const SeqMeta* meta, void* kpool,
+                         void* vpool, int32_t* pos, int slot_lo, int slot_hi,
+                         hipStream_t s) {
   const dim3 grid((slot_hi - slot_lo) * sh.L * sh.Hkv);
   if (sh.dtype == 1) {
-    hipLaunchKernelGGL((evict_kernel<NT, KPT, uint16_t, POS_ONLY>), grid,
+    hipLaunchKernelGGL((evict_kernel<NT, KPT, uint16_t, POS_ONLY, LAYOUT>), grid,
                        dim3(NT), 0, s, meta, static_cast<uint16_t*>(kpool),
                        static_cast<uint16_t*>(vpool), pos, sh.L, sh.Hkv, sh.r,
                        slot_lo);
   } else {
-    hipLaunchKernelGGL((evict_kernel<NT, KPT, float, POS_ONLY>), grid,
+    hipLaunchKernelGGL((evict_kernel<NT, KPT, float, POS_ONLY, LAYOUT>), grid,
                        dim3(NT), 0, s, meta, static_cast<float*>(kpool),
                        static_cast<float*>(vpool), pos, sh.L, sh.Hkv, sh.r,
                        slot_lo);
   }
   return hipGetLastError();
+}
+
+template <int NT, int KPT, bool POS_ONLY>
+hipError_t launch_kpt(const Shape& sh, const SeqMeta* meta, void* kpool,
+                      void* vpool, int32_t* pos, int slot_lo, int slot_hi,
+                      hipStream_t s) {
+  if (sh.layout == 1)
+    return launch_layout<NT, KPT, POS_ONLY, 1>(sh, meta, kpool, vpool, pos, slot_lo,
+                                               slot_hi, s);
+  return launch_layout<NT, KPT, POS_ONLY, 0>(sh, meta, kpool, vpool, pos, slot_lo,
+                                             slot_hi, s);
 }
 
 template <bool POS_ONLY>

@@ -45,6 +45,7 @@ static_assert(sizeof(SeqMeta) == 64, "SeqMeta must stay 64 bytes");
 
 struct Shape {
   int L, Hq, Hkv, G, r, every, dtype;  // dtype: 0 f32, 1 bf16
+  int layout;                          // 0 chronological, 1 hole-fill
 };
 
 // ---- launch wrappers (defined in the .hip files) ----------------------------

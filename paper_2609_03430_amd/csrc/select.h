@@ -1,8 +1,8 @@
 // Block-wide selection of the m smallest candidates, shared by the eviction
 // kernel (64-bit random scores) and the observation-window scorer (32-bit
-// score bits).  Each thread holds KPT consecutive candidates in registers
-// (candidate c = thread * KPT + i); the order is the composite
-// (key, candidate index), so the result is unique even with equal keys.
+// score bits).  Each thread holds KPT candidates in registers; the order is
+// the composite (key, tie) with a distinct 32-bit tie per candidate (the
+// token position, or the row), so the result is unique even with equal keys.
 // MSB-first radix select, 8 bits per pass, 256-bin LDS histogram; a pass
 // ends the selection as soon as the whole bucket holding the m-th smallest is
 // dropped (usually after two passes for uniform keys).
@@ -30,31 +30,33 @@ __device__ __forceinline__ int wave_inclusive_scan(int x) {
 }
 
 template <int KEY_BITS>
-__device__ __forceinline__ int select_digit(int level, uint64_t key, int c) {
+__device__ __forceinline__ int select_digit(int level, uint64_t key, uint32_t tie) {
   constexpr int kKeyLevels = KEY_BITS / 8;
   if (level < kKeyLevels)
     return static_cast<int>((key >> (KEY_BITS - 8 - 8 * level)) & 0xFF);
-  return level == kKeyLevels ? ((c >> 8) & 0xFF) : (c & 0xFF);
+  return static_cast<int>((tie >> (24 - 8 * (level - kKeyLevels))) & 0xFF);
 }
 
-// Returns this thread's drop mask (bit i: candidate thread*KPT + i is among
-// the m smallest).  `valid` marks the thread's real candidates; candidate
-// indices must be < 65536.  All threads of the block must call it.
+// Returns this thread's drop mask (bit i: its candidate i is among the m
+// smallest (key, tie)).  `valid` marks the thread's real candidates.  All
+// threads of the block must call it.
 template <int NT, int KPT, int KEY_BITS>
-__device__ __forceinline__ uint32_t select_smallest(const uint64_t (&key)[KPT], uint32_t valid,
-                                    int m, SelectShared& sh) {
+__device__ __forceinline__ uint32_t select_smallest(const uint64_t (&key)[KPT],
+                                                   const uint32_t (&tie)[KPT],
+                                                   uint32_t valid, int m,
+                                                   SelectShared& sh) {
   static_assert(KPT <= 32, "one 32-bit mask per thread");
   const int t = threadIdx.x;
   uint32_t undecided = valid, drop = 0;
   int remaining = m;
   if (m <= 0) return 0;
-  for (int level = 0; level < KEY_BITS / 8 + 2; ++level) {
+  for (int level = 0; level < KEY_BITS / 8 + 4; ++level) {
     for (int i = t; i < 256; i += NT) sh.hist[i] = 0;
     __syncthreads();
 #pragma unroll
     for (int i = 0; i < KPT; ++i)
       if ((undecided >> i) & 1)
-        atomicAdd(&sh.hist[select_digit<KEY_BITS>(level, key[i], t * KPT + i)], 1);
+        atomicAdd(&sh.hist[select_digit<KEY_BITS>(level, key[i], tie[i])], 1);
     __syncthreads();
     if (t < 64) {
       const int h0 = sh.hist[4 * t], h1 = sh.hist[4 * t + 1];
@@ -77,7 +79,7 @@ __device__ __forceinline__ uint32_t select_smallest(const uint64_t (&key)[KPT], 
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       if ((undecided >> i) & 1) {
-        const int dg = select_digit<KEY_BITS>(level, key[i], t * KPT + i);
+        const int dg = select_digit<KEY_BITS>(level, key[i], tie[i]);
         if (dg < v) {
           drop |= 1u << i;
           undecided &= ~(1u << i);

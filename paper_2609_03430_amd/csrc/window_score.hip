@@ -208,11 +208,13 @@ __global__ __launch_bounds__(kNT) void window_score_kernel(
   }
   // max-pool and select the m lowest candidates
   uint64_t key[KPT];
+  uint32_t tie[KPT];
   uint32_t valid = 0;
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
     const int c = t * KPT + i;
     key[i] = 0;
+    tie[i] = static_cast<uint32_t>(c);      // ties by row, lower first
     if (c < n_cand) {
       float mxp = 0.f;
       for (int j = max(0, c - kPoolHalf); j <= min(len - 1, c + kPoolHalf); ++j)
@@ -221,7 +223,7 @@ __global__ __launch_bounds__(kNT) void window_score_kernel(
       valid |= 1u << i;
     }
   }
-  const uint32_t drop = select_smallest<kNT, KPT, 32>(key, valid, m, sel_sh);
+  const uint32_t drop = select_smallest<kNT, KPT, 32>(key, tie, valid, m, sel_sh);
   drop_list<kNT, KPT>(drop, 0, f, sel_sh);
   if (drops_out) {
     for (int k = t; k < m; k += kNT) drops_out[head_out * every + k] = f[k] + k;

@@ -26,7 +26,8 @@ class Run:
     def __init__(self, L, Hq, Hkv, K, lps, r=64, every=64, dtype=B.RA_BF16,
                  mode=B.RA_BUDGET_EVICTABLE, seeds=None, rids=None,
                  scaled=True, wl_seed=1000, ring=None, attn_split=0,
-                 max_seqs=None, write_prompt=True, begin=True):
+                 max_seqs=None, write_prompt=True, begin=True,
+                 layout=B.RA_LAYOUT_CHRONOLOGICAL):
         self.L, self.Hq, self.Hkv, self.K, self.r, self.every = L, Hq, Hkv, K, r, every
         self.G = Hq // Hkv
         self.lps = list(lps)
@@ -37,8 +38,9 @@ class Run:
         self.rids = list(rids) if rids is not None else list(range(n))
         self.mode = mode
         self.tdtype = torch.bfloat16 if dtype == B.RA_BF16 else torch.float32
+        self.layout = layout
         self.cfg = B.make_config(L, Hq, Hkv, K, r, every, mode, dtype, self.max_seqs,
-                                 attn_split=attn_split)
+                                 attn_split=attn_split, layout=layout)
         rows = sum(B.ra_seq_rows(self.cfg, lp) for lp in self.lps)
         self.cache = B.Cache(self.cfg, rows)
         self.h = self.cache.handle
@@ -123,16 +125,26 @@ class Run:
         del k, v, pos
 
     def positions(self, slot, layer, g):
+        """Cached positions in row order (ascending only in the chronological
+        layout)."""
         info = B.ra_get_seq_info(self.h, slot)
         return B.ra_read_positions(self.h, slot, layer, g, info.cap)
 
-    def rows(self, slot, layer, g):
+    def sorted_positions(self, slot, layer, g):
+        return np.sort(self.positions(slot, layer, g))
+
+    def rows(self, slot, layer, g, by_position=False):
+        """Cached key and value rows in row order, or ordered by position."""
         info = B.ra_get_seq_info(self.h, slot)
         k = torch.empty(info.len, 128, dtype=self.tdtype, device=DEV)
         v = torch.empty_like(k)
         B.ra_read_rows(self.h, slot, layer, g, k, v)
         torch.cuda.synchronize()
-        return k.cpu(), v.cpu()
+        k, v = k.cpu(), v.cpu()
+        if by_position:
+            order = torch.from_numpy(np.argsort(self.positions(slot, layer, g), kind="stable"))
+            k, v = k[order], v[order]
+        return k, v
 
     def close(self):
         self.cache.close()

@@ -30,13 +30,15 @@ T = 32768
 WINDOW = 72          # steps decoded on the GPU (events at 32704 and 32768)
 
 
-@pytest.mark.parametrize("name", sorted(SHAPES))
-def test_full_size(name):
+@pytest.mark.parametrize("name,layout", [(n, 0) for n in sorted(SHAPES)] +
+                         [("qwen3-14b", 1)])
+def test_full_size(name, layout):
     L, Hq, Hkv, Bsz, lp, K, seed = SHAPES[name]
-    log("full size %s: L=%d Hq=%d Hkv=%d B=%d lp=%d K=%d" % (name, L, Hq, Hkv, Bsz, lp, K))
+    log("full size %s layout %d: L=%d Hq=%d Hkv=%d B=%d lp=%d K=%d"
+        % (name, layout, L, Hq, Hkv, Bsz, lp, K))
     run = Run(L=L, Hq=Hq, Hkv=Hkv, K=K, lps=[lp] * Bsz, r=64, every=64,
               seeds=[seed * 1000003 + b for b in range(Bsz)], rids=list(range(Bsz)),
-              wl_seed=seed, ring=64, write_prompt=False)
+              wl_seed=seed, ring=64, write_prompt=False, layout=layout)
     t0 = T - WINDOW
     run.fast_forward(t0)
     for b in range(Bsz):
@@ -67,7 +69,7 @@ def test_full_size(name):
         for o in oracles.values():
             o.rep.end_step()
     for b, l, g in sites:
-        got = run.positions(b, l, g)
+        got = run.sorted_positions(b, l, g) if layout else run.positions(b, l, g)
         want = oracles[b].rep.P[(l, g)]
         assert np.array_equal(got, want), (name, b, l, g)
     assert oracles[0].rep.event >= 2

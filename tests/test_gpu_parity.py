@@ -19,24 +19,33 @@ TOL = {B.RA_BF16: 2e-2, B.RA_F32: 1e-5}
 
 
 def _check_heads(run, oracles, rows=True):
+    """Kept positions equal the oracle's (as a sorted list in the hole-fill
+    layout, whose rows are unordered), and every row holds its position's
+    key and value."""
+    holefill = run.layout == B.RA_LAYOUT_HOLE_FILL
     for o in oracles:
         for (layer, g) in o.heads:
             got = run.positions(o.slot, layer, g)
             want = o.rep.P[(layer, g)]
+            if holefill:
+                assert len(set(got.tolist())) == len(got)
+                got = np.sort(got)
             assert np.array_equal(got, want), (o.slot, layer, g, o.rep.step)
             if rows:
-                k, v = run.rows(o.slot, layer, g)
+                k, v = run.rows(o.slot, layer, g, by_position=holefill)
                 kw, vw = o.rows(layer, g, want)
                 assert torch.equal(k, kw), (o.slot, layer, g)
                 assert torch.equal(v, vw), (o.slot, layer, g)
 
 
+@pytest.mark.parametrize("layout", [B.RA_LAYOUT_CHRONOLOGICAL, B.RA_LAYOUT_HOLE_FILL])
 @pytest.mark.parametrize("dtype", [B.RA_BF16, B.RA_F32])
-def test_small_decode_parity(dtype):
+def test_small_decode_parity(dtype, layout):
     """Three sequences (prompts 5, 0, 17), r=8, every=8, K=40, 150 steps:
     every output, and every head's positions and rows after every event."""
-    log("small decode parity dtype=%d" % dtype)
-    run = Run(L=2, Hq=4, Hkv=2, K=40, lps=[5, 0, 17], r=8, every=8, dtype=dtype)
+    log("small decode parity dtype=%d layout=%d" % (dtype, layout))
+    run = Run(L=2, Hq=4, Hkv=2, K=40, lps=[5, 0, 17], r=8, every=8, dtype=dtype,
+              layout=layout)
     oracles = [OracleSeq(run, s) for s in range(run.n)]
     worst = 0.0
     events = 0
@@ -59,20 +68,24 @@ def test_small_decode_parity(dtype):
     run.close()
 
 
-@pytest.mark.parametrize("lp,K,r,every,mode", [
-    (37, 100, 16, 16, B.RA_BUDGET_EVICTABLE),
-    (0, 64, 0, 1, B.RA_BUDGET_EVICTABLE),
-    (300, 300, 64, 64, B.RA_BUDGET_TOTAL),        # k_keep = 0
-    (5, 1000, 64, 64, B.RA_BUDGET_EVICTABLE),
-    (129, 8192, 64, 64, B.RA_BUDGET_EVICTABLE),   # 8256 candidates
+@pytest.mark.parametrize("lp,K,r,every,mode,layout", [
+    (37, 100, 16, 16, B.RA_BUDGET_EVICTABLE, 0),
+    (0, 64, 0, 1, B.RA_BUDGET_EVICTABLE, 0),
+    (300, 300, 64, 64, B.RA_BUDGET_TOTAL, 0),        # k_keep = 0
+    (5, 1000, 64, 64, B.RA_BUDGET_EVICTABLE, 0),
+    (129, 8192, 64, 64, B.RA_BUDGET_EVICTABLE, 0),   # 8256 candidates
+    (37, 100, 16, 16, B.RA_BUDGET_EVICTABLE, 1),
+    (3, 50, 40, 8, B.RA_BUDGET_EVICTABLE, 1),        # r > every: recent rows move
+    (0, 64, 0, 1, B.RA_BUDGET_EVICTABLE, 1),
+    (129, 8192, 64, 64, B.RA_BUDGET_EVICTABLE, 1),
 ])
-def test_fast_forward_and_evict_now(lp, K, r, every, mode):
+def test_fast_forward_and_evict_now(lp, K, r, every, mode, layout):
     """Positions-only fast forward and explicit events at arbitrary steps
     keep the same sets as the oracle; rows written afterwards are compacted
     exactly by a full event."""
-    log("fast forward lp=%d K=%d r=%d every=%d mode=%d" % (lp, K, r, every, mode))
+    log("fast forward lp=%d K=%d r=%d every=%d mode=%d layout=%d" % (lp, K, r, every, mode, layout))
     run = Run(L=2, Hq=2, Hkv=2, K=K, lps=[lp, max(0, lp - 3)], r=r, every=every, mode=mode,
-              seeds=[2**63 + 11, 5], rids=[2**40 + 1, 9])
+              seeds=[2**63 + 11, 5], rids=[2**40 + 1, 9], layout=layout)
     oracles = [OracleSeq(run, s) for s in range(run.n)]
     rng = np.random.default_rng(lp + K)
     for rep in range(3 if K <= 1000 else 1):
