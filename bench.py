@@ -274,6 +274,12 @@ def main():
     ap.add_argument("--layout", default="chronological",
                     choices=["chronological", "holefill"],
                     help="row order kept by eviction (chronological: the paper's)")
+    ap.add_argument("--policy", default="random",
+                    choices=["random", "shared", "block", "recency"],
+                    help="eviction policy: Random Attention, or one of the paper's "
+                         "controls (shared draw, block-wise, recency + prompt)")
+    ap.add_argument("--block", type=int, default=64,
+                    help="tokens per block for --policy block (a divisor of 64)")
     ap.add_argument("--evict-cost", action="store_true",
                     help="eviction-round cost of one sequence at K=1024 (budget counting "
                          "the prompt, prompt 300) over 4096 decode steps, as in the "
@@ -322,8 +328,14 @@ def main():
     lps, starts = sequence_plan(args.workload, w, total)
     assert min(starts) >= 0
     layout = B.RA_LAYOUT_HOLE_FILL if args.layout == "holefill" else B.RA_LAYOUT_CHRONOLOGICAL
+    policy = {"random": B.RA_POLICY_RANDOM, "shared": B.RA_POLICY_SHARED,
+              "block": B.RA_POLICY_BLOCK, "recency": B.RA_POLICY_RECENCY}[args.policy]
+    if policy == B.RA_POLICY_BLOCK and (args.block < 1 or EVERY % args.block):
+        print("--block must divide %d" % EVERY, file=sys.stderr)
+        sys.exit(2)
     cfg = B.make_config(L, Hq, Hkv, K, R, EVERY, B.RA_BUDGET_EVICTABLE, B.RA_BF16, Bsz,
-                        attn_split=args.attn_split, layout=layout)
+                        attn_split=args.attn_split, layout=layout, policy=policy,
+                        policy_block=args.block)
     rows = sum(B.ra_seq_rows(cfg, lp) for lp in lps)
     log("workload %s: pools %.1f GB" % (args.workload, rows * (128 * 2 * 2 + 4) / 1e9))
     cache = B.Cache(cfg, rows, device=dev)
@@ -423,14 +435,22 @@ def main():
     seq_events = 0
     C = K + EVERY                      # candidates at every event of these workloads
     m = EVERY
+    # expected rows an event moves; drops fall on whole units of `unit` rows
+    # (1 for the per-token draws, B for block-wise), m / unit of C / unit units
+    unit = args.block if policy == B.RA_POLICY_BLOCK else 1
     if layout == B.RA_LAYOUT_HOLE_FILL:
         # the surviving rows among the last m slots fill the holes below the
-        # new length: expected h = m * (C - m) / C of them... plus all slots'
-        # positions read by the selection
-        moved = m * (1.0 - m / C)
+        # new length (recency drops none of them), plus all slots' positions
+        # read by the selection
+        moved = m if policy == B.RA_POLICY_RECENCY else m * (1.0 - m / C)
         per_head = moved * (2 * 128 * s_el + 4) * 2 + (C + R) * 4
     else:
-        moved = K + R - (C - m) / (m + 1)  # rows from the expected first drop to the end
+        # rows from the first drop to the end: recency drops the first
+        # candidate; otherwise the first of j dropped units among n is
+        # preceded by (n - j) / (j + 1) kept units on average
+        n_u, j_u = C // unit, m // unit
+        first = 0.0 if policy == B.RA_POLICY_RECENCY else unit * (n_u - j_u) / (j_u + 1)
+        moved = K + R - first
         per_head = moved * (2 * 128 * s_el + 4) * 2 + C * 4
     for lens, evs, (x0, x1), nev in rec:
         per_launch = sum(Hkv * ((n + 1) * 2 * 128 * s_el + (2 * 128 * s_el + 4)) +
@@ -483,6 +503,8 @@ def main():
         "config": {
             "workload": w["desc"],
             "layout": args.layout,
+            "policy": args.policy if policy != B.RA_POLICY_BLOCK
+            else "block%d" % args.block,
             "timed_window": window,
             "global_batch": Bsz,
             "seq_len": max(lp + st + total for lp, st in zip(lps, starts)),

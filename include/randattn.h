@@ -45,7 +45,10 @@
  * (key, p) pairs are dropped and the survivors are compacted in place,
  * chronological order kept.  k_keep = budget_k (RA_BUDGET_EVICTABLE) or
  * budget_k - lp (RA_BUDGET_TOTAL, the convention of Eq. 1, where the
- * prompt counts against K).
+ * prompt counts against K).  The diagnostic policies of ra_policy change
+ * only the key: the shared draw uses counter (p/4, e, 0, 0); the block
+ * policy uses the key of s = lp + policy_block * floor((p - lp) /
+ * policy_block) in place of that of p; recency uses p itself.
  */
 #ifndef RANDATTN_H
 #define RANDATTN_H
@@ -88,6 +91,8 @@ typedef struct {
   int32_t attn_split;     /* keys per attention work item (multiple of 32),
                              0 = chosen by the library */
   int32_t layout;         /* ra_layout: row order kept in each region */
+  int32_t policy;         /* ra_policy: which candidates an eviction keeps */
+  int32_t policy_block;   /* RA_POLICY_BLOCK: tokens per block (>= 1) */
 } ra_config;
 
 typedef enum {
@@ -98,6 +103,22 @@ typedef enum {
                                   last m slots into the holes; rows are unordered
                                   (positions travel with them); the same kept sets */
 } ra_layout;
+
+typedef enum {
+  RA_POLICY_RANDOM = 0,   /* Random Attention (Section 3): an independent
+                             uniform draw per candidate, per KV head, per event */
+  RA_POLICY_SHARED = 1,   /* shared-draw control (Section 5, Appendix D): the
+                             same random positions in every head -- the draw
+                             omits the layer and the KV head */
+  RA_POLICY_BLOCK = 2,    /* block-wise eviction (Section 5): history kept in
+                             contiguous blocks of policy_block tokens -- every
+                             position takes the draw of its block's first
+                             position (blocks aligned at the prompt end), so
+                             policy_block = 1 is RA_POLICY_RANDOM */
+  RA_POLICY_RECENCY = 3   /* recency+prompt (Section 4.1): the prompt plus the
+                             contiguous recent window -- the oldest candidates
+                             are dropped, no draw */
+} ra_policy;
 
 typedef struct ra_cache ra_cache;   /* host-side descriptor + host mirror */
 

@@ -38,6 +38,23 @@ Readings where the paper is silent (each is also listed in the design notes)
 * Event index e counts the evictions performed on the sequence so far
   (0-based), shared by all its layers and KV heads.
 
+Diagnostic policies (the paper's controls, on the same trigger and select)
+--------------------------------------------------------------------------
+Only the key of a candidate changes; the m smallest (key, position) pairs
+are still the ones dropped.
+* Shared draw (Section 5, Appendix D): the same random positions in every
+  head.  Reading: the key of p is the Random Attention key with the layer and
+  KV head fixed at 0, so every (layer, head) keeps the set that (0, 0) keeps.
+* Block-wise (Section 5): history kept in contiguous blocks of B tokens.
+  Reading: blocks are aligned at the end of the prompt, block b covering
+  positions lp + bB .. lp + bB + B - 1, and every position takes the key of
+  its block's first position, so whole blocks go together (the one block that
+  straddles the cut loses its earliest positions first) and B = 1 is Random
+  Attention.
+* Recency + prompt (Section 4.1): the prompt plus the contiguous recent
+  window.  The key is the position itself, so the oldest candidates go and
+  the cache is always the prompt plus the last k_keep + r positions.
+
 Parity: pinned by the tests against brute-force subset enumeration, the
 exact subset law and marginal inclusion (chi-square), cross-head and
 cross-event independence, the survival law of Appendix D, the structural
@@ -52,6 +69,11 @@ from .philox import philox4x64_10_np
 
 BUDGET_EVICTABLE = 0
 BUDGET_TOTAL = 1
+
+POLICY_RANDOM = 0
+POLICY_SHARED = 1
+POLICY_BLOCK = 2
+POLICY_RECENCY = 3
 
 
 def keep_count(budget_k, prompt_len, mode):
@@ -75,6 +97,24 @@ def position_keys(positions, seed, request_id, event, layer, kv_head):
     return np.choose(lane, words)
 
 
+def policy_keys(policy, candidates, prompt_len, seed, request_id, event,
+                layer, kv_head, block=1):
+    """Keys of the candidates under one of the policies above."""
+    cand = np.asarray(candidates, dtype=np.int64)
+    if policy == POLICY_RANDOM:
+        return position_keys(cand, seed, request_id, event, layer, kv_head)
+    if policy == POLICY_SHARED:
+        return position_keys(cand, seed, request_id, event, 0, 0)
+    if policy == POLICY_BLOCK:
+        if block < 1:
+            raise ValueError("block size must be >= 1")
+        first = prompt_len + (cand - prompt_len) // block * block
+        return position_keys(first, seed, request_id, event, layer, kv_head)
+    if policy == POLICY_RECENCY:
+        return cand.astype(np.uint64)
+    raise ValueError("unknown policy")
+
+
 def drop_set(candidates, keys, m):
     """Indices (into candidates) of the m smallest (key, position) pairs."""
     candidates = np.asarray(candidates)
@@ -88,7 +128,7 @@ def eviction_due(step, n_cached, prompt_len, recent_r, k_keep, every):
 
 
 def evict_head(P, prompt_len, recent_r, k_keep, seed, request_id, event,
-               layer, kv_head):
+               layer, kv_head, policy=POLICY_RANDOM, block=1):
     """One eviction of one (layer, KV head) cache.
 
     P: ascending positions currently cached.  Returns the new ascending
@@ -102,7 +142,8 @@ def evict_head(P, prompt_len, recent_r, k_keep, seed, request_id, event,
     m = cand.shape[0] - k_keep
     if m <= 0:
         return P.copy()
-    keys = position_keys(cand, seed, request_id, event, layer, kv_head)
+    keys = policy_keys(policy, cand, prompt_len, seed, request_id, event,
+                       layer, kv_head, block)
     keep = np.ones(cand.shape[0], dtype=bool)
     keep[drop_set(cand, keys, m)] = False
     return np.concatenate([P[:prompt_len], cand[keep], P[n - recent_r:]])
@@ -116,7 +157,9 @@ class SequenceReplay:
     """
 
     def __init__(self, prompt_len, k_keep, recent_r, every, seed, request_id,
-                 heads):
+                 heads, policy=POLICY_RANDOM, block=1):
+        self.policy = int(policy)
+        self.block = int(block)
         self.lp = int(prompt_len)
         self.k_keep = int(k_keep)
         self.r = int(recent_r)
@@ -153,7 +196,8 @@ class SequenceReplay:
         for (layer, g) in self.heads:
             self.P[(layer, g)] = evict_head(self.P[(layer, g)], self.lp,
                                             self.r, self.k_keep, self.seed,
-                                            self.rid, self.event, layer, g)
+                                            self.rid, self.event, layer, g,
+                                            self.policy, self.block)
         self.log.append((self.step, self.event))
         self.event += 1
         return True

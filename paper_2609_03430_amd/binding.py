@@ -30,6 +30,7 @@ RA_ERR_STATE = -6
 RA_F32, RA_BF16 = 0, 1
 RA_BUDGET_EVICTABLE, RA_BUDGET_TOTAL = 0, 1
 RA_LAYOUT_CHRONOLOGICAL, RA_LAYOUT_HOLE_FILL = 0, 1
+RA_POLICY_RANDOM, RA_POLICY_SHARED, RA_POLICY_BLOCK, RA_POLICY_RECENCY = 0, 1, 2, 3
 
 # Every entry point declared in include/randattn.h.
 EXPORTS = (
@@ -55,7 +56,7 @@ class ra_config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "num_layers", "num_q_heads", "num_kv_heads", "head_dim", "budget_k",
         "recent_r", "evict_every", "budget_mode", "dtype", "max_seqs",
-        "attn_split", "layout")]
+        "attn_split", "layout", "policy", "policy_block")]
 
 
 class ra_seq_info(ctypes.Structure):
@@ -143,10 +144,11 @@ def _stream(stream):
 def make_config(num_layers, num_q_heads, num_kv_heads, budget_k, recent_r=64,
                 evict_every=64, budget_mode=RA_BUDGET_EVICTABLE, dtype=RA_BF16,
                 max_seqs=1, head_dim=128, attn_split=0,
-                layout=RA_LAYOUT_CHRONOLOGICAL):
+                layout=RA_LAYOUT_CHRONOLOGICAL, policy=RA_POLICY_RANDOM,
+                policy_block=1):
     return ra_config(num_layers, num_q_heads, num_kv_heads, head_dim, budget_k,
                      recent_r, evict_every, budget_mode, dtype, max_seqs,
-                     attn_split, layout)
+                     attn_split, layout, policy, policy_block)
 
 
 # ---- one wrapper per C entry point ------------------------------------------

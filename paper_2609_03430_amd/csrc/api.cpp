@@ -62,7 +62,8 @@ struct ra_cache {
 
   ra::Shape shape() const {
     return ra::Shape{cfg.num_layers, cfg.num_q_heads, cfg.num_kv_heads, G,
-                     cfg.recent_r, cfg.evict_every, cfg.dtype, cfg.layout};
+                     cfg.recent_r, cfg.evict_every, cfg.dtype, cfg.layout,
+                     cfg.policy, std::max(1, cfg.policy_block)};
   }
   bool step_open() const { return n_appended != 0; }
   void update_range() {
@@ -168,6 +169,8 @@ ra_status ra_config_check(const ra_config* c) {
       (c->budget_mode != RA_BUDGET_EVICTABLE && c->budget_mode != RA_BUDGET_TOTAL) ||
       (c->dtype != RA_F32 && c->dtype != RA_BF16) || c->num_layers > 4096 ||
       (c->layout != RA_LAYOUT_CHRONOLOGICAL && c->layout != RA_LAYOUT_HOLE_FILL) ||
+      c->policy < RA_POLICY_RANDOM || c->policy > RA_POLICY_RECENCY ||
+      (c->policy == RA_POLICY_BLOCK && c->policy_block < 1) ||
       c->num_kv_heads > 4096)
     return RA_ERR_INVALID_ARG;
   if (c->head_dim != ra::kHeadDim) return RA_ERR_UNSUPPORTED;

@@ -42,6 +42,29 @@ __device__ __forceinline__ int count_le(const int* f, int m, int x) {
   return lo;
 }
 
+// The key whose m smallest values an event drops (ties by position).
+// Random Attention: the per-head uniform draw of position p; the diagnostic
+// policies of the paper change only this key (see ra_policy).
+__device__ __forceinline__ uint64_t policy_key(int policy, int block, int p, int lp,
+                                               int event, int layer, int g,
+                                               uint64_t seed, uint64_t rid) {
+  const uint64_t e = static_cast<uint64_t>(event);
+  switch (policy) {
+    case 1:   // shared draw: the same positions in every (layer, KV head)
+      return philox_score(static_cast<uint64_t>(p), e, 0, 0, seed, rid);
+    case 2: { // block-wise: every position takes the draw of its block's first
+      const int first = lp + (p - lp) / block * block;
+      return philox_score(static_cast<uint64_t>(first), e, static_cast<uint64_t>(layer),
+                          static_cast<uint64_t>(g), seed, rid);
+    }
+    case 3:   // recency: drop the oldest
+      return static_cast<uint64_t>(p);
+    default:
+      return philox_score(static_cast<uint64_t>(p), e, static_cast<uint64_t>(layer),
+                          static_cast<uint64_t>(g), seed, rid);
+  }
+}
+
 // Number of drops d_k (= f[k] + k, ascending) with d_k <= x.
 __device__ __forceinline__ int count_le_slot(const int* f, int m, int x) {
   int lo = 0, hi = m;
@@ -95,7 +118,7 @@ template <int NT, int KPT, typename E, bool POS_ONLY, int LAYOUT>
 __global__ __launch_bounds__(NT) void evict_kernel(
     const SeqMeta* __restrict__ meta, E* __restrict__ kpool,
     E* __restrict__ vpool, int32_t* __restrict__ pos, int L, int Hkv, int r,
-    int slot_lo) {
+    int slot_lo, int policy, int block) {
   static_assert(KPT <= 32, "drop flags live in one 32-bit mask");
   constexpr int kEpu = 16 / sizeof(E);            // elements per 16-byte unit
   constexpr int kKUnitsRow = kHeadDim / kEpu;     // 16-byte units per key row
@@ -143,9 +166,7 @@ __global__ __launch_bounds__(NT) void evict_kernel(
     if (c < span) {
       const int p = P[lp + c];
       if (p < thr) {
-        score[i] = philox_score(static_cast<uint64_t>(p), static_cast<uint64_t>(event),
-                                static_cast<uint64_t>(layer), static_cast<uint64_t>(g),
-                                seed, rid);
+        score[i] = policy_key(policy, block, p, lp, event, layer, g, seed, rid);
         tie[i] = static_cast<uint32_t>(p);
         valid |= 1u << i;
       }
@@ -289,12 +310,12 @@ hipError_t launch_layout(const Shape& sh, const SeqMeta* meta, void* kpool,
     hipLaunchKernelGGL((evict_kernel<NT, KPT, uint16_t, POS_ONLY, LAYOUT>), grid,
                        dim3(NT), 0, s, meta, static_cast<uint16_t*>(kpool),
                        static_cast<uint16_t*>(vpool), pos, sh.L, sh.Hkv, sh.r,
-                       slot_lo);
+                       slot_lo, sh.policy, sh.block);
   } else {
     hipLaunchKernelGGL((evict_kernel<NT, KPT, float, POS_ONLY, LAYOUT>), grid,
                        dim3(NT), 0, s, meta, static_cast<float*>(kpool),
                        static_cast<float*>(vpool), pos, sh.L, sh.Hkv, sh.r,
-                       slot_lo);
+                       slot_lo, sh.policy, sh.block);
   }
   return hipGetLastError();
 }

@@ -46,6 +46,8 @@ static_assert(sizeof(SeqMeta) == 64, "SeqMeta must stay 64 bytes");
 struct Shape {
   int L, Hq, Hkv, G, r, every, dtype;  // dtype: 0 f32, 1 bf16
   int layout;                          // 0 chronological, 1 hole-fill
+  int policy;                          // ra_policy
+  int block;                           // tokens per block (block policy)
 };
 
 // ---- launch wrappers (defined in the .hip files) ----------------------------

@@ -27,7 +27,8 @@ class Run:
                  mode=B.RA_BUDGET_EVICTABLE, seeds=None, rids=None,
                  scaled=True, wl_seed=1000, ring=None, attn_split=0,
                  max_seqs=None, write_prompt=True, begin=True,
-                 layout=B.RA_LAYOUT_CHRONOLOGICAL):
+                 layout=B.RA_LAYOUT_CHRONOLOGICAL, policy=B.RA_POLICY_RANDOM,
+                 block=1):
         self.L, self.Hq, self.Hkv, self.K, self.r, self.every = L, Hq, Hkv, K, r, every
         self.G = Hq // Hkv
         self.lps = list(lps)
@@ -39,8 +40,10 @@ class Run:
         self.mode = mode
         self.tdtype = torch.bfloat16 if dtype == B.RA_BF16 else torch.float32
         self.layout = layout
+        self.policy, self.block = policy, block
         self.cfg = B.make_config(L, Hq, Hkv, K, r, every, mode, dtype, self.max_seqs,
-                                 attn_split=attn_split, layout=layout)
+                                 attn_split=attn_split, layout=layout, policy=policy,
+                                 policy_block=block)
         rows = sum(B.ra_seq_rows(self.cfg, lp) for lp in self.lps)
         self.cache = B.Cache(self.cfg, rows)
         self.h = self.cache.handle
@@ -160,7 +163,8 @@ class OracleSeq:
         self.rid = run.rids[slot]
         self.heads = heads or [(l, g) for l in range(run.L) for g in range(run.Hkv)]
         self.rep = SequenceReplay(self.lp, run.k_keep(slot), run.r, run.every,
-                                  run.seeds[slot], self.rid, self.heads)
+                                  run.seeds[slot], self.rid, self.heads,
+                                  policy=run.policy, block=run.block)
         self.wl = run.wl.to("cpu")
 
     def advance(self, n):

@@ -109,6 +109,66 @@ def test_fast_forward_and_evict_now(lp, K, r, every, mode, layout):
     run.close()
 
 
+POLICIES = [(B.RA_POLICY_SHARED, 1), (B.RA_POLICY_BLOCK, 4), (B.RA_POLICY_BLOCK, 64),
+            (B.RA_POLICY_RECENCY, 1)]
+
+
+@pytest.mark.parametrize("layout", [B.RA_LAYOUT_CHRONOLOGICAL, B.RA_LAYOUT_HOLE_FILL])
+@pytest.mark.parametrize("policy,block", POLICIES)
+def test_policy_decode_parity(policy, block, layout):
+    """The diagnostic policies (shared draw, block-wise, recency + prompt):
+    same kept sets, rows and attention outputs as the oracle."""
+    log("policy decode parity policy=%d block=%d layout=%d" % (policy, block, layout))
+    run = Run(L=2, Hq=4, Hkv=2, K=40, lps=[5, 0, 17], r=8, every=8, layout=layout,
+              policy=policy, block=block)
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    worst, events = 0.0, 0
+    for t in range(120):
+        outs, ev = run.step()
+        outs = outs.float().cpu()
+        for o in oracles:
+            o.rep.append()
+            for layer in range(run.L):
+                err = max_abs(outs[layer, o.slot], o.attend(layer, t))
+                worst = max(worst, err)
+                assert err <= TOL[B.RA_BF16], (t, o.slot, layer, err)
+            o.rep.end_step()
+        if ev:
+            events += 1
+            _check_heads(run, oracles)
+    log("  events=%d worst=%.3g" % (events, worst))
+    assert events >= 8
+    run.close()
+
+
+@pytest.mark.parametrize("layout", [B.RA_LAYOUT_CHRONOLOGICAL, B.RA_LAYOUT_HOLE_FILL])
+@pytest.mark.parametrize("policy,block", POLICIES + [(B.RA_POLICY_BLOCK, 16)])
+def test_policy_large_select(policy, block, layout):
+    """8256 candidates per head (the 1024-thread select): kept sets after a
+    fast forward and an explicit event, with rows compacted exactly."""
+    log("policy large select policy=%d block=%d layout=%d" % (policy, block, layout))
+    run = Run(L=2, Hq=2, Hkv=2, K=8192, lps=[129, 40], r=64, every=64, layout=layout,
+              policy=policy, block=block, seeds=[2**63 + 11, 5], rids=[2**40 + 1, 9])
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    n = 8192 + 3 * 64 + 17
+    run.fast_forward(n)
+    for o in oracles:
+        o.advance(n)
+    _check_heads(run, oracles, rows=False)
+    for s in range(run.n):
+        run.materialise(s)
+    for _ in range(5):
+        run.step()
+        for o in oracles:
+            o.rep.append()
+            o.rep.end_step()
+    for s in range(run.n):
+        B.ra_evict_now(run.h, s)
+        oracles[s].rep.evict_now()
+    _check_heads(run, oracles, rows=True)
+    run.close()
+
+
 def test_batching_invariance():
     """A request keeps the same sets alone in slot 0 and inside a batch in
     slot 3 (the scores depend on the request, not on the memory slot)."""
