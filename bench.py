@@ -269,7 +269,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=64)
     ap.add_argument("--workload", default="qwen3-14b", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-steps", type=int, default=96)
+    ap.add_argument("--cpu-steps", type=int, default=384,
+                    help="decode steps of the oracle's timed sample (about 10 s)")
     ap.add_argument("--attn-split", type=int, default=0)
     ap.add_argument("--layout", default="chronological",
                     choices=["chronological", "holefill"],
@@ -385,8 +386,9 @@ def main():
             v_ring[j, l] = v
     out = torch.empty(Bsz, Hq, 128, dtype=torch.bfloat16, device=dev)
     torch.cuda.synchronize()
-    split_keys, max_splits = B.ra_attention_plan(h)
-    log("inputs ready; attention split %d keys x %d" % (split_keys, max_splits))
+    split_keys, max_splits, waves = B.ra_attention_plan(h)
+    log("inputs ready; attention split %d keys x %d, %d wavefronts per item"
+        % (split_keys, max_splits, waves))
 
     def run_steps(first, n, timed):
         # HIP events bracket each step's L attention launches (one pair per
@@ -509,6 +511,8 @@ def main():
             "global_batch": Bsz,
             "seq_len": max(lp + st + total for lp, st in zip(lps, starts)),
             "attn_split_keys": split_keys,
+            "attn_splits": max_splits,
+            "attn_waves_per_item": waves,
         },
         "roofline": {
             "bound": "hbm",
@@ -537,9 +541,9 @@ def main():
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
-        # sequence 0, a 96-step sample ending 192 steps before its last step
-        # (96 > 64, so the sample contains an eviction event)
-        c0 = starts[0] + total - 288
+        # sequence 0, a sample of its last cpu_steps steps (> 64 steps, so
+        # the sample contains eviction events)
+        c0 = starts[0] + total - args.cpu_steps
         result["cpu_baseline"] = cpu_baseline(w, seed, lps[0], c0, args.cpu_steps)
     print(json.dumps(result), flush=True)
 

@@ -286,10 +286,11 @@ const char* ra_status_string(int32_t status);
 /* hipError_t of the last failed HIP call in this process (0 if none). */
 int32_t ra_last_hip_error(void);
 
-/* Keys per attention work item and work items per head that the next
- * ra_decode_attention launch uses (host mirror; for measurement). */
+/* Keys per attention work item, work items per head and wavefronts per work
+ * item that the next ra_decode_attention launch uses (host mirror; for
+ * measurement and tests).  `waves` may be NULL. */
 ra_status ra_attention_plan(const ra_cache* cache, int32_t* split_keys,
-                            int32_t* max_splits);
+                            int32_t* max_splits, int32_t* waves);
 
 #ifdef __cplusplus
 }

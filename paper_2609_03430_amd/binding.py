@@ -95,7 +95,8 @@ _SIGS = {
                                  ctypes.POINTER(_I32), _P]),
     "ra_status_string": (ctypes.c_char_p, [_I32]),
     "ra_last_hip_error": (_I32, []),
-    "ra_attention_plan": (_I32, [_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32)]),
+    "ra_attention_plan": (_I32, [_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32),
+                                 ctypes.POINTER(_I32)]),
     "ra_window_select": (_I32, [_P, _I32, _I32, _P, _P, _I32, _P, _P]),
 }
 
@@ -279,10 +280,11 @@ def ra_window_select(handle, seq_lo, seq_hi, q_window, scores=None, scores_strid
 
 
 def ra_attention_plan(handle):
-    sk, ms = ctypes.c_int32(0), ctypes.c_int32(0)
-    _check(_lib().ra_attention_plan(handle, ctypes.byref(sk), ctypes.byref(ms)),
-           "ra_attention_plan")
-    return sk.value, ms.value
+    """(split_keys, max_splits, waves) of the next attention launch."""
+    sk, ms, w = ctypes.c_int32(0), ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(_lib().ra_attention_plan(handle, ctypes.byref(sk), ctypes.byref(ms),
+                                    ctypes.byref(w)), "ra_attention_plan")
+    return sk.value, ms.value, w.value
 
 
 # ---- owner of the device buffers ----------------------------------------------

@@ -114,7 +114,24 @@ void mirror_plan(SeqMeta& M, int r, bool at_trigger) {
 //  - fp32: one wavefront per (head, split), ~1024 work items.
 // cfg.attn_split > 0 fixes the keys per work item (rounded up to a multiple
 // of 32 per wavefront).
-void attention_plan(const ra_cache* c, int* split_keys, int* max_splits, int* waves) {
+// Launch plan of the decode attention (measured on the workloads' shapes).
+// A bf16 work item is one (sequence, KV head, split) on a workgroup of W
+// wavefronts, each streaming a contiguous W-th of the split's keys.  The
+// chip has 256 CUs: with at most 256 heads, the heads are split so that
+// about 256 workgroups run, one per CU, and W is the largest of 12, 8, 4
+// that leaves each wavefront a long enough run of keys (12 or 8
+// wavefronts keep 3 or 2 per SIMD in flight; a short run per wavefront
+// costs more in prologue than the extra wavefronts gain).  With many more
+// heads than CUs the workgroups run in several waves of dispatch, and 4
+// wavefronts built for one wavefront per SIMD (accumulators in the
+// accumulation registers) stream best; between 256 and 768 heads the 4-
+// wavefront build that fits three workgroups per CU keeps every head
+// resident at once.  fp32 (VALU): one wavefront per item, about 1024 items.
+struct Plan {
+  int split_keys, max_splits, waves, wide_regs;
+};
+
+Plan attention_plan(const ra_cache* c) {
   int cap_max = 32, n_active = 0;
   for (int s = c->slot_lo; s < c->slot_hi; ++s) {
     if (!c->mirror[s].active) continue;
@@ -122,23 +139,31 @@ void attention_plan(const ra_cache* c, int* split_keys, int* max_splits, int* wa
     ++n_active;
   }
   const int heads = std::max(1, n_active * c->cfg.num_kv_heads);
-  const int target = 1024;
-  int w = 1;
-  if (c->cfg.dtype == RA_BF16)
-    while (w < 4 && heads * w * 2 <= target) w *= 2;
-  const int unit = 32 * w;
-  int sk;
-  if (c->cfg.attn_split > 0) {
-    sk = static_cast<int>(round_up(c->cfg.attn_split, unit));
+  Plan p{0, 0, 1, 0};
+  int splits = 1;
+  if (c->cfg.dtype == RA_BF16) {
+    if (heads >= 768) {
+      p.waves = 4;
+      p.wide_regs = 1;
+    } else if (heads > 256) {
+      p.waves = 4;
+    } else {
+      splits = std::max(1, (256 + heads / 2) / heads);
+      const int keys = (cap_max + splits - 1) / splits;
+      p.waves = keys >= 12 * 640 ? 12 : keys >= 8 * 256 ? 8 : keys >= 4 * 128 ? 4 : 1;
+      p.wide_regs = p.waves == 4;
+    }
   } else {
-    const int per_head = (target + heads - 1) / heads;          // wavefronts per head
-    const int splits = std::min(ra::kMaxSplits, std::max(1, (per_head + w - 1) / w));
-    sk = static_cast<int>(round_up((cap_max + splits - 1) / splits, unit));
+    splits = (1024 + heads - 1) / heads;
   }
+  splits = std::min(ra::kMaxSplits, splits);
+  const int unit = 32 * p.waves;
+  int sk = c->cfg.attn_split > 0 ? static_cast<int>(round_up(c->cfg.attn_split, unit))
+                                 : static_cast<int>(round_up((cap_max + splits - 1) / splits, unit));
   sk = std::max<int>(sk, static_cast<int>(round_up((cap_max + ra::kMaxSplits - 1) / ra::kMaxSplits, unit)));
-  *split_keys = sk;
-  *max_splits = (cap_max + sk - 1) / sk;
-  *waves = w;
+  p.split_keys = sk;
+  p.max_splits = (cap_max + sk - 1) / sk;
+  return p;
 }
 
 }  // namespace
@@ -274,12 +299,13 @@ ra_status ra_get_seq_info(const ra_cache* c, int32_t seq, ra_seq_info* out) {
   return RA_OK;
 }
 
-ra_status ra_attention_plan(const ra_cache* c, int32_t* split_keys, int32_t* max_splits) {
+ra_status ra_attention_plan(const ra_cache* c, int32_t* split_keys, int32_t* max_splits,
+                            int32_t* waves) {
   if (!c || !split_keys || !max_splits) return RA_ERR_INVALID_ARG;
-  int sk, ms, w;
-  attention_plan(c, &sk, &ms, &w);
-  *split_keys = sk;
-  *max_splits = ms;
+  const Plan p = attention_plan(c);
+  *split_keys = p.split_keys;
+  *max_splits = p.max_splits;
+  if (waves) *waves = p.waves;
   return RA_OK;
 }
 
@@ -364,8 +390,7 @@ ra_status ra_decode_attention(ra_cache* c, int32_t layer, const void* q,
   c->appended[layer] = 1;
   ++c->n_appended;
   if (c->slot_hi <= c->slot_lo) return RA_OK;
-  int sk, ms, waves;
-  attention_plan(c, &sk, &ms, &waves);
+  const Plan plan = attention_plan(c);
   const size_t G = static_cast<size_t>(c->G);
   const size_t items = static_cast<size_t>(c->cfg.max_seqs) * c->cfg.num_kv_heads * ra::kMaxSplits;
   float* ws = static_cast<float*>(workspace);
@@ -382,9 +407,10 @@ ra_status ra_decode_attention(ra_cache* c, int32_t layer, const void* q,
   a.ws_ml = ws + items * G * ra::kHeadDim;
   a.layer = layer;
   a.max_seqs = c->slot_hi;
-  a.split_keys = sk;
-  a.max_splits = ms;
-  a.waves = waves;
+  a.split_keys = plan.split_keys;
+  a.max_splits = plan.max_splits;
+  a.waves = plan.waves;
+  a.wide_regs = plan.wide_regs;
   const hipError_t e = ra::launch_attention(c->shape(), a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) {
     c->appended[layer] = 0;

@@ -282,9 +282,11 @@ __device__ __forceinline__ void compute_block(Softmax& st, const BlockRegs& b,
 // wavefront v takes the v-th W-th of the split's keys, and the wavefronts
 // merge their online-softmax states in LDS at the end.  When the
 // head needs a single split, the workgroup writes the normalised output
-// itself and no merge kernel runs.
-template <int W>
-__global__ __launch_bounds__(64 * W, W == 1 ? 2 : 1) void attn_bf16_kernel(
+// itself and no merge kernel runs.  MINW is the number of wavefronts per
+// SIMD the build must allow (1 lets the accumulators live in the
+// accumulation registers, 2 keeps each wavefront within 256 registers).
+template <int W, int MINW>
+__global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
     AttnLaunch a, int G, int Hq, int Hkv, float scale_log2) {
   constexpr int kNBuf = 2;   // register buffers (3 or 4 measured no faster)
   __shared__ float s_m[W][kMaxGroup];
@@ -572,15 +574,23 @@ hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s)
   const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(kHeadDim));
   const dim3 cgrid(sh.Hkv, a.max_seqs);
   if (sh.dtype == 1) {
-    if (a.waves == 4)
-      hipLaunchKernelGGL(attn_bf16_kernel<4>, grid, dim3(256), 0, s, a, sh.G, sh.Hq,
+    if (a.waves == 12)
+      hipLaunchKernelGGL((attn_bf16_kernel<12, 1>), grid, dim3(768), 0, s, a, sh.G, sh.Hq,
                          sh.Hkv, scale_log2);
-    else if (a.waves == 2)
-      hipLaunchKernelGGL(attn_bf16_kernel<2>, grid, dim3(128), 0, s, a, sh.G, sh.Hq,
+    else if (a.waves == 8)
+      hipLaunchKernelGGL((attn_bf16_kernel<8, 1>), grid, dim3(512), 0, s, a, sh.G, sh.Hq,
+                         sh.Hkv, scale_log2);
+    else if (a.waves == 4 && a.wide_regs)
+      hipLaunchKernelGGL((attn_bf16_kernel<4, 1>), grid, dim3(256), 0, s, a, sh.G, sh.Hq,
+                         sh.Hkv, scale_log2);
+    else if (a.waves == 4)
+      hipLaunchKernelGGL((attn_bf16_kernel<4, 2>), grid, dim3(256), 0, s, a, sh.G, sh.Hq,
+                         sh.Hkv, scale_log2);
+    else if (a.waves == 1)
+      hipLaunchKernelGGL((attn_bf16_kernel<1, 2>), grid, dim3(64), 0, s, a, sh.G, sh.Hq,
                          sh.Hkv, scale_log2);
     else
-      hipLaunchKernelGGL(attn_bf16_kernel<1>, grid, dim3(64), 0, s, a, sh.G, sh.Hq,
-                         sh.Hkv, scale_log2);
+      return hipErrorInvalidConfiguration;
     if (a.max_splits > 1)
       hipLaunchKernelGGL(combine_kernel<uint16_t>, cgrid, dim3(256), 0, s, a, sh.G,
                          sh.Hq, sh.Hkv, true);

@@ -89,7 +89,8 @@ struct AttnLaunch {
   int max_seqs;
   int split_keys;
   int max_splits;
-  int waves;           // wavefronts per work item (bf16 path: 1 or 4)
+  int waves;           // wavefronts per work item (bf16 path: 1, 4, 8 or 12)
+  int wide_regs;       // bf16, 4 wavefronts: the build for one wavefront per SIMD
 };
 hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s);
 

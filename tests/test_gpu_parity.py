@@ -169,6 +169,57 @@ def test_policy_large_select(policy, block, layout):
     run.close()
 
 
+# (tag, KV heads, group, batch, K, wavefronts per item the plan must pick)
+PLAN_CASES = [
+    ("12 wavefronts, 1 split", 8, 2, 25, 7600, 12),
+    ("8 wavefronts, 2 splits", 8, 2, 16, 4000, 8),
+    ("4 wavefronts, 4 splits", 4, 2, 16, 2000, 4),
+    ("320 heads", 8, 2, 40, 600, 4),
+    ("800 heads", 8, 1, 100, 300, 4),
+]
+
+
+@pytest.mark.parametrize("tag,Hkv,G,Bsz,K,waves", PLAN_CASES)
+def test_attention_plans(tag, Hkv, G, Bsz, K, waves):
+    """Each branch of the attention launch plan, on a ragged batch (prompts
+    and generated lengths differ per sequence): every query head of every
+    sequence against the oracle for two steps, the second after the
+    sequences that were due have evicted."""
+    log("attention plan: %s" % tag)
+    rng = np.random.default_rng(Bsz * 31 + K)
+    lps = rng.integers(0, 300, Bsz).tolist()
+    gens = sorted(rng.integers(K + 70, K + 700, Bsz).tolist(), reverse=True)
+    run = Run(L=1, Hq=Hkv * G, Hkv=Hkv, K=K, lps=lps, r=64, every=64, begin=False,
+              write_prompt=False, wl_seed=77)
+    for b in range(Bsz):
+        run.begin(b)
+        nxt = gens[b + 1] if b + 1 < Bsz else 0
+        if gens[b] > nxt:
+            run.fast_forward(gens[b] - nxt)
+    for b in range(Bsz):
+        run.materialise(b)
+    _, _, w = B.ra_attention_plan(run.h)
+    assert w == waves, (tag, w)
+    oracles = [OracleSeq(run, b, heads=[(0, g) for g in range(Hkv)]) for b in range(Bsz)]
+    for b, o in enumerate(oracles):
+        o.advance(gens[b])
+    worst = 0.0
+    for i in range(66):
+        outs, _ = run.step()
+        check = i in (0, 65)
+        if check:
+            outs = outs.float().cpu()
+        for b, o in enumerate(oracles):
+            o.rep.append()
+            if check:
+                err = max_abs(outs[0, b], o.attend(0, gens[b] + i))
+                worst = max(worst, err)
+                assert err <= TOL[B.RA_BF16], (tag, i, b, err)
+            o.rep.end_step()
+    log("  worst %.3g" % worst)
+    run.close()
+
+
 def test_batching_invariance():
     """A request keeps the same sets alone in slot 0 and inside a batch in
     slot 3 (the scores depend on the request, not on the memory slot)."""
