@@ -148,7 +148,7 @@ def cpu_baseline(w, seed, lp, t0, steps):
     }
 
 
-def evict_cost(B, torch, Workload):
+def evict_cost(B, torch, Workload, methods=("random", "snapkv")):
     """Per-layer eviction-round time of a single decoding sequence.
 
     The paper times one eviction round (scoring + compaction) per layer with
@@ -156,60 +156,81 @@ def evict_cost(B, torch, Workload):
     table).  Here: the Qwen3-4B and Qwen3-14B attention shapes, one sequence,
     budget K=1024 counting the prompt (Eq. 1), prompt 300, r=64, every 64:
     52 events in 4096 steps, i.e. 1872 / 2080 per-layer rounds, the paper's
-    call counts.  One event covers every layer in one launch; per-layer time =
-    event time / layers.  Decode time = all attention launches + events.
+    call counts.  One event covers every layer; per-layer time = event time /
+    layers.  Decode time = all attention launches + end-of-step work.
+    Random Attention evicts at the end of the step; the score-based rounds
+    (external policy) run right after it on the same steps, scored on the
+    queries of the last 64 steps, and their time includes that end of step.
     """
     dev = torch.device("cuda:0")
     stream = torch.cuda.current_stream()
-    res = {"metric": "eviction round ms per layer (random sampler + compaction)",
+    scorers = {"snapkv": B.RA_SCORER_SNAPKV, "rkv": B.RA_SCORER_RKV,
+               "vase": B.RA_SCORER_VASE}
+    res = {"metric": "eviction round ms per layer (scoring + selection + compaction)",
            "protocol": "1 sequence, K=1024 incl. prompt 300, r=64, every 64, 4096 "
                        "decode steps from the prompt, HIP events", "shapes": {}}
     for name, (L, Hq, Hkv) in (("qwen3-4b", (36, 32, 8)), ("qwen3-14b", (40, 40, 8))):
         lp, K, steps = 300, 1024, 4096
-        cfg = B.make_config(L, Hq, Hkv, K, R, EVERY, B.RA_BUDGET_TOTAL, B.RA_BF16, 1)
-        cache = B.Cache(cfg, B.ra_seq_rows(cfg, lp), device=dev)
-        h = cache.handle
         wl = Workload(2000, L, Hq, Hkv, 128, torch.bfloat16, True, ring=RING, device=dev)
         ls = torch.arange(L, device=dev).view(-1, 1, 1)
         gs = torch.arange(Hkv, device=dev).view(1, -1, 1)
         ps = torch.arange(lp, device=dev).view(1, 1, -1)
-        B.ra_seq_begin(h, 0, lp, 77, 0, wl.k_rows(0, ls, gs, ps, lp).contiguous(),
-                       wl.v_rows(0, ls, gs, ps, lp).contiguous())
+        kp = wl.k_rows(0, ls, gs, ps, lp).contiguous()
+        vp = wl.v_rows(0, ls, gs, ps, lp).contiguous()
         qs = torch.stack([torch.stack([wl.q_step([0], l, [j]) for l in range(L)])
-                          for j in range(RING)])
+                          for j in range(RING)])              # [64][L][1][Hq][128]
+        # window row w of an event at a multiple of 64 steps is ring slot w
+        qwin = qs.permute(2, 1, 3, 0, 4).contiguous()          # [1][L][Hq][64][128]
         kv = [[wl.kv_step([0], l, [lp + j], [lp]) for l in range(L)] for j in range(RING)]
         out = torch.empty(1, Hq, 128, dtype=torch.bfloat16, device=dev)
-        torch.cuda.synchronize()
-        ev, dec = [], []
-        for t in range(steps):
-            j = t % RING
-            a0 = torch.cuda.Event(enable_timing=True)
-            a1 = torch.cuda.Event(enable_timing=True)
-            a0.record(stream)
-            for l in range(L):
-                B.ra_decode_attention(h, l, qs[j, l], kv[j][l][0], kv[j][l][1], out,
-                                      cache.workspace, stream)
-            a1.record(stream)
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            n = B.ra_end_step(h, stream)
-            e1.record(stream)
-            dec.append((a0, a1))
-            if n:
-                ev.append((e0, e1))
-        torch.cuda.synchronize()
-        ev_ms = [a.elapsed_time(b) for a, b in ev]
-        dec_ms = sum(a.elapsed_time(b) for a, b in dec) + sum(ev_ms)
-        res["shapes"][name] = {
-            "layers": L, "kv_heads": Hkv, "events": len(ev_ms),
-            "per_layer_rounds": len(ev_ms) * L,
-            "ms_per_event_all_layers": sum(ev_ms) / len(ev_ms),
-            "ms_per_layer_round": sum(ev_ms) / len(ev_ms) / L,
-            "percent_of_decode": 100.0 * sum(ev_ms) / dec_ms,
-        }
-        cache.close()
-        torch.cuda.empty_cache()
+        res["shapes"][name] = {"layers": L, "kv_heads": Hkv}
+        for method in methods:
+            scored = method != "random"
+            policy = B.RA_POLICY_EXTERNAL if scored else B.RA_POLICY_RANDOM
+            cfg = B.make_config(L, Hq, Hkv, K, R, EVERY, B.RA_BUDGET_TOTAL, B.RA_BF16, 1,
+                                policy=policy)
+            cache = B.Cache(cfg, B.ra_seq_rows(cfg, lp), device=dev)
+            h = cache.handle
+            B.ra_seq_begin(h, 0, lp, 77, 0, kp, vp)
+            if scored:
+                prm = B.make_scorer(scorers[method], vase_seed=99)
+                scratch = torch.empty(B.ra_scored_scratch_bytes(cfg, lp) // 4 + 1,
+                                      dtype=torch.int32, device=dev)
+            torch.cuda.synchronize()
+            ev, dec = [], []
+            for t in range(steps):
+                j = t % RING
+                a0 = torch.cuda.Event(enable_timing=True)
+                a1 = torch.cuda.Event(enable_timing=True)
+                a0.record(stream)
+                for l in range(L):
+                    B.ra_decode_attention(h, l, qs[j, l], kv[j][l][0], kv[j][l][1], out,
+                                          cache.workspace, stream)
+                a1.record(stream)
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                n = B.ra_end_step(h, stream)
+                if scored and (t + 1) % EVERY == 0:
+                    info = B.ra_get_seq_info(h, 0)
+                    if info.len - R > K:
+                        B.ra_scored_evict(h, 0, 1, prm, qwin, scratch, stream)
+                        n = 1
+                e1.record(stream)
+                dec.append((a0, a1))
+                (ev if n else dec).append((e0, e1))
+            torch.cuda.synchronize()
+            ev_ms = [a.elapsed_time(b) for a, b in ev]
+            dec_ms = sum(a.elapsed_time(b) for a, b in dec) + sum(ev_ms)
+            res["shapes"][name][method] = {
+                "events": len(ev_ms),
+                "per_layer_rounds": len(ev_ms) * L,
+                "ms_per_event_all_layers": sum(ev_ms) / len(ev_ms),
+                "ms_per_layer_round": sum(ev_ms) / len(ev_ms) / L,
+                "percent_of_decode": 100.0 * sum(ev_ms) / dec_ms,
+            }
+            cache.close()
+            torch.cuda.empty_cache()
     return res
 
 
@@ -285,6 +306,9 @@ def main():
                     help="eviction-round cost of one sequence at K=1024 (budget counting "
                          "the prompt, prompt 300) over 4096 decode steps, as in the "
                          "paper's eviction-cost table; prints its own JSON line")
+    ap.add_argument("--evict-cost-methods", default="random,snapkv",
+                    help="comma-separated rounds timed by --evict-cost: random and the "
+                         "score-based snapkv, rkv, vase")
     ap.add_argument("--window-scorer", action="store_true",
                     help="also time the observation-window scoring pass (always on for "
                          "phi4-ragged)")
@@ -312,7 +336,8 @@ def main():
         return
 
     if args.evict_cost:
-        print(json.dumps(evict_cost(B, torch, Workload)), flush=True)
+        print(json.dumps(evict_cost(B, torch, Workload, tuple(args.evict_cost_methods.split(",")))),
+              flush=True)
         return
 
     w = WORKLOADS[args.workload]

@@ -115,10 +115,42 @@ typedef enum {
                              position takes the draw of its block's first
                              position (blocks aligned at the prompt end), so
                              policy_block = 1 is RA_POLICY_RANDOM */
-  RA_POLICY_RECENCY = 3   /* recency+prompt (Section 4.1): the prompt plus the
+  RA_POLICY_RECENCY = 3,  /* recency+prompt (Section 4.1): the prompt plus the
                              contiguous recent window -- the oldest candidates
                              are dropped, no draw */
+  RA_POLICY_EXTERNAL = 4  /* no eviction at the end of a step: the caller runs
+                             score-based rounds with ra_scored_evict (used to
+                             price the selection signal, not by the method) */
 } ra_policy;
+
+/* Score-based evictors of Section 2 ("Baselines as choices of s"), run only
+ * to measure what Random Attention saves.  Every cached row outside the r
+ * most recent is a candidate (the prompt competes, as in those methods), and
+ * a round keeps lp + k_keep of them. */
+typedef enum {
+  RA_SCORER_SNAPKV = 0,   /* sum of the attention weights of the last 64
+                             queries of the group's query heads, max-pooled
+                             over 7 neighbouring rows; the lowest are dropped */
+  RA_SCORER_RKV = 1,      /* lambda * SnapKV - (1 - lambda) * softmax(c), c_i
+                             the mean cosine similarity of key i to the other
+                             cached keys, its `rkv_recent_dups` most recent
+                             near-duplicates (cosine > rkv_threshold) not
+                             counted */
+  RA_SCORER_VASE = 2      /* keep the vase_n_large rows of largest value range
+                             (max - min over channels), fill the rest of the
+                             budget by sampling without replacement with
+                             probability proportional to the SnapKV score */
+} ra_scorer;
+
+typedef struct {
+  int32_t scorer;          /* ra_scorer */
+  float rkv_lambda;        /* R-KV weight of the SnapKV term, in [0, 1] */
+  float rkv_threshold;     /* R-KV near-duplicate cosine threshold */
+  int32_t rkv_recent_dups; /* R-KV near-duplicates not counted (>= 0) */
+  int32_t vase_n_large;    /* VaSE rows kept by value range (< 0: half the
+                              kept budget) */
+  uint64_t vase_seed;      /* VaSE: seed of the proportional fill's draws */
+} ra_scorer_params;
 
 typedef struct ra_cache ra_cache;   /* host-side descriptor + host mirror */
 
@@ -278,6 +310,24 @@ ra_status ra_read_positions(ra_cache* cache, int32_t seq, int32_t layer,
 ra_status ra_window_select(ra_cache* cache, int32_t seq_lo, int32_t seq_hi,
                            const void* dev_q_window, float* dev_scores,
                            int32_t scores_stride, int32_t* dev_drops, void* stream);
+
+/* Bytes of device scratch ra_scored_evict needs for a cache whose longest
+ * prompt is max_prompt_len (0 on an invalid config). */
+size_t ra_scored_scratch_bytes(const ra_config* cfg, int32_t max_prompt_len);
+
+/* One score-based eviction round (scoring + selection + compaction) for every
+ * active sequence in [seq_lo, seq_hi) whose rows outside the r most recent
+ * exceed lp + k_keep; the others are left as they are.  dev_q_window is
+ * [max_seqs][L][Hq][64][128] bf16: the queries of each sequence's last 64
+ * decode steps, oldest first.  The kept rows stay in chronological order;
+ * len becomes lp + k_keep + r.  bf16 and the chronological layout only
+ * (RA_ERR_UNSUPPORTED otherwise); RA_ERR_STATE inside an open step, before
+ * step 64 or when a sequence has more than evict_every rows over its
+ * budget; RA_ERR_INVALID_ARG on a bad parameter or a scratch smaller than
+ * ra_scored_scratch_bytes.  Asynchronous on `stream`. */
+ra_status ra_scored_evict(ra_cache* cache, int32_t seq_lo, int32_t seq_hi,
+                          const ra_scorer_params* params, const void* dev_q_window,
+                          void* dev_scratch, size_t scratch_bytes, void* stream);
 
 /* ---- diagnostics ----------------------------------------------------------- */
 

@@ -31,6 +31,8 @@ RA_F32, RA_BF16 = 0, 1
 RA_BUDGET_EVICTABLE, RA_BUDGET_TOTAL = 0, 1
 RA_LAYOUT_CHRONOLOGICAL, RA_LAYOUT_HOLE_FILL = 0, 1
 RA_POLICY_RANDOM, RA_POLICY_SHARED, RA_POLICY_BLOCK, RA_POLICY_RECENCY = 0, 1, 2, 3
+RA_POLICY_EXTERNAL = 4
+RA_SCORER_SNAPKV, RA_SCORER_RKV, RA_SCORER_VASE = 0, 1, 2
 
 # Every entry point declared in include/randattn.h.
 EXPORTS = (
@@ -40,6 +42,7 @@ EXPORTS = (
     "ra_end_step", "ra_evict_now", "ra_fast_forward", "ra_export_positions",
     "ra_write_rows", "ra_read_rows", "ra_read_positions", "ra_status_string",
     "ra_last_hip_error", "ra_attention_plan", "ra_window_select",
+    "ra_scored_scratch_bytes", "ra_scored_evict",
 )
 
 
@@ -57,6 +60,18 @@ class ra_config(ctypes.Structure):
         "num_layers", "num_q_heads", "num_kv_heads", "head_dim", "budget_k",
         "recent_r", "evict_every", "budget_mode", "dtype", "max_seqs",
         "attn_split", "layout", "policy", "policy_block")]
+
+
+class ra_scorer_params(ctypes.Structure):
+    _fields_ = [("scorer", ctypes.c_int32), ("rkv_lambda", ctypes.c_float),
+                ("rkv_threshold", ctypes.c_float), ("rkv_recent_dups", ctypes.c_int32),
+                ("vase_n_large", ctypes.c_int32), ("vase_seed", ctypes.c_uint64)]
+
+
+def make_scorer(scorer, rkv_lambda=0.1, rkv_threshold=0.9, rkv_recent_dups=1,
+                vase_n_large=-1, vase_seed=0):
+    return ra_scorer_params(scorer, rkv_lambda, rkv_threshold, rkv_recent_dups,
+                            vase_n_large, vase_seed)
 
 
 class ra_seq_info(ctypes.Structure):
@@ -98,6 +113,8 @@ _SIGS = {
     "ra_attention_plan": (_I32, [_P, ctypes.POINTER(_I32), ctypes.POINTER(_I32),
                                  ctypes.POINTER(_I32)]),
     "ra_window_select": (_I32, [_P, _I32, _I32, _P, _P, _I32, _P, _P]),
+    "ra_scored_scratch_bytes": (ctypes.c_size_t, [_P, _I32]),
+    "ra_scored_evict": (_I32, [_P, _I32, _I32, _P, _P, _P, ctypes.c_size_t, _P]),
 }
 
 _handle = None
@@ -277,6 +294,18 @@ def ra_window_select(handle, seq_lo, seq_hi, q_window, scores=None, scores_strid
     _check(_lib().ra_window_select(handle, int(seq_lo), int(seq_hi), _ptr(q_window),
                                    _ptr(scores), int(scores_stride), _ptr(drops),
                                    _stream(stream)), "ra_window_select")
+
+
+def ra_scored_scratch_bytes(cfg, max_prompt_len):
+    return int(_lib().ra_scored_scratch_bytes(ctypes.byref(cfg), int(max_prompt_len)))
+
+
+def ra_scored_evict(handle, seq_lo, seq_hi, params, q_window, scratch, stream=None):
+    """Measurement only: one score-based eviction round (see the header)."""
+    nbytes = scratch.numel() * scratch.element_size()
+    _check(_lib().ra_scored_evict(handle, int(seq_lo), int(seq_hi), ctypes.byref(params),
+                                  _ptr(q_window), _ptr(scratch), ctypes.c_size_t(nbytes),
+                                  _stream(stream)), "ra_scored_evict")
 
 
 def ra_attention_plan(handle):

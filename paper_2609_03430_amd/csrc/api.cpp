@@ -38,6 +38,16 @@ ra_status hip_fail(hipError_t e) {
 
 int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 
+// Trigger period of the end-of-step rule; 0 = never (external rounds only).
+int trigger_every(const ra_config& c) {
+  return c.policy == RA_POLICY_EXTERNAL ? 0 : c.evict_every;
+}
+
+bool at_trigger(const ra_config& c, int step) {
+  const int e = trigger_every(c);
+  return e > 0 && step % e == 0;
+}
+
 int64_t keep_rows(const ra_config& c, int32_t lp) {
   if (c.budget_mode == RA_BUDGET_EVICTABLE) return c.budget_k;
   return static_cast<int64_t>(c.budget_k) - lp;
@@ -103,17 +113,6 @@ void mirror_plan(SeqMeta& M, int r, bool at_trigger) {
   }
 }
 
-// Work decomposition of one attention launch, from the host mirror:
-//  - bf16: about 1024 wavefronts (one per SIMD on 256 CUs, measured best on
-//    the 40-layer workloads against 512..4096) in at least 256 workgroups (a
-//    workgroup runs on one CU; 8-wavefront groups for 128 heads left half
-//    the CUs idle): W = min(4, 1024 / heads) wavefronts per workgroup (a
-//    power of two), one workgroup per (head, split), as few splits as reach
-//    ~1024 wavefronts, so from 256 KV heads up a head is one workgroup that
-//    writes its output and no merge kernel runs;
-//  - fp32: one wavefront per (head, split), ~1024 work items.
-// cfg.attn_split > 0 fixes the keys per work item (rounded up to a multiple
-// of 32 per wavefront).
 // Launch plan of the decode attention (measured on the workloads' shapes).
 // A bf16 work item is one (sequence, KV head, split) on a workgroup of W
 // wavefronts, each streaming a contiguous W-th of the split's keys.  The
@@ -194,7 +193,7 @@ ra_status ra_config_check(const ra_config* c) {
       (c->budget_mode != RA_BUDGET_EVICTABLE && c->budget_mode != RA_BUDGET_TOTAL) ||
       (c->dtype != RA_F32 && c->dtype != RA_BF16) || c->num_layers > 4096 ||
       (c->layout != RA_LAYOUT_CHRONOLOGICAL && c->layout != RA_LAYOUT_HOLE_FILL) ||
-      c->policy < RA_POLICY_RANDOM || c->policy > RA_POLICY_RECENCY ||
+      c->policy < RA_POLICY_RANDOM || c->policy > RA_POLICY_EXTERNAL ||
       (c->policy == RA_POLICY_BLOCK && c->policy_block < 1) ||
       c->num_kv_heads > 4096)
     return RA_ERR_INVALID_ARG;
@@ -430,14 +429,14 @@ ra_status ra_end_step(ra_cache* c, void* stream, int32_t* n_evicted) {
   c->n_appended = 0;
   if (!any_active) return RA_OK;
   RA_LAUNCH(ra::launch_advance(c->meta, c->slot_lo, c->slot_hi, 1, c->cfg.recent_r,
-                               c->cfg.evict_every, s));
+                               trigger_every(c->cfg), s));
   int due = 0;
   for (int i = c->slot_lo; i < c->slot_hi; ++i) {
     SeqMeta& M = c->mirror[i];
     if (!M.active) continue;
     M.step += 1;
     M.len += 1;
-    mirror_plan(M, c->cfg.recent_r, M.step % c->cfg.evict_every == 0);
+    mirror_plan(M, c->cfg.recent_r, at_trigger(c->cfg, M.step));
     due += M.due;
   }
   if (due) {
@@ -481,14 +480,14 @@ ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
     RA_LAUNCH(ra::launch_append_positions(c->meta, c->pos, c->slot_lo, c->slot_hi,
                                           c->cfg.num_layers, c->cfg.num_kv_heads, run, s));
     RA_LAUNCH(ra::launch_advance(c->meta, c->slot_lo, c->slot_hi, run, c->cfg.recent_r,
-                                 every, s));
+                                 trigger_every(c->cfg), s));
     int due = 0;
     for (int i = c->slot_lo; i < c->slot_hi; ++i) {
       SeqMeta& M = c->mirror[i];
       if (!M.active) continue;
       M.step += run;
       M.len += run;
-      mirror_plan(M, c->cfg.recent_r, M.step % every == 0);
+      mirror_plan(M, c->cfg.recent_r, at_trigger(c->cfg, M.step));
       due += M.due;
     }
     if (due) {
@@ -562,6 +561,63 @@ ra_status ra_window_select(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
   RA_LAUNCH(ra::launch_window_score(c->shape(), c->meta, c->kpool, c->pos, dev_q_window,
                                     dev_scores, dev_drops, scores_stride, seq_lo, seq_hi,
                                     max_len, static_cast<hipStream_t>(stream)));
+  return RA_OK;
+}
+
+size_t ra_scored_scratch_bytes(const ra_config* cfg, int32_t max_prompt_len) {
+  if (ra_config_check(cfg) != RA_OK || max_prompt_len < 0) return 0;
+  const int64_t cap = ra_region_rows(cfg, max_prompt_len);
+  if (cap < 0) return 0;
+  const size_t heads = static_cast<size_t>(cfg->max_seqs) * cfg->num_layers * cfg->num_kv_heads;
+  return heads * (static_cast<size_t>(cfg->evict_every) + static_cast<size_t>(round_up(cap, 64))) *
+         sizeof(int32_t);
+}
+
+ra_status ra_scored_evict(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
+                          const ra_scorer_params* prm, const void* dev_q_window,
+                          void* dev_scratch, size_t scratch_bytes, void* stream) {
+  if (!c || !prm || seq_lo < 0 || seq_hi > c->cfg.max_seqs || seq_lo >= seq_hi ||
+      !dev_q_window || !dev_scratch)
+    return RA_ERR_INVALID_ARG;
+  if (prm->scorer < RA_SCORER_SNAPKV || prm->scorer > RA_SCORER_VASE)
+    return RA_ERR_INVALID_ARG;
+  if (c->cfg.dtype != RA_BF16 || c->cfg.layout != RA_LAYOUT_CHRONOLOGICAL)
+    return RA_ERR_UNSUPPORTED;
+  if (prm->scorer != RA_SCORER_SNAPKV) return RA_ERR_UNSUPPORTED;
+  if (c->step_open()) return RA_ERR_STATE;
+  const int r = c->cfg.recent_r, every = c->cfg.evict_every;
+  int max_len = 0, max_cap = 0, due = 0;
+  for (int s = seq_lo; s < seq_hi; ++s) {
+    const SeqMeta& M = c->mirror[s];
+    if (!M.active) continue;
+    const int m = M.len - M.prompt_len - r - M.k_keep;
+    if (m <= 0) continue;
+    if (M.step < 64 || m > every) return RA_ERR_STATE;
+    max_len = std::max(max_len, M.len);
+    max_cap = std::max(max_cap, M.cap);
+    ++due;
+  }
+  if (!due) return RA_OK;
+  if (max_len - r > 512 * 32) return RA_ERR_UNSUPPORTED;
+  const size_t heads = static_cast<size_t>(seq_hi - seq_lo) * c->cfg.num_layers *
+                       c->cfg.num_kv_heads;
+  const int score_stride = static_cast<int>(round_up(max_cap, 64));
+  if (scratch_bytes < heads * (static_cast<size_t>(every) + score_stride) * sizeof(int32_t))
+    return RA_ERR_INVALID_ARG;
+  int32_t* drops = static_cast<int32_t*>(dev_scratch);
+  float* scores = reinterpret_cast<float*>(drops + heads * every);
+  (void)scores;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  // 1. score and select on the current rows; 2. the plan rule (new length,
+  // event count) on device and mirror; 3. compaction from the drop lists
+  RA_LAUNCH(ra::launch_window_score(c->shape(), c->meta, c->kpool, c->pos, dev_q_window,
+                                    nullptr, drops, score_stride, seq_lo, seq_hi, max_len, s));
+  RA_LAUNCH(ra::launch_plan_range(c->meta, seq_lo, seq_hi, r, s));
+  for (int i = c->slot_lo; i < c->slot_hi; ++i) c->mirror[i].due = 0;
+  for (int i = seq_lo; i < seq_hi; ++i)
+    if (c->mirror[i].active) mirror_plan(c->mirror[i], r, true);
+  RA_LAUNCH(ra::launch_compact_drops(c->shape(), c->meta, c->kpool, c->vpool, c->pos, drops,
+                                     every, seq_lo, seq_hi, s));
   return RA_OK;
 }
 

@@ -114,12 +114,19 @@ __device__ __forceinline__ u32x4 funnel8(u32x4 a, u32x4 b, int off) {
   }
 }
 
-template <int NT, int KPT, typename E, bool POS_ONLY, int LAYOUT>
-__global__ __launch_bounds__(NT) void evict_kernel(
-    const SeqMeta* __restrict__ meta, E* __restrict__ kpool,
-    E* __restrict__ vpool, int32_t* __restrict__ pos, int L, int Hkv, int r,
-    int slot_lo, int policy, int block) {
-  static_assert(KPT <= 32, "drop flags live in one 32-bit mask");
+// Order-preserving in-place compaction of one head's region: destination
+// row j < new_len (from the first drop d0 on) receives source row
+// j + #{k : f[k] <= j}, where f[k] = d_k - k for the ascending drop list d.
+// Chunks of kChunk destination rows: every thread gathers its part of the
+// chunk into registers, the block waits until all loads have returned and
+// synchronises, then writes.  Sources are never below destinations and a
+// chunk's writes land below the next chunk's sources, so the move is
+// race-free.  Called by every thread of the workgroup.
+template <int NT, typename E, bool POS_ONLY>
+__device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, int d0,
+                                             int new_len, int old_len, int64_t region,
+                                             E* __restrict__ kpool, E* __restrict__ vpool,
+                                             int32_t* __restrict__ P) {
   constexpr int kEpu = 16 / sizeof(E);            // elements per 16-byte unit
   constexpr int kKUnitsRow = kHeadDim / kEpu;     // 16-byte units per key row
   constexpr int kVUnitsCh = 8 / kEpu;             // units per (tile, channel)
@@ -127,95 +134,7 @@ __global__ __launch_bounds__(NT) void evict_kernel(
   constexpr int kVUnits = (kChunk / 8) * kHeadDim * kVUnitsCh;
   constexpr int kKPer = (kKUnits + NT - 1) / NT;
   constexpr int kVPer = (kVUnits + NT - 1) / NT;
-
-  __shared__ SelectShared sel_sh;
-  __shared__ int f[kMaxEvery];
-  __shared__ int src_of[kChunk];
-
-  const int per_seq = L * Hkv;
-  const int slot = slot_lo + static_cast<int>(blockIdx.x) / per_seq;
-  const int lg = static_cast<int>(blockIdx.x) % per_seq;
-  const int layer = lg / Hkv, g = lg % Hkv;
-  const SeqMeta& Mref = meta[slot];
-  if (!Mref.active || !Mref.due) return;
-  const int lp = Mref.prompt_len, old_len = Mref.plan_len;
-  const int event = Mref.plan_event;
-  const uint64_t seed = Mref.seed, rid = Mref.rid;
-  const int C = old_len - lp - r;          // candidates: every cached position
-  const int m = C - Mref.k_keep;           // outside the prompt and the r most
-  if (m <= 0) return;                      // recent ones (positions < thr)
-  const int thr = lp + Mref.step - r;
-  const int new_len = old_len - m;
-  // slots that can hold candidates: all of them in the chronological layout
-  // are [lp, old_len - r); after hole-fill events the recent rows may sit
-  // anywhere above the prompt, so every slot from lp is examined
-  const int span = LAYOUT == 0 ? C : old_len - lp;
-  const int64_t region = Mref.base + static_cast<int64_t>(lg) * Mref.cap;
-  int32_t* P = pos + region;
   const int t = threadIdx.x;
-
-  // 1. scores of this thread's KPT consecutive slots; ties by position
-  uint64_t score[KPT];
-  uint32_t tie[KPT];
-  uint32_t valid = 0;
-#pragma unroll
-  for (int i = 0; i < KPT; ++i) {
-    const int c = t * KPT + i;
-    score[i] = 0;
-    tie[i] = 0;
-    if (c < span) {
-      const int p = P[lp + c];
-      if (p < thr) {
-        score[i] = policy_key(policy, block, p, lp, event, layer, g, seed, rid);
-        tie[i] = static_cast<uint32_t>(p);
-        valid |= 1u << i;
-      }
-    }
-  }
-
-  // 2. radix select of the m smallest (score, position); 3. drop list
-  const uint32_t drop = select_smallest<NT, KPT, 64>(score, tie, valid, m, sel_sh);
-  drop_list<NT, KPT>(drop, lp, f, sel_sh);
-  const int d0 = f[0];
-
-  if constexpr (LAYOUT == 1) {
-    // hole-fill: the h holes below new_len take the h surviving rows of the
-    // tail [new_len, old_len), in ascending order; nothing else moves
-    __shared__ int mv_src[kMaxEvery];
-    __shared__ int mv_dst[kMaxEvery];
-    __shared__ int n_holes;
-    if (t == 0) n_holes = count_le_slot(f, m, new_len - 1);
-    __syncthreads();
-    const int h = n_holes;
-    for (int i = t; i < m; i += NT) {
-      const int s = new_len + i;                 // tail slot
-      const int before = count_le_slot(f, m, s - 1) - h;   // tail drops below s
-      const bool dropped = h + before < m && f[h + before] + h + before == s;
-      if (!dropped) {
-        const int j = i - before;                // rank among tail survivors
-        mv_src[j] = s;
-        mv_dst[j] = f[j] + j;
-      }
-    }
-    __syncthreads();
-    for (int j = t; j < h; j += NT) P[mv_dst[j]] = P[mv_src[j]];
-    if constexpr (!POS_ONLY) {
-      constexpr int kUnitsRow = kHeadDim * sizeof(E) / 16;
-      for (int idx = t; idx < h * kUnitsRow; idx += NT) {
-        const int j = idx / kUnitsRow, col = idx % kUnitsRow;
-        *reinterpret_cast<u32x4*>(kpool + (region + mv_dst[j]) * kHeadDim + col * (16 / sizeof(E))) =
-            *reinterpret_cast<const u32x4*>(kpool + (region + mv_src[j]) * kHeadDim +
-                                            col * (16 / sizeof(E)));
-      }
-      for (int idx = t; idx < h * kHeadDim; idx += NT) {
-        const int j = idx / kHeadDim, ch = idx % kHeadDim;
-        vpool[vt_index(region + mv_dst[j], ch)] = vpool[vt_index(region + mv_src[j], ch)];
-      }
-    }
-    return;
-  }
-
-  // 4. order-preserving in-place compaction of positions, keys and values
   const E zero_e = E(0);
   for (int j0 = d0 & ~7; j0 < new_len; j0 += kChunk) {
     if (t < kChunk) src_of[t] = j0 + t + count_le(f, m, j0 + t);
@@ -301,6 +220,129 @@ __global__ __launch_bounds__(NT) void evict_kernel(
   }
 }
 
+template <int NT, int KPT, typename E, bool POS_ONLY, int LAYOUT>
+__global__ __launch_bounds__(NT) void evict_kernel(
+    const SeqMeta* __restrict__ meta, E* __restrict__ kpool,
+    E* __restrict__ vpool, int32_t* __restrict__ pos, int L, int Hkv, int r,
+    int slot_lo, int policy, int block) {
+  static_assert(KPT <= 32, "drop flags live in one 32-bit mask");
+  __shared__ SelectShared sel_sh;
+  __shared__ int f[kMaxEvery];
+
+  const int per_seq = L * Hkv;
+  const int slot = slot_lo + static_cast<int>(blockIdx.x) / per_seq;
+  const int lg = static_cast<int>(blockIdx.x) % per_seq;
+  const int layer = lg / Hkv, g = lg % Hkv;
+  const SeqMeta& Mref = meta[slot];
+  if (!Mref.active || !Mref.due) return;
+  const int lp = Mref.prompt_len, old_len = Mref.plan_len;
+  const int event = Mref.plan_event;
+  const uint64_t seed = Mref.seed, rid = Mref.rid;
+  const int C = old_len - lp - r;          // candidates: every cached position
+  const int m = C - Mref.k_keep;           // outside the prompt and the r most
+  if (m <= 0) return;                      // recent ones (positions < thr)
+  const int thr = lp + Mref.step - r;
+  const int new_len = old_len - m;
+  // slots that can hold candidates: all of them in the chronological layout
+  // are [lp, old_len - r); after hole-fill events the recent rows may sit
+  // anywhere above the prompt, so every slot from lp is examined
+  const int span = LAYOUT == 0 ? C : old_len - lp;
+  const int64_t region = Mref.base + static_cast<int64_t>(lg) * Mref.cap;
+  int32_t* P = pos + region;
+  const int t = threadIdx.x;
+
+  // 1. scores of this thread's KPT consecutive slots; ties by position
+  uint64_t score[KPT];
+  uint32_t tie[KPT];
+  uint32_t valid = 0;
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    const int c = t * KPT + i;
+    score[i] = 0;
+    tie[i] = 0;
+    if (c < span) {
+      const int p = P[lp + c];
+      if (p < thr) {
+        score[i] = policy_key(policy, block, p, lp, event, layer, g, seed, rid);
+        tie[i] = static_cast<uint32_t>(p);
+        valid |= 1u << i;
+      }
+    }
+  }
+
+  // 2. radix select of the m smallest (score, position); 3. drop list
+  const uint32_t drop = select_smallest<NT, KPT, 64>(score, tie, valid, m, sel_sh);
+  drop_list<NT, KPT>(drop, lp, f, sel_sh);
+  const int d0 = f[0];
+
+  if constexpr (LAYOUT == 1) {
+    // hole-fill: the h holes below new_len take the h surviving rows of the
+    // tail [new_len, old_len), in ascending order; nothing else moves
+    __shared__ int mv_src[kMaxEvery];
+    __shared__ int mv_dst[kMaxEvery];
+    __shared__ int n_holes;
+    if (t == 0) n_holes = count_le_slot(f, m, new_len - 1);
+    __syncthreads();
+    const int h = n_holes;
+    for (int i = t; i < m; i += NT) {
+      const int s = new_len + i;                 // tail slot
+      const int before = count_le_slot(f, m, s - 1) - h;   // tail drops below s
+      const bool dropped = h + before < m && f[h + before] + h + before == s;
+      if (!dropped) {
+        const int j = i - before;                // rank among tail survivors
+        mv_src[j] = s;
+        mv_dst[j] = f[j] + j;
+      }
+    }
+    __syncthreads();
+    for (int j = t; j < h; j += NT) P[mv_dst[j]] = P[mv_src[j]];
+    if constexpr (!POS_ONLY) {
+      constexpr int kUnitsRow = kHeadDim * sizeof(E) / 16;
+      for (int idx = t; idx < h * kUnitsRow; idx += NT) {
+        const int j = idx / kUnitsRow, col = idx % kUnitsRow;
+        *reinterpret_cast<u32x4*>(kpool + (region + mv_dst[j]) * kHeadDim + col * (16 / sizeof(E))) =
+            *reinterpret_cast<const u32x4*>(kpool + (region + mv_src[j]) * kHeadDim +
+                                            col * (16 / sizeof(E)));
+      }
+      for (int idx = t; idx < h * kHeadDim; idx += NT) {
+        const int j = idx / kHeadDim, ch = idx % kHeadDim;
+        vpool[vt_index(region + mv_dst[j], ch)] = vpool[vt_index(region + mv_src[j], ch)];
+      }
+    }
+    return;
+  }
+
+  // 4. order-preserving in-place compaction of positions, keys and values
+  __shared__ int src_of[kChunk];
+  compact_rows<NT, E, POS_ONLY>(f, m, src_of, d0, new_len, old_len, region, kpool, vpool, P);
+}
+
+// Compaction of a score-based round: each due head's drop list comes from
+// `drops` (ascending slot indices, `stride` per head, head index =
+// (slot - slot_lo) * L * Hkv + layer * Hkv + g); the state kernels have
+// already set len to the new length and plan_len to the old one.
+template <int NT, typename E>
+__global__ __launch_bounds__(NT) void compact_drops_kernel(
+    const SeqMeta* __restrict__ meta, E* __restrict__ kpool, E* __restrict__ vpool,
+    int32_t* __restrict__ pos, const int32_t* __restrict__ drops, int stride, int L,
+    int Hkv, int slot_lo) {
+  __shared__ int f[kMaxEvery];
+  __shared__ int src_of[kChunk];
+  const int per_seq = L * Hkv;
+  const int slot = slot_lo + static_cast<int>(blockIdx.x) / per_seq;
+  const int lg = static_cast<int>(blockIdx.x) % per_seq;
+  const SeqMeta& M = meta[slot];
+  if (!M.active || !M.due) return;
+  const int old_len = M.plan_len, new_len = M.len, m = old_len - new_len;
+  if (m <= 0 || m > stride) return;
+  const int32_t* d = drops + static_cast<int64_t>(blockIdx.x) * stride;
+  for (int k = threadIdx.x; k < m; k += NT) f[k] = d[k] - k;
+  __syncthreads();
+  const int64_t region = M.base + static_cast<int64_t>(lg) * M.cap;
+  compact_rows<NT, E, false>(f, m, src_of, f[0], new_len, old_len, region, kpool, vpool,
+                             pos + region);
+}
+
 template <int NT, int KPT, bool POS_ONLY, int LAYOUT>
 hipError_t launch_layout(const Shape& sh, const SeqMeta* meta, void* kpool,
                          void* vpool, int32_t* pos, int slot_lo, int slot_hi,
@@ -356,6 +398,22 @@ hipError_t launch_mode(const Shape& sh, const SeqMeta* meta, void* kpool,
 }
 
 }  // namespace
+
+hipError_t launch_compact_drops(const Shape& sh, const SeqMeta* meta, void* kpool,
+                                void* vpool, int32_t* pos, const int32_t* drops,
+                                int stride, int slot_lo, int slot_hi, hipStream_t s) {
+  if (slot_hi <= slot_lo) return hipSuccess;
+  const dim3 grid((slot_hi - slot_lo) * sh.L * sh.Hkv);
+  if (sh.dtype == 1)
+    hipLaunchKernelGGL((compact_drops_kernel<512, uint16_t>), grid, dim3(512), 0, s, meta,
+                       static_cast<uint16_t*>(kpool), static_cast<uint16_t*>(vpool), pos,
+                       drops, stride, sh.L, sh.Hkv, slot_lo);
+  else
+    hipLaunchKernelGGL((compact_drops_kernel<512, float>), grid, dim3(512), 0, s, meta,
+                       static_cast<float*>(kpool), static_cast<float*>(vpool), pos,
+                       drops, stride, sh.L, sh.Hkv, slot_lo);
+  return hipGetLastError();
+}
 
 hipError_t launch_evict(const Shape& sh, const SeqMeta* meta, void* kpool,
                         void* vpool, int32_t* pos, int slot_lo, int slot_hi,

@@ -94,6 +94,13 @@ struct AttnLaunch {
 };
 hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s);
 
+// Score-based rounds (measurement only): compaction from given drop lists,
+// and the plan rule applied to a slot range.
+hipError_t launch_compact_drops(const Shape& sh, const SeqMeta* meta, void* kpool,
+                                void* vpool, int32_t* pos, const int32_t* drops,
+                                int stride, int slot_lo, int slot_hi, hipStream_t s);
+hipError_t launch_plan_range(SeqMeta* meta, int slot_lo, int slot_hi, int r, hipStream_t s);
+
 // Observation-window scorer (measurement only, window_score.hip).
 hipError_t launch_window_score(const Shape& sh, const SeqMeta* meta, const void* kpool,
                                const int32_t* pos, const void* qwin, float* scores_out,

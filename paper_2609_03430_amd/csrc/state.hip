@@ -44,7 +44,17 @@ __global__ void advance_kernel(SeqMeta* meta, int lo, int hi, int n_steps,
   if (!M.active) return;
   M.step += n_steps;
   M.len += n_steps;
-  plan(M, r, M.step % every == 0);
+  plan(M, r, every > 0 && M.step % every == 0);   // every = 0: never triggers
+  meta[s] = M;
+}
+
+// The plan rule applied now to every active slot of [lo, hi).
+__global__ void plan_range_kernel(SeqMeta* meta, int lo, int hi, int r) {
+  const int s = lo + blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= hi) return;
+  SeqMeta M = meta[s];
+  if (!M.active) return;
+  plan(M, r, true);
   meta[s] = M;
 }
 
@@ -168,6 +178,14 @@ hipError_t launch_advance(SeqMeta* meta, int slot_lo, int slot_hi, int n_steps,
 
 hipError_t launch_plan_now(SeqMeta* meta, int slot, int r, hipStream_t s) {
   hipLaunchKernelGGL(plan_now_kernel, dim3(1), dim3(64), 0, s, meta, slot, r);
+  return hipGetLastError();
+}
+
+hipError_t launch_plan_range(SeqMeta* meta, int slot_lo, int slot_hi, int r, hipStream_t s) {
+  if (slot_hi <= slot_lo) return hipSuccess;
+  const int n = slot_hi - slot_lo;
+  hipLaunchKernelGGL(plan_range_kernel, dim3((n + 255) / 256), dim3(256), 0, s, meta,
+                     slot_lo, slot_hi, r);
   return hipGetLastError();
 }
 

@@ -206,6 +206,7 @@ __global__ __launch_bounds__(kNT) void window_score_kernel(
   if (scores_out) {
     for (int i = t; i < len; i += kNT) scores_out[head_out * scores_stride + i] = score[i];
   }
+  if (!drops_out || m <= 0) return;
   // max-pool and select the m lowest candidates
   uint64_t key[KPT];
   uint32_t tie[KPT];
@@ -225,9 +226,7 @@ __global__ __launch_bounds__(kNT) void window_score_kernel(
   }
   const uint32_t drop = select_smallest<kNT, KPT, 32>(key, tie, valid, m, sel_sh);
   drop_list<kNT, KPT>(drop, 0, f, sel_sh);
-  if (drops_out) {
-    for (int k = t; k < m; k += kNT) drops_out[head_out * every + k] = f[k] + k;
-  }
+  for (int k = t; k < m; k += kNT) drops_out[head_out * every + k] = f[k] + k;
 }
 
 template <int KPT>

@@ -35,7 +35,7 @@ def test_config_validation():
         dict(num_q_heads=41), dict(num_layers=0), dict(budget_k=-1),
         dict(recent_r=-1), dict(evict_every=0), dict(max_seqs=0),
         dict(attn_split=33), dict(budget_mode=7), dict(dtype=9), dict(layout=2),
-        dict(policy=4), dict(policy=-1), dict(policy=2, policy_block=0),
+        dict(policy=5), dict(policy=-1), dict(policy=2, policy_block=0),
     ]
     for kw in bad:
         c = B.make_config(40, 40, 8, 8192, max_seqs=32)
