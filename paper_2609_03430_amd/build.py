@@ -16,7 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 LIBDIR = os.path.join(PKG, "lib")
 LIB = os.path.join(LIBDIR, "librandattn.so")
 OBJDIR = os.path.join(ROOT, "_build")
-SOURCES = ["attention.hip", "evict.hip", "state.hip", "window_score.hip", "api.cpp"]
+SOURCES = ["attention.hip", "evict.hip", "state.hip", "window_score.hip", "scored.hip", "api.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

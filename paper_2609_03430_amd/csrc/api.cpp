@@ -583,7 +583,10 @@ ra_status ra_scored_evict(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
     return RA_ERR_INVALID_ARG;
   if (c->cfg.dtype != RA_BF16 || c->cfg.layout != RA_LAYOUT_CHRONOLOGICAL)
     return RA_ERR_UNSUPPORTED;
-  if (prm->scorer != RA_SCORER_SNAPKV) return RA_ERR_UNSUPPORTED;
+  if (prm->scorer == RA_SCORER_RKV &&
+      (!(prm->rkv_lambda >= 0.f && prm->rkv_lambda <= 1.f) || prm->rkv_recent_dups < 0 ||
+       !std::isfinite(prm->rkv_threshold)))
+    return RA_ERR_INVALID_ARG;
   if (c->step_open()) return RA_ERR_STATE;
   const int r = c->cfg.recent_r, every = c->cfg.evict_every;
   int max_len = 0, max_cap = 0, due = 0;
@@ -599,6 +602,8 @@ ra_status ra_scored_evict(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
   }
   if (!due) return RA_OK;
   if (max_len - r > 512 * 32) return RA_ERR_UNSUPPORTED;
+  // R-KV keeps two floats per row in LDS
+  if (prm->scorer == RA_SCORER_RKV && max_len > 8192) return RA_ERR_UNSUPPORTED;
   const size_t heads = static_cast<size_t>(seq_hi - seq_lo) * c->cfg.num_layers *
                        c->cfg.num_kv_heads;
   const int score_stride = static_cast<int>(round_up(max_cap, 64));
@@ -606,12 +611,21 @@ ra_status ra_scored_evict(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
     return RA_ERR_INVALID_ARG;
   int32_t* drops = static_cast<int32_t*>(dev_scratch);
   float* scores = reinterpret_cast<float*>(drops + heads * every);
-  (void)scores;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   // 1. score and select on the current rows; 2. the plan rule (new length,
   // event count) on device and mirror; 3. compaction from the drop lists
-  RA_LAUNCH(ra::launch_window_score(c->shape(), c->meta, c->kpool, c->pos, dev_q_window,
-                                    nullptr, drops, score_stride, seq_lo, seq_hi, max_len, s));
+  if (prm->scorer == RA_SCORER_SNAPKV) {
+    RA_LAUNCH(ra::launch_window_score(c->shape(), c->meta, c->kpool, c->pos, dev_q_window,
+                                      nullptr, drops, score_stride, seq_lo, seq_hi, max_len, s));
+  } else {
+    RA_LAUNCH(ra::launch_window_score(c->shape(), c->meta, c->kpool, c->pos, dev_q_window,
+                                      scores, nullptr, score_stride, seq_lo, seq_hi, max_len, s));
+    RA_LAUNCH(ra::launch_scored_select(c->shape(), prm->scorer, c->meta, c->kpool, c->vpool,
+                                       c->pos, scores, score_stride, drops, seq_lo, seq_hi,
+                                       max_len, prm->rkv_lambda, prm->rkv_threshold,
+                                       prm->rkv_recent_dups, prm->vase_n_large,
+                                       prm->vase_seed, s));
+  }
   RA_LAUNCH(ra::launch_plan_range(c->meta, seq_lo, seq_hi, r, s));
   for (int i = c->slot_lo; i < c->slot_hi; ++i) c->mirror[i].due = 0;
   for (int i = seq_lo; i < seq_hi; ++i)

@@ -100,6 +100,13 @@ hipError_t launch_compact_drops(const Shape& sh, const SeqMeta* meta, void* kpoo
                                 void* vpool, int32_t* pos, const int32_t* drops,
                                 int stride, int slot_lo, int slot_hi, hipStream_t s);
 hipError_t launch_plan_range(SeqMeta* meta, int slot_lo, int slot_hi, int r, hipStream_t s);
+// R-KV (scorer 1) or VaSE (scorer 2) selection from raw window scores (scored.hip).
+hipError_t launch_scored_select(const Shape& sh, int scorer, const SeqMeta* meta,
+                                const void* kpool, const void* vpool, const int32_t* pos,
+                                const float* raw_scores, int score_stride, int32_t* drops,
+                                int slot_lo, int slot_hi, int max_len, float lambda,
+                                float threshold, int recent_dups, int n_large,
+                                uint64_t seed, hipStream_t s);
 
 // Observation-window scorer (measurement only, window_score.hip).
 hipError_t launch_window_score(const Shape& sh, const SeqMeta* meta, const void* kpool,

@@ -1,14 +1,15 @@
 """Score-based eviction rounds (measurement only) against the oracle.
 
 A cache with the external policy decodes without end-of-step eviction; at
-every 64th step a SnapKV round (Section 2: window attention weights of the
-last 64 queries, max-pooled over 7 rows; the prompt competes) drops the
-rows over budget.  The GPU's drop set must be a valid lowest-m selection of
-the oracle's fp64 pooled scores (unique up to near-ties within the bf16 /
-fp32 tolerance), the surviving rows must be exactly the rows of the kept
-positions in chronological order, sequences under budget must be left as
-they are, and attention after the round must match the oracle on the kept
-rows.
+every 64th step a scored round (Section 2: SnapKV, R-KV or VaSE; the prompt
+competes) drops the rows over budget.  The GPU's drop set must be a valid
+selection under the oracle's fp64 scores: lowest-m of the SnapKV or R-KV
+score up to near-ties within the bf16 / fp32 tolerance; for VaSE the large
+set (value ranges are exact) bit-exact and the proportional fill consistent
+with the oracle's keys log(u)/w for every w within the score tolerance.  The
+surviving rows must be exactly the rows of the kept positions in
+chronological order, sequences under budget must be left as they are, and
+attention after the round must match the oracle on the kept rows.
 """
 
 import numpy as np
@@ -17,6 +18,7 @@ import torch
 
 from gpu_harness import Run, log, max_abs
 from oracle.attention import gqa_decode
+from oracle.scored import es_uniform, lowest, rkv_redundancy, rkv_scores, value_range
 from oracle.window_score import max_pool, window_scores
 from paper_2609_03430_amd import binding as B
 
@@ -33,19 +35,39 @@ def _qwin(run, steps_done):
     return qw
 
 
-def _valid_lowest(pooled, drops, n_cand, m, where):
+def _valid_lowest(pooled, drops, n_cand, m, where, tol=None):
     d = np.asarray(drops)
     assert d.shape[0] == m and np.all(np.diff(d) > 0) and d.min() >= 0 and d.max() < n_cand, where
     thr = np.sort(pooled[:n_cand])[m - 1]
-    tol = 4e-3 + 2e-3 * thr
+    if tol is None:
+        tol = 4e-3 + 2e-3 * thr
     kept = np.setdiff1d(np.arange(n_cand), d)
     assert np.all(pooled[d] <= thr + tol), where
     assert np.all(pooled[kept] >= thr - tol), where
 
 
+def _valid_vase(pooled, vr, u, P, drops, n_cand, budget, n_large, m, where):
+    d = np.asarray(drops)
+    assert d.shape[0] == m and np.all(np.diff(d) > 0), where
+    small = lowest(vr[:n_cand], P[:n_cand], n_cand - n_large)
+    large = np.setdiff1d(np.arange(n_cand), small)
+    assert not set(d.tolist()) & set(large.tolist()), where     # large set kept exactly
+    assert set(d.tolist()) <= set(small.tolist()), where
+    w = pooled[:n_cand]
+    delta = 4e-3 + 2e-3 * w
+    lo = np.log(u[:n_cand]) / np.maximum(w - delta, 1e-12)      # keys log(u)/w over the
+    hi = np.log(u[:n_cand]) / (w + delta)                       # tolerance interval of w
+    kept_small = np.setdiff1d(small, d)
+    assert lo[d].max() <= hi[kept_small].min(), where
+
+
+SCORERS = [(B.RA_SCORER_SNAPKV, "snapkv"), (B.RA_SCORER_RKV, "rkv"), (B.RA_SCORER_VASE, "vase")]
+
+
+@pytest.mark.parametrize("scorer,name", SCORERS)
 @pytest.mark.parametrize("Hq,Hkv,lps,K", [(8, 2, [40, 7, 0], 100), (10, 2, [150, 3], 60)])
-def test_snapkv_rounds(Hq, Hkv, lps, K):
-    log("snapkv rounds Hq=%d Hkv=%d lps=%s K=%d" % (Hq, Hkv, lps, K))
+def test_scored_rounds(Hq, Hkv, lps, K, scorer, name):
+    log("%s rounds Hq=%d Hkv=%d lps=%s K=%d" % (name, Hq, Hkv, lps, K))
     L, r, every = 2, 64, 64
     run = Run(L=L, Hq=Hq, Hkv=Hkv, K=K, lps=lps, r=r, every=every,
               policy=B.RA_POLICY_EXTERNAL)
@@ -53,7 +75,9 @@ def test_snapkv_rounds(Hq, Hkv, lps, K):
     wl = run.wl.to("cpu")
     scratch = torch.empty(B.ra_scored_scratch_bytes(run.cfg, max(lps)) // 4 + 1,
                           dtype=torch.int32, device="cuda")
-    prm = B.make_scorer(B.RA_SCORER_SNAPKV)
+    lam, thr_dup, n_dups, vseed = 0.1, 0.9, 1, 4242
+    prm = B.make_scorer(scorer, rkv_lambda=lam, rkv_threshold=thr_dup,
+                        rkv_recent_dups=n_dups, vase_n_large=-1, vase_seed=vseed)
     # the oracle's view: positions per (slot, layer, head)
     P = {(b, l, g): np.arange(lps[b]) for b in range(run.n) for l in range(L) for g in range(Hkv)}
     rounds = 0
@@ -80,7 +104,7 @@ def test_snapkv_rounds(Hq, Hkv, lps, K):
                 for l in range(L):
                     for g in range(Hkv):
                         Pold = P[(b, l, g)]
-                        k, _ = wl.k_rows(run.rids[b], l, g, torch.as_tensor(Pold), lps[b]), None
+                        k = wl.k_rows(run.rids[b], l, g, torch.as_tensor(Pold), lps[b])
                         q = wl.q_rows(run.rids[b], l, torch.arange(g * G, (g + 1) * G).view(-1, 1),
                                       torch.arange(t - 64, t).view(1, -1))
                         qpos = np.repeat((lps[b] + np.arange(t - 64, t))[None, :], G, 0)
@@ -90,7 +114,21 @@ def test_snapkv_rounds(Hq, Hkv, lps, K):
                         got = run.positions(b, l, g)
                         drops = np.setdiff1d(np.arange(n), np.searchsorted(Pold, got))
                         assert np.all(np.diff(got) > 0), (b, l, g)
-                        _valid_lowest(pooled, drops, n - r, m, (t, b, l, g))
+                        where = (name, t, b, l, g)
+                        budget = lps[b] + K
+                        if scorer == B.RA_SCORER_SNAPKV:
+                            _valid_lowest(pooled, drops, n - r, m, where)
+                        elif scorer == B.RA_SCORER_RKV:
+                            cbar = rkv_redundancy(k.double().numpy(), Pold, thr_dup, n_dups)
+                            s = rkv_scores(pooled, cbar, n - r, lam)
+                            # the SnapKV term carries the scorer's tolerance, scaled by lambda
+                            tol = lam * (4e-3 + 2e-3 * pooled.max()) + 1e-5
+                            _valid_lowest(s, drops, n - r, m, where, tol)
+                        else:
+                            v = wl.v_rows(run.rids[b], l, g, torch.as_tensor(Pold), lps[b])
+                            u = es_uniform(Pold, vseed, run.rids[b], before[b].event, l, g)
+                            _valid_vase(pooled, value_range(v.double().numpy()), u, Pold,
+                                        drops, n - r, budget, budget // 2, m, where)
                         P[(b, l, g)] = got.astype(np.int64)
                         kg, vg = run.rows(b, l, g)
                         kw = wl.k_rows(run.rids[b], l, g, torch.as_tensor(got), lps[b])
