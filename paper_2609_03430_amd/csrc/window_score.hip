@@ -122,13 +122,17 @@ __global__ __launch_bounds__(kNT) void window_score_kernel(
     for (int i = 0; i < 4; ++i) qpos[j][i] = first_pos + 16 * (qt % 4) + 4 * grp + i;
   }
 
-  float mx[TPW][4], sm[TPW][4];
+  // running max (raw dot units) and sum of 2^((x - max) * scale) per
+  // (tile, D-row) of this lane's key column; after pass 1, lse2 holds
+  // log2 of the full sum in the same scaled units
+  float mx[TPW][4], sm[TPW][4], lse2[TPW][4];
 #pragma unroll
   for (int j = 0; j < TPW; ++j)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       mx[j][i] = kNegInf;
       sm[j][i] = 0.f;
+      lse2[j][i] = 0.f;
     }
 
   const int nblk = (len + kBlk - 1) / kBlk;
@@ -141,14 +145,17 @@ __global__ __launch_bounds__(kNT) void window_score_kernel(
     for (int b = 0; b < nblk; ++b) {
       const int cur = b & 1;
       if (b + 1 < nblk) fetch_block(nb, Kr, P, (b + 1) * kBlk, len);
+      // every window query sees every key of the block unless the block
+      // reaches past the first window position (rows beyond len carry an
+      // infinite position): only then is the causal mask applied
+      const bool masked = lpos[cur][kBlk - 1] > first_pos;
+      float x[TPW][4][4];                      // [tile][subtile][D-row]
 #pragma unroll
       for (int kt = 0; kt < kBlk / 16; ++kt) {
         const uint16_t* krow = lk[cur] + (kt * 16 + qi) * kRowStride + 8 * grp;
         bf16x8 kop[4];
 #pragma unroll
         for (int s = 0; s < 4; ++s) kop[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(krow + 32 * s));
-        const int kpos = lpos[cur][kt * 16 + qi];
-        float colsum = 0.f;
 #pragma unroll
         for (int j = 0; j < TPW; ++j) {
           f32x4 d = {0.f, 0.f, 0.f, 0.f};
@@ -156,21 +163,49 @@ __global__ __launch_bounds__(kNT) void window_score_kernel(
           for (int s = 0; s < 4; ++s)
             d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qop[j][s], kop[s], d, 0, 0, 0);
 #pragma unroll
+          for (int i = 0; i < 4; ++i) x[j][kt][i] = d[i];
+        }
+      }
+      if (masked) {
+#pragma unroll
+        for (int kt = 0; kt < kBlk / 16; ++kt) {
+          const int kpos = lpos[cur][kt * 16 + qi];
+#pragma unroll
+          for (int j = 0; j < TPW; ++j)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              if (kpos > qpos[j][i]) x[j][kt][i] = kNegInf;
+        }
+      }
+      if (pass == 0) {
+#pragma unroll
+        for (int j = 0; j < TPW; ++j) {
+          if (!tile_ok[j]) continue;
+#pragma unroll
           for (int i = 0; i < 4; ++i) {
-            const bool vis = tile_ok[j] && kpos <= qpos[j][i];
-            const float x = d[i] * scale_log2;
-            if (pass == 0) {
-              if (vis) {
-                const float mn = fmaxf(mx[j][i], x);
-                sm[j][i] = sm[j][i] * exp2f(mx[j][i] - mn) + exp2f(x - mn);
-                mx[j][i] = mn;
-              }
-            } else if (vis) {
-              colsum += exp2f(x - mx[j][i]);     // mx holds the lse in pass 2
-            }
+            const float bm = fmaxf(fmaxf(x[j][0][i], x[j][1][i]), fmaxf(x[j][2][i], x[j][3][i]));
+            const float mn = fmaxf(mx[j][i], bm);
+            if (mn == kNegInf) continue;           // nothing visible yet
+            const float off = -mn * scale_log2;
+            float acc = sm[j][i] * __builtin_amdgcn_exp2f(fmaf(mx[j][i], scale_log2, off));
+#pragma unroll
+            for (int kt = 0; kt < kBlk / 16; ++kt)
+              acc += __builtin_amdgcn_exp2f(fmaf(x[j][kt][i], scale_log2, off));
+            sm[j][i] = acc;
+            mx[j][i] = mn;
           }
         }
-        if (pass == 1) {
+      } else {
+#pragma unroll
+        for (int kt = 0; kt < kBlk / 16; ++kt) {
+          float colsum = 0.f;
+#pragma unroll
+          for (int j = 0; j < TPW; ++j) {
+            if (!tile_ok[j]) continue;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+              colsum += __builtin_amdgcn_exp2f(fmaf(x[j][kt][i], scale_log2, -lse2[j][i]));
+          }
           colsum += __shfl_xor(colsum, 16, 64);
           colsum += __shfl_xor(colsum, 32, 64);
           const int key = b * kBlk + kt * 16 + qi;
@@ -182,7 +217,7 @@ __global__ __launch_bounds__(kNT) void window_score_kernel(
       __syncthreads();
     }
     if (pass == 0) {
-      // merge the 16 lanes holding the same queries, then lse = max + log2(sum)
+      // merge the 16 lanes holding the same queries, then the log2-sum-exp
 #pragma unroll
       for (int j = 0; j < TPW; ++j)
 #pragma unroll
@@ -193,11 +228,12 @@ __global__ __launch_bounds__(kNT) void window_score_kernel(
             const float b_m = __shfl_xor(a_m, o, 64), b_s = __shfl_xor(a_s, o, 64);
             const float mn = fmaxf(a_m, b_m);
             if (mn != kNegInf) {
-              a_s = a_s * exp2f(a_m - mn) + b_s * exp2f(b_m - mn);
+              a_s = a_s * __builtin_amdgcn_exp2f((a_m - mn) * scale_log2) +
+                    b_s * __builtin_amdgcn_exp2f((b_m - mn) * scale_log2);
               a_m = mn;
             }
           }
-          mx[j][i] = a_m + log2f(a_s);
+          lse2[j][i] = a_m * scale_log2 + __builtin_amdgcn_logf(a_s);
         }
     }
   }
