@@ -168,20 +168,26 @@ def evict_cost(B, torch, Workload, methods=("random", "snapkv")):
                "vase": B.RA_SCORER_VASE}
     res = {"metric": "eviction round ms per layer (scoring + selection + compaction)",
            "protocol": "1 sequence, K=1024 incl. prompt 300, r=64, every 64, 4096 "
-                       "decode steps from the prompt, HIP events", "shapes": {}}
+                       "decode steps from the prompt, distinct rows every step, HIP events",
+           "shapes": {}}
     for name, (L, Hq, Hkv) in (("qwen3-4b", (36, 32, 8)), ("qwen3-14b", (40, 40, 8))):
         lp, K, steps = 300, 1024, 4096
-        wl = Workload(2000, L, Hq, Hkv, 128, torch.bfloat16, True, ring=RING, device=dev)
+        # every step's rows are distinct (no input ring): the redundancy term
+        # of R-KV sees the near-duplicates of the generator's row collisions,
+        # not a 64-step period
+        wl = Workload(2000, L, Hq, Hkv, 128, torch.bfloat16, True, ring=None, device=dev)
         ls = torch.arange(L, device=dev).view(-1, 1, 1)
         gs = torch.arange(Hkv, device=dev).view(1, -1, 1)
         ps = torch.arange(lp, device=dev).view(1, 1, -1)
         kp = wl.k_rows(0, ls, gs, ps, lp).contiguous()
         vp = wl.v_rows(0, ls, gs, ps, lp).contiguous()
-        qs = torch.stack([torch.stack([wl.q_step([0], l, [j]) for l in range(L)])
-                          for j in range(RING)])              # [64][L][1][Hq][128]
-        # window row w of an event at a multiple of 64 steps is ring slot w
-        qwin = qs.permute(2, 1, 3, 0, 4).contiguous()          # [1][L][Hq][64][128]
-        kv = [[wl.kv_step([0], l, [lp + j], [lp]) for l in range(L)] for j in range(RING)]
+        zero = torch.zeros(steps, dtype=torch.long, device=dev)
+        st = torch.arange(steps, device=dev)
+        qs = torch.stack([wl.q_step(zero, l, st) for l in range(L)], 1)   # [T][L][Hq][128]
+        ks = torch.empty(steps, L, Hkv, 128, dtype=torch.bfloat16, device=dev)
+        vs = torch.empty_like(ks)
+        for l in range(L):
+            ks[:, l], vs[:, l] = wl.kv_step(zero, l, lp + st, zero + lp)
         out = torch.empty(1, Hq, 128, dtype=torch.bfloat16, device=dev)
         res["shapes"][name] = {"layers": L, "kv_heads": Hkv}
         for method in methods:
@@ -199,23 +205,25 @@ def evict_cost(B, torch, Workload, methods=("random", "snapkv")):
             torch.cuda.synchronize()
             ev, dec = [], []
             for t in range(steps):
-                j = t % RING
+                due = False
+                if scored and (t + 1) % EVERY == 0:
+                    due = B.ra_get_seq_info(h, 0).len + 1 - R > K
+                    if due:   # the window: queries of steps t - 63 .. t, oldest first
+                        qwin = qs[t - 63:t + 1].permute(1, 2, 0, 3).unsqueeze(0).contiguous()
                 a0 = torch.cuda.Event(enable_timing=True)
                 a1 = torch.cuda.Event(enable_timing=True)
                 a0.record(stream)
                 for l in range(L):
-                    B.ra_decode_attention(h, l, qs[j, l], kv[j][l][0], kv[j][l][1], out,
-                                          cache.workspace, stream)
+                    B.ra_decode_attention(h, l, qs[t, l].unsqueeze(0), ks[t, l].unsqueeze(0),
+                                          vs[t, l].unsqueeze(0), out, cache.workspace, stream)
                 a1.record(stream)
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
                 e0.record(stream)
                 n = B.ra_end_step(h, stream)
-                if scored and (t + 1) % EVERY == 0:
-                    info = B.ra_get_seq_info(h, 0)
-                    if info.len - R > K:
-                        B.ra_scored_evict(h, 0, 1, prm, qwin, scratch, stream)
-                        n = 1
+                if due:
+                    B.ra_scored_evict(h, 0, 1, prm, qwin, scratch, stream)
+                    n = 1
                 e1.record(stream)
                 dec.append((a0, a1))
                 (ev if n else dec).append((e0, e1))

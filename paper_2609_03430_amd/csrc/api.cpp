@@ -569,7 +569,7 @@ size_t ra_scored_scratch_bytes(const ra_config* cfg, int32_t max_prompt_len) {
   const int64_t cap = ra_region_rows(cfg, max_prompt_len);
   if (cap < 0) return 0;
   const size_t heads = static_cast<size_t>(cfg->max_seqs) * cfg->num_layers * cfg->num_kv_heads;
-  return heads * (static_cast<size_t>(cfg->evict_every) + static_cast<size_t>(round_up(cap, 64))) *
+  return heads * (static_cast<size_t>(cfg->evict_every) + 2 * static_cast<size_t>(round_up(cap, 64))) *
          sizeof(int32_t);
 }
 
@@ -602,12 +602,11 @@ ra_status ra_scored_evict(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
   }
   if (!due) return RA_OK;
   if (max_len - r > 512 * 32) return RA_ERR_UNSUPPORTED;
-  // R-KV keeps two floats per row in LDS
-  if (prm->scorer == RA_SCORER_RKV && max_len > 8192) return RA_ERR_UNSUPPORTED;
+
   const size_t heads = static_cast<size_t>(seq_hi - seq_lo) * c->cfg.num_layers *
                        c->cfg.num_kv_heads;
   const int score_stride = static_cast<int>(round_up(max_cap, 64));
-  if (scratch_bytes < heads * (static_cast<size_t>(every) + score_stride) * sizeof(int32_t))
+  if (scratch_bytes < heads * (static_cast<size_t>(every) + 2 * score_stride) * sizeof(int32_t))
     return RA_ERR_INVALID_ARG;
   int32_t* drops = static_cast<int32_t*>(dev_scratch);
   float* scores = reinterpret_cast<float*>(drops + heads * every);
@@ -621,8 +620,9 @@ ra_status ra_scored_evict(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
     RA_LAUNCH(ra::launch_window_score(c->shape(), c->meta, c->kpool, c->pos, dev_q_window,
                                       scores, nullptr, score_stride, seq_lo, seq_hi, max_len, s));
     RA_LAUNCH(ra::launch_scored_select(c->shape(), prm->scorer, c->meta, c->kpool, c->vpool,
-                                       c->pos, scores, score_stride, drops, seq_lo, seq_hi,
-                                       max_len, prm->rkv_lambda, prm->rkv_threshold,
+                                       c->pos, scores, scores + heads * score_stride,
+                                       score_stride, drops, seq_lo, seq_hi, max_len,
+                                       prm->rkv_lambda, prm->rkv_threshold,
                                        prm->rkv_recent_dups, prm->vase_n_large,
                                        prm->vase_seed, s));
   }

@@ -103,10 +103,10 @@ hipError_t launch_plan_range(SeqMeta* meta, int slot_lo, int slot_hi, int r, hip
 // R-KV (scorer 1) or VaSE (scorer 2) selection from raw window scores (scored.hip).
 hipError_t launch_scored_select(const Shape& sh, int scorer, const SeqMeta* meta,
                                 const void* kpool, const void* vpool, const int32_t* pos,
-                                const float* raw_scores, int score_stride, int32_t* drops,
-                                int slot_lo, int slot_hi, int max_len, float lambda,
-                                float threshold, int recent_dups, int n_large,
-                                uint64_t seed, hipStream_t s);
+                                const float* raw_scores, float* cbar_scratch,
+                                int score_stride, int32_t* drops, int slot_lo, int slot_hi,
+                                int max_len, float lambda, float threshold, int recent_dups,
+                                int n_large, uint64_t seed, hipStream_t s);
 
 // Observation-window scorer (measurement only, window_score.hip).
 hipError_t launch_window_score(const Shape& sh, const SeqMeta* meta, const void* kpool,

@@ -199,121 +199,165 @@ __global__ __launch_bounds__(kNT) void vase_kernel(
 // R-KV
 // ---------------------------------------------------------------------------
 
-constexpr int kRowTiles = 4;   // 16-row tiles a wavefront carries per column sweep
+constexpr int kRowTiles = 4;                          // 16-row tiles per wavefront
+constexpr int kChunkRows = (kNT / 64) * kRowTiles * 16;   // rows per workgroup: 512
 
-template <int KPT>
-__global__ __launch_bounds__(kNT) void rkv_kernel(
+// Sum of squares of this lane's 32 channels of an operand row (8 per k-step).
+__device__ __forceinline__ float sumsq(const bf16x8 (&v)[4]) {
+  float s = 0.f;
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float x = static_cast<float>(v[k][e]);
+      s = fmaf(x, x, s);
+    }
+  return s;
+}
+
+__device__ __forceinline__ void load_operand(bf16x8 (&v)[4], const uint16_t* Kr, int row,
+                                             int grp) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+    v[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(
+        Kr + static_cast<int64_t>(row) * kHeadDim + 32 * s + 8 * grp));
+}
+
+// cbar of the candidate rows [chunk * 512, chunk * 512 + 512) of one head.
+// D = K_rows . K_cols^T on v_mfma_f32_16x16x32_bf16: lane l holds rows
+// 4*(l/16) + i of a row tile and column l % 16 of a column tile; the four
+// lane groups hold a row's (or column's) channels in four parts of 32, so a
+// norm is a lane sum plus two shuffles.  Column tiles are swept from the
+// most recent (highest slot = highest position in the chronological layout)
+// down, so the first `recent_dups` near-duplicates a row meets are the ones
+// not counted; a ballot gives each row its near-duplicate columns in a tile.
+__global__ __launch_bounds__(kNT) void rkv_cbar_kernel(
     const SeqMeta* __restrict__ meta, const uint16_t* __restrict__ kpool,
-    const int32_t* __restrict__ pos, const float* __restrict__ raw_scores, int score_stride,
+    float* __restrict__ cbar_out, int stride, int n_chunks, int L, int Hkv, int r,
+    int slot_lo, float threshold, int recent_dups) {
+  const int head_idx = static_cast<int>(blockIdx.x) / n_chunks;
+  const int chunk = static_cast<int>(blockIdx.x) % n_chunks;
+  const int per_seq = L * Hkv;
+  const int slot = slot_lo + head_idx / per_seq;
+  const int lg = head_idx % per_seq;
+  const SeqMeta& M = meta[slot];
+  const int len = M.len, n_cand = M.len - r;
+  if (!M.active || n_cand - (M.prompt_len + M.k_keep) <= 0) return;
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int qi = lane & 15, grp = lane >> 4;
+  const int rt0 = (chunk * kChunkRows) / 16 + wave * kRowTiles;
+  if (rt0 * 16 >= n_cand) return;
+  const uint16_t* Kr = kpool + (M.base + static_cast<int64_t>(lg) * M.cap) * kHeadDim;
+
+  bf16x8 a[kRowTiles][4];
+  float sum[kRowTiles][4], dup[kRowTiles][4], invr[kRowTiles][4];
+  int found[kRowTiles][4];
+#pragma unroll
+  for (int q = 0; q < kRowTiles; ++q) {
+    load_operand(a[q], Kr, min((rt0 + q) * 16 + qi, len - 1), grp);
+    float ss = sumsq(a[q]);
+    ss += __shfl_xor(ss, 16, 64);
+    ss += __shfl_xor(ss, 32, 64);
+    const float inv = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;      // row qi of the tile
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      sum[q][i] = 0.f;
+      dup[q][i] = 0.f;
+      found[q][i] = 0;
+      invr[q][i] = __shfl(inv, 4 * grp + i, 64);             // D-row 4*grp + i
+    }
+  }
+  const int n_ct = (len + 15) / 16;
+  bf16x8 b[4], bn[4];
+  load_operand(b, Kr, min((n_ct - 1) * 16 + qi, len - 1), grp);
+  for (int ct = n_ct - 1; ct >= 0; --ct) {
+    if (ct > 0) load_operand(bn, Kr, (ct - 1) * 16 + qi, grp);   // next tile in flight
+    const int col = ct * 16 + qi;
+    float ss = sumsq(b);
+    ss += __shfl_xor(ss, 16, 64);
+    ss += __shfl_xor(ss, 32, 64);
+    const float invc = ss > 0.f ? 1.f / sqrtf(ss) : 0.f;
+    float c[kRowTiles][4];
+    bool near = false;
+#pragma unroll
+    for (int q = 0; q < kRowTiles; ++q) {
+      f32x4 d = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+        d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[q][s], b[s], d, 0, 0, 0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        c[q][i] = d[i] * invr[q][i] * invc;
+        near |= c[q][i] > threshold;
+      }
+    }
+    // the last (ragged) column tile, the tiles holding a row's own column,
+    // and tiles with a near-duplicate take the full bookkeeping; the rest
+    // (nearly all) only accumulate
+    const bool edge = ct == n_ct - 1 || (ct >= rt0 && ct < rt0 + kRowTiles);
+    if (!edge && !__ballot(near)) {
+#pragma unroll
+      for (int q = 0; q < kRowTiles; ++q)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) sum[q][i] += c[q][i];
+    } else {
+#pragma unroll
+      for (int q = 0; q < kRowTiles; ++q)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int row = (rt0 + q) * 16 + 4 * grp + i;
+          const bool ok = col < len && col != row;
+          if (ok) sum[q][i] += c[q][i];
+          const uint64_t bal = __ballot(ok && c[q][i] > threshold);
+          const uint32_t bits = static_cast<uint32_t>(bal >> (16 * grp)) & 0xFFFFu;
+          const int need = recent_dups - found[q][i];
+          if (need > 0 && bits) {
+            if (((bits >> qi) & 1u) && __popc(bits >> (qi + 1)) < need) dup[q][i] += c[q][i];
+            found[q][i] += min(need, __popc(bits));
+          }
+        }
+    }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) b[s] = bn[s];
+  }
+  float* out = cbar_out + static_cast<int64_t>(head_idx) * stride;
+#pragma unroll
+  for (int q = 0; q < kRowTiles; ++q)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float v = sum[q][i] - dup[q][i];
+#pragma unroll
+      for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
+      const int row = (rt0 + q) * 16 + 4 * grp + i;
+      if (qi == 0 && row < n_cand) out[row] = v / static_cast<float>(len - 1);
+    }
+}
+
+// softmax of cbar over the candidates, the mix with SnapKV, and the m lowest.
+template <int KPT>
+__global__ __launch_bounds__(kNT) void rkv_select_kernel(
+    const SeqMeta* __restrict__ meta, const int32_t* __restrict__ pos,
+    const float* __restrict__ raw_scores, const float* __restrict__ cbar_in, int stride,
     int32_t* __restrict__ drops, int every, int L, int Hkv, int r, int slot_lo,
-    float lambda, float threshold, int recent_dups) {
-  extern __shared__ float lds[];                // inv_norm [len], then cbar [n_cand]
+    float lambda) {
   __shared__ SelectShared sel_sh;
   __shared__ int f[kMaxEvery];
   __shared__ float red[kNT / 64];
   const Head h = locate_head(meta, L, Hkv, r, slot_lo);
   if (!h.active) return;
   const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int qi = lane & 15, grp = lane >> 4;
   const int32_t* P = pos + h.region;
-  const uint16_t* Kr = kpool + h.region * kHeadDim;
-  const float* raw = raw_scores + static_cast<int64_t>(blockIdx.x) * score_stride;
-  float* inv_norm = lds;
-  float* cbar = lds + h.len;
+  const float* raw = raw_scores + static_cast<int64_t>(blockIdx.x) * stride;
+  const float* cbar = cbar_in + static_cast<int64_t>(blockIdx.x) * stride;
 
-  // 1. inverse key norms (fp32 sums of squares of the bf16 channels)
-  for (int j = t; j < h.len; j += kNT) {
-    const u32x4* row = reinterpret_cast<const u32x4*>(Kr + static_cast<int64_t>(j) * kHeadDim);
-    float s = 0.f;
-#pragma unroll
-    for (int q = 0; q < 16; ++q) {
-      const u32x4 v = row[q];
-      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float x = bf16_bits_to_f32((w[e >> 1] >> (16 * (e & 1))) & 0xFFFF);
-        s += x * x;
-      }
-    }
-    inv_norm[j] = s > 0.f ? 1.f / sqrtf(s) : 0.f;
-  }
-  __syncthreads();
-
-  // 2. cbar of every candidate row.  D = K_rows . K_cols^T on
-  // v_mfma_f32_16x16x32_bf16: lane l holds rows 4*(l/16) + i of the row tile
-  // and column l % 16 of the column tile.  Column tiles are swept from the
-  // most recent (highest slot = highest position, chronological layout) down,
-  // so the first `recent_dups` near-duplicates a row meets are the ones not
-  // counted; a ballot gives each row its near-duplicate columns in a tile.
-  const int n_rt = (h.n_cand + 15) / 16;
-  const int n_ct = (h.len + 15) / 16;
-  for (int rt0 = wave * kRowTiles; rt0 < n_rt; rt0 += (kNT / 64) * kRowTiles) {
-    bf16x8 a[kRowTiles][4];
-    float sum[kRowTiles][4], dup[kRowTiles][4], invr[kRowTiles][4];
-    int found[kRowTiles][4];
-#pragma unroll
-    for (int q = 0; q < kRowTiles; ++q) {
-      const int row = min((rt0 + q) * 16 + qi, h.len - 1);
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-        a[q][s] = as_bf16x8(*reinterpret_cast<const u32x4*>(
-            Kr + static_cast<int64_t>(row) * kHeadDim + 32 * s + 8 * grp));
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        sum[q][i] = 0.f;
-        dup[q][i] = 0.f;
-        found[q][i] = 0;
-        invr[q][i] = inv_norm[min((rt0 + q) * 16 + 4 * grp + i, h.len - 1)];
-      }
-    }
-    for (int ct = n_ct - 1; ct >= 0; --ct) {
-      const int col = ct * 16 + qi;
-      const int colc = min(col, h.len - 1);
-      bf16x8 b[4];
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-        b[s] = as_bf16x8(*reinterpret_cast<const u32x4*>(
-            Kr + static_cast<int64_t>(colc) * kHeadDim + 32 * s + 8 * grp));
-      const float invc = inv_norm[colc];
-#pragma unroll
-      for (int q = 0; q < kRowTiles; ++q) {
-        f32x4 d = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-          d = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[q][s], b[s], d, 0, 0, 0);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int row = (rt0 + q) * 16 + 4 * grp + i;
-          const bool ok = col < h.len && col != row;
-          const float c = d[i] * invr[q][i] * invc;
-          if (ok) sum[q][i] += c;
-          const uint64_t bal = __ballot(ok && c > threshold);
-          const uint32_t bits = static_cast<uint32_t>(bal >> (16 * grp)) & 0xFFFFu;
-          const int need = recent_dups - found[q][i];
-          if (need > 0 && bits) {
-            if (((bits >> qi) & 1u) && __popc(bits >> (qi + 1)) < need) dup[q][i] += c;
-            found[q][i] += min(need, __popc(bits));
-          }
-        }
-      }
-    }
-    // reduce each row over its 16 lanes and store cbar
-#pragma unroll
-    for (int q = 0; q < kRowTiles; ++q)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float v = sum[q][i] - dup[q][i];
-#pragma unroll
-        for (int o = 1; o < 16; o <<= 1) v += __shfl_xor(v, o, 64);
-        const int row = (rt0 + q) * 16 + 4 * grp + i;
-        if (qi == 0 && row < h.n_cand) cbar[row] = v / static_cast<float>(h.len - 1);
-      }
-  }
-  __syncthreads();
-
-  // 3. softmax of cbar over the candidates, mixed with the SnapKV score
+  float cb[KPT];
   float mx = -__builtin_huge_valf();
-  for (int c = t; c < h.n_cand; c += kNT) mx = fmaxf(mx, cbar[c]);
+#pragma unroll
+  for (int i = 0; i < KPT; ++i) {
+    const int c = t * KPT + i;
+    cb[i] = c < h.n_cand ? cbar[c] : -__builtin_huge_valf();
+    mx = fmaxf(mx, cb[i]);
+  }
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
   if (lane == 0) red[wave] = mx;
@@ -323,7 +367,9 @@ __global__ __launch_bounds__(kNT) void rkv_kernel(
   for (int w = 1; w < kNT / 64; ++w) mx = fmaxf(mx, red[w]);
   __syncthreads();
   float sm = 0.f;
-  for (int c = t; c < h.n_cand; c += kNT) sm += expf(cbar[c] - mx);
+#pragma unroll
+  for (int i = 0; i < KPT; ++i)
+    if (t * KPT + i < h.n_cand) sm += expf(cb[i] - mx);
 #pragma unroll
   for (int o = 1; o < 64; o <<= 1) sm += __shfl_xor(sm, o, 64);
   if (lane == 0) red[wave] = sm;
@@ -342,7 +388,7 @@ __global__ __launch_bounds__(kNT) void rkv_kernel(
     tie[i] = 0;
     if (c < h.n_cand) {
       const float s = lambda * pooled_score(raw, c, h.len) -
-                      (1.f - lambda) * (expf(cbar[c] - mx) / sm);
+                      (1.f - lambda) * (expf(cb[i] - mx) / sm);
       key[i] = order_key_f32(s);
       tie[i] = static_cast<uint32_t>(P[c]);
       valid |= 1u << i;
@@ -356,18 +402,17 @@ __global__ __launch_bounds__(kNT) void rkv_kernel(
 
 template <int KPT>
 hipError_t launch_kpt(int scorer, dim3 grid, size_t lds_rows, hipStream_t s,
-                      const SeqMeta* meta, const void* kpool, const void* vpool,
-                      const int32_t* pos, const float* raw, int stride, int32_t* drops,
+                      const SeqMeta* meta, const void* vpool, const int32_t* pos,
+                      const float* raw, const float* cbar, int stride, int32_t* drops,
                       int every, int L, int Hkv, int r, int slot_lo, float lambda,
-                      float threshold, int recent_dups, int n_large, uint64_t seed) {
+                      int n_large, uint64_t seed) {
   if (scorer == 2) {
     hipLaunchKernelGGL((vase_kernel<KPT>), grid, dim3(kNT), lds_rows * sizeof(uint32_t), s,
                        meta, static_cast<const uint16_t*>(vpool), pos, raw, stride, drops,
                        every, L, Hkv, r, slot_lo, n_large, seed);
   } else {
-    hipLaunchKernelGGL((rkv_kernel<KPT>), grid, dim3(kNT), 2 * lds_rows * sizeof(float), s,
-                       meta, static_cast<const uint16_t*>(kpool), pos, raw, stride, drops,
-                       every, L, Hkv, r, slot_lo, lambda, threshold, recent_dups);
+    hipLaunchKernelGGL((rkv_select_kernel<KPT>), grid, dim3(kNT), 0, s, meta, pos, raw,
+                       cbar, stride, drops, every, L, Hkv, r, slot_lo, lambda);
   }
   return hipGetLastError();
 }
@@ -376,18 +421,27 @@ hipError_t launch_kpt(int scorer, dim3 grid, size_t lds_rows, hipStream_t s,
 
 hipError_t launch_scored_select(const Shape& sh, int scorer, const SeqMeta* meta,
                                 const void* kpool, const void* vpool, const int32_t* pos,
-                                const float* raw_scores, int score_stride, int32_t* drops,
-                                int slot_lo, int slot_hi, int max_len, float lambda,
-                                float threshold, int recent_dups, int n_large,
-                                uint64_t seed, hipStream_t s) {
+                                const float* raw_scores, float* cbar_scratch,
+                                int score_stride, int32_t* drops, int slot_lo, int slot_hi,
+                                int max_len, float lambda, float threshold, int recent_dups,
+                                int n_large, uint64_t seed, hipStream_t s) {
   if (slot_hi <= slot_lo) return hipSuccess;
-  const dim3 grid((slot_hi - slot_lo) * sh.L * sh.Hkv);
+  const int heads = (slot_hi - slot_lo) * sh.L * sh.Hkv;
+  const dim3 grid(heads);
   const int n_cand = max_len;   // upper bound of len - r
+  if (scorer == 1) {
+    const int n_chunks = (n_cand + kChunkRows - 1) / kChunkRows;
+    hipLaunchKernelGGL(rkv_cbar_kernel, dim3(heads * n_chunks), dim3(kNT), 0, s, meta,
+                       static_cast<const uint16_t*>(kpool), cbar_scratch, score_stride,
+                       n_chunks, sh.L, sh.Hkv, sh.r, slot_lo, threshold, recent_dups);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
   const size_t rows = static_cast<size_t>(max_len);
-#define RA_SC_LAUNCH(K)                                                                   \
-  launch_kpt<K>(scorer, grid, rows, s, meta, kpool, vpool, pos, raw_scores, score_stride, \
-                drops, sh.every, sh.L, sh.Hkv, sh.r, slot_lo, lambda, threshold,          \
-                recent_dups, n_large, seed)
+#define RA_SC_LAUNCH(K)                                                                  \
+  launch_kpt<K>(scorer, grid, rows, s, meta, vpool, pos, raw_scores, cbar_scratch,       \
+                score_stride, drops, sh.every, sh.L, sh.Hkv, sh.r, slot_lo, lambda,      \
+                n_large, seed)
   if (n_cand <= kNT * 4) return RA_SC_LAUNCH(4);
   if (n_cand <= kNT * 8) return RA_SC_LAUNCH(8);
   if (n_cand <= kNT * 16) return RA_SC_LAUNCH(16);
