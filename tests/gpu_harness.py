@@ -28,7 +28,7 @@ class Run:
                  scaled=True, wl_seed=1000, ring=None, attn_split=0,
                  max_seqs=None, write_prompt=True, begin=True,
                  layout=B.RA_LAYOUT_CHRONOLOGICAL, policy=B.RA_POLICY_RANDOM,
-                 block=1):
+                 block=1, pool_rows=None):
         self.L, self.Hq, self.Hkv, self.K, self.r, self.every = L, Hq, Hkv, K, r, every
         self.G = Hq // Hkv
         self.lps = list(lps)
@@ -44,7 +44,7 @@ class Run:
         self.cfg = B.make_config(L, Hq, Hkv, K, r, every, mode, dtype, self.max_seqs,
                                  attn_split=attn_split, layout=layout, policy=policy,
                                  policy_block=block)
-        rows = sum(B.ra_seq_rows(self.cfg, lp) for lp in self.lps)
+        rows = pool_rows or sum(B.ra_seq_rows(self.cfg, lp) for lp in self.lps)
         self.cache = B.Cache(self.cfg, rows)
         self.h = self.cache.handle
         self.wl = Workload(wl_seed, L, Hq, Hkv, 128, self.tdtype, scaled, ring=ring,
@@ -64,6 +64,10 @@ class Run:
         B.ra_seq_begin(self.h, slot, lp, self.seeds[slot], self.rids[slot], kp, vp)
         self.steps[slot] = 0
         self.active = getattr(self, "active", set()) | {slot}
+
+    def end(self, slot):
+        B.ra_seq_end(self.h, slot)
+        self.active.discard(slot)
 
     def k_keep(self, slot):
         return keep_count(self.K, self.lps[slot], self.mode)
