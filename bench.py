@@ -242,6 +242,147 @@ def evict_cost(B, torch, Workload, methods=("random", "snapkv")):
     return res
 
 
+def serving(B, torch, Workload, steps, log):
+    """Continuous batching of a request stream (the paper's serving regime:
+    staggered compressions, requests finishing and being replaced).
+
+    Phi-4-reasoning attention shape (40 layers, 40 Q / 10 KV heads), 128
+    slots, budget K = 2048 evictable rows per head (the paper's budget for its
+    32k benchmark traces), r = 64, every 64; requests with prompts ~U[64, 2048]
+    and a fixed 8192-token generation (the paper's shortest serving length).
+    At the window start every slot holds a request at a uniformly drawn age
+    (reached through the real sampler by staggered begins and fast forward),
+    so compressions happen on every sequence's own phase and a request
+    completes every ~64 steps on average; a finished request ends, and the
+    next request of the stream begins in its slot with its prompt rows
+    written (first fit over the released rows).  Timed: every decode step's
+    launches, end-of-step evictions and the admissions, wall clock; the rows
+    of the requests to admit are generated before the window.
+    """
+    import numpy as np
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    L, Hq, Hkv, S, K, GEN = 40, 40, 10, 128, 2048, 8192
+    rng = np.random.default_rng(1005)
+    n_req = S + 64
+    lps = rng.integers(64, 2049, n_req).tolist()
+    ages = rng.integers(0, GEN, S).tolist()
+    cfg = B.make_config(L, Hq, Hkv, K, R, EVERY, B.RA_BUDGET_EVICTABLE, B.RA_BF16, S)
+    pool = S * B.ra_seq_rows(cfg, 2048)
+    cache = B.Cache(cfg, pool, device=dev)
+    h = cache.handle
+    wl = Workload(1005, L, Hq, Hkv, 128, torch.bfloat16, True, ring=RING, device=dev)
+    ls = torch.arange(L, device=dev).view(-1, 1, 1)
+    gs = torch.arange(Hkv, device=dev).view(1, -1, 1)
+    hq = torch.arange(Hq, device=dev)
+
+    def prompt(rid, lp):
+        ps = torch.arange(lp, device=dev).view(1, 1, -1)
+        return wl.k_rows(rid, ls, gs, ps, lp).contiguous(), wl.v_rows(rid, ls, gs, ps, lp).contiguous()
+
+    def ring_of(rid, lp, step0):
+        """[64][L][Hq|Hkv][128] inputs of steps step0 .. step0 + 63."""
+        st = torch.arange(step0, step0 + RING, device=dev)
+        rr = torch.full((RING,), rid, device=dev)
+        q = torch.stack([wl.q_step(rr, l, st) for l in range(L)], 1)
+        kv = [wl.kv_step(rr, l, lp + st, torch.full_like(st, lp)) for l in range(L)]
+        return q, torch.stack([k for k, _ in kv], 1), torch.stack([v for _, v in kv], 1)
+
+    # the snapshot: request s in slot s at age ages[s] (oldest begun first)
+    t0 = time.time()
+    order = sorted(range(S), key=lambda s: -ages[s])
+    for i, s in enumerate(order):
+        B.ra_seq_begin(h, s, lps[s], 7 * s + 1, s)
+        nxt = ages[order[i + 1]] if i + 1 < S else 0
+        if ages[s] > nxt:
+            B.ra_fast_forward(h, ages[s] - nxt)
+    for s in range(S):
+        n = B.ra_get_seq_info(h, s).len
+        posb = torch.empty(L * Hkv * n, dtype=torch.int32, device=dev)
+        B.ra_export_positions(h, s, posb)
+        posb = posb.view(L, Hkv, n).long()
+        kr = torch.empty(L, Hkv, n, 128, dtype=torch.bfloat16, device=dev)
+        vr = torch.empty_like(kr)
+        for l in range(L):
+            kr[l] = wl.k_rows(s, l, gs.view(-1, 1), posb[l], lps[s])
+            vr[l] = wl.v_rows(s, l, gs.view(-1, 1), posb[l], lps[s])
+        B.ra_write_rows(h, s, kr, vr)
+        del posb, kr, vr
+    # ring slot j = (iteration mod 64) holds every slot's inputs of the step it
+    # decodes at that iteration (the generator's inputs repeat every 64 steps)
+    q_ring = torch.empty(RING, L, S, Hq, 128, dtype=torch.bfloat16, device=dev)
+    k_ring = torch.empty(RING, L, S, Hkv, 128, dtype=torch.bfloat16, device=dev)
+    v_ring = torch.empty_like(k_ring)
+    for s in range(S):
+        q, k, v = ring_of(s, lps[s], ages[s])
+        q_ring[:, :, s], k_ring[:, :, s], v_ring[:, :, s] = q, k, v
+    # requests admitted during the window (a slot finishes at iteration
+    # GEN - age - 1 and its successor decodes step 0 at iteration GEN - age),
+    # prepared in advance, their rings rotated to that iteration
+    finishing = sorted((GEN - a, s) for s, a in enumerate(ages) if GEN - a < steps)
+    queued = {}
+    for i, (ia, s) in enumerate(finishing):
+        rid = S + i
+        q, k, v = ring_of(rid, lps[rid], 0)
+        queued[(ia, s)] = (rid, prompt(rid, lps[rid]),
+                           tuple(torch.roll(x, ia % RING, 0) for x in (q, k, v)))
+    out = torch.empty(S, Hq, 128, dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    log("serving snapshot ready (%.1fs); %d admissions expected in %d steps"
+        % (time.time() - t0, len(finishing), steps))
+
+    slot_step = list(ages)
+    slot_lp = lps[:S]
+    slot_len = [B.ra_get_seq_info(h, s).len for s in range(S)]
+    kv_bytes = 0                      # algorithmic K/V bytes read by attention
+    tokens = events = admissions = 0
+    adm_ms = 0.0
+    wall0 = time.perf_counter()
+    for it in range(steps):
+        j = it % RING
+        for l in range(L):
+            B.ra_decode_attention(h, l, q_ring[j, l], k_ring[j, l], v_ring[j, l], out,
+                                  cache.workspace, stream)
+        events += B.ra_end_step(h, stream)
+        tokens += S
+        kv_bytes += L * Hkv * 2 * 128 * 2 * sum(n + 1 for n in slot_len)
+        slot_step = [st + 1 for st in slot_step]
+        for s in range(S):
+            slot_len[s] += 1                  # the host rule of the trigger
+            if slot_step[s] % EVERY == 0 and slot_len[s] - slot_lp[s] - R > K:
+                slot_len[s] = slot_lp[s] + K + R
+            if slot_step[s] == GEN:
+                a0 = time.perf_counter()
+                rid, (kp, vp), (q, k, v) = queued.pop((it + 1, s))
+                B.ra_seq_end(h, s, stream)
+                B.ra_seq_begin(h, s, lps[rid], 7 * rid + 1, rid, kp, vp, stream)
+                q_ring[:, :, s], k_ring[:, :, s], v_ring[:, :, s] = q, k, v
+                slot_step[s] = 0
+                slot_lp[s] = lps[rid]
+                slot_len[s] = lps[rid]
+                admissions += 1
+                adm_ms += 1e3 * (time.perf_counter() - a0)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    res = {
+        "metric": "serving decode tokens/s with staggered compressions and request churn",
+        "value": tokens / wall, "unit": "tokens/s", "steps": steps,
+        "ms_per_step": 1e3 * wall / steps,
+        "config": {"workload": "Phi-4-reasoning-shaped attention stack, 128 slots, "
+                               "prompts ~U[64,2048], 8192-token generations, K=2048, r=64, "
+                               "evict every 64 steps, uniform request ages at the start"},
+        "attention_kv_gbs": kv_bytes / wall / 1e9,
+        "attention_kv_gbs_note": "every kept K and V row read once per step, over the "
+                                 "whole wall time (evictions and admissions included)",
+        "compressions_per_step": events / steps,
+        "admissions": admissions,
+        "admission_host_ms_avg": adm_ms / max(1, admissions),
+    }
+    cache.close()
+    torch.cuda.empty_cache()
+    return res
+
+
 def time_window_scorer(B, torch, h, wl, cfg, Bsz, L, Hq, Hkv, stream, comp, log):
     """One round of the observation-window scoring pass over every sequence
     (what a score-based evictor computes before it can evict, and Random
@@ -314,6 +455,10 @@ def main():
                     help="eviction-round cost of one sequence at K=1024 (budget counting "
                          "the prompt, prompt 300) over 4096 decode steps, as in the "
                          "paper's eviction-cost table; prints its own JSON line")
+    ap.add_argument("--serving", action="store_true",
+                    help="continuous batching of a request stream on the Phi-4 shape "
+                         "(staggered compressions, requests finishing and replaced); "
+                         "prints its own JSON line; --steps sets the window")
     ap.add_argument("--evict-cost-methods", default="random,snapkv",
                     help="comma-separated rounds timed by --evict-cost: random and the "
                          "score-based snapkv, rkv, vase")
@@ -341,6 +486,12 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes": src.numel() * 4}))
+        return
+
+    if args.serving:
+        def slog(msg):
+            print("[bench] " + msg, file=sys.stderr, flush=True)
+        print(json.dumps(serving(B, torch, Workload, args.steps, slog)), flush=True)
         return
 
     if args.evict_cost:
