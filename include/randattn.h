@@ -243,14 +243,17 @@ ra_status ra_decode_attention(ra_cache* cache, int32_t layer, const void* q,
 
 /* End the decode step of every active sequence: step += 1, then run the
  * periodic eviction (Eq. 1 with Random Attention's scores, Appendix F
- * trigger) on every (layer, KV head) of each sequence that is due.
+ * trigger) on every (layer, KV head) of each sequence that is due (never
+ * under RA_POLICY_EXTERNAL).
  * Requires every layer to have been appended this step.  If n_evicted is
  * non-NULL it receives the number of sequences evicted (host mirror). */
 ra_status ra_end_step(ra_cache* cache, void* stream, int32_t* n_evicted);
 
 /* Run one eviction event on slot `seq` now, whatever the step count, if
  * its evictable rows exceed k_keep (otherwise a no-op).  Not allowed in
- * the middle of a step (RA_ERR_STATE). */
+ * the middle of a step, nor with more than 1024 rows over k_keep (possible
+ * only under RA_POLICY_EXTERNAL): RA_ERR_STATE.  The keys are Random
+ * Attention's (or the policy's). */
 ra_status ra_evict_now(ra_cache* cache, int32_t seq, void* stream);
 
 /* ---- state transfer and audit --------------------------------------------- */

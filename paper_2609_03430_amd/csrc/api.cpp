@@ -335,9 +335,11 @@ ra_status ra_seq_begin(ra_cache* c, int32_t seq, int32_t prompt_len, uint64_t se
   M.rid = request_id;
   M.active = 1;
   const hipStream_t s = static_cast<hipStream_t>(stream);
-  RA_LAUNCH(ra::launch_seq_set(c->meta, seq, M, s));
+  // rows first, then the metadata that makes the slot active: a failed launch
+  // leaves the slot inactive on the device as in the mirror
   RA_LAUNCH(ra::launch_write_rows(c->shape(), base, M.cap, prompt_len, dev_k_prompt,
                                   dev_v_prompt, nullptr, c->kpool, c->vpool, c->pos, s));
+  RA_LAUNCH(ra::launch_seq_set(c->meta, seq, M, s));
   const int64_t rest = it->second - need;
   c->free_rows.erase(it);
   if (rest > 0) c->free_rows[base + need] = rest;
@@ -452,6 +454,9 @@ ra_status ra_evict_now(ra_cache* c, int32_t seq, void* stream) {
   if (c->step_open()) return RA_ERR_STATE;
   SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
+  // the drop list of one event holds at most kMaxEvery rows (more can pile up
+  // only when no end-of-step rule evicts, i.e. under the external policy)
+  if (M.len - M.prompt_len - c->cfg.recent_r - M.k_keep > ra::kMaxEvery) return RA_ERR_STATE;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   RA_LAUNCH(ra::launch_plan_now(c->meta, seq, c->cfg.recent_r, s));
   for (int i = c->slot_lo; i < c->slot_hi; ++i) c->mirror[i].due = 0;

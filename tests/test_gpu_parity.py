@@ -289,3 +289,28 @@ def test_tiny_config_full_run():
     log("  events=%d worst=%.3g" % (events, worst))
     assert events == 11
     run.close()
+
+
+def test_external_policy_evict_now_bounds():
+    """Under the external policy nothing evicts at the end of a step; an
+    explicit event with up to 1024 rows over budget uses Random Attention's
+    keys (same set as the oracle), and more than that is refused before any
+    launch."""
+    log("external policy: evict-now bounds")
+    from oracle.evict import SequenceReplay
+    run = Run(L=1, Hq=2, Hkv=1, K=8, lps=[3], r=4, every=1024,
+              policy=B.RA_POLICY_EXTERNAL, seeds=[17], rids=[5])
+    for _ in range(1030):
+        _, ev = run.step()
+        assert ev == 0
+    B.ra_evict_now(run.h, 0)                        # 1033 rows: 1018 over budget
+    rep = SequenceReplay(3, 8, 4, 10 ** 9, 17, 5, [(0, 0)])   # no end-of-step trigger
+    rep.advance(1030)
+    rep.evict_now()
+    assert np.array_equal(run.positions(0, 0, 0), rep.P[(0, 0)])
+    for _ in range(1030):                           # 1030 more rows: 1042 over budget
+        run.step()
+    with pytest.raises(B.RandAttnError) as e:
+        B.ra_evict_now(run.h, 0)
+    assert e.value.status == B.RA_ERR_STATE
+    run.close()
