@@ -60,6 +60,14 @@ __device__ __forceinline__ u32x4 ld16(const void* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
 
+// Streaming load (nontemporal): the cached rows are read once per launch, so
+// they are fetched without being kept in the caches.  Used where a load
+// instruction covers whole 128-byte lines (the value tiles); a key load
+// covers half lines of 16 rows, whose other halves the next load reads.
+__device__ __forceinline__ u32x4 ld16_stream(const void* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+
 __device__ __forceinline__ float bf16_to_f32(uint16_t h) {
   return __uint_as_float(static_cast<uint32_t>(h) << 16);
 }
@@ -217,7 +225,7 @@ __device__ __forceinline__ void load_block(BlockRegs& b, const uint16_t* Kr,
   }
   const uint16_t* vt = Vr + static_cast<int64_t>(kb + lm.vrow) * kHeadDim + lm.vch * 8;
 #pragma unroll
-  for (int u = 0; u < 8; ++u) b.v[u] = ld16(vt + 16 * 8 * u);
+  for (int u = 0; u < 8; ++u) b.v[u] = ld16_stream(vt + 16 * 8 * u);
 }
 
 struct Softmax {
