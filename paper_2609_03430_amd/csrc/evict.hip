@@ -75,6 +75,21 @@ __device__ __forceinline__ int count_le_slot(const int* f, int m, int x) {
   return lo;
 }
 
+// Nontemporal 16-byte load and store for the compaction's row moves: a key
+// unit is read once and every destination unit written once per event.  The
+// value units stay on ordinary loads: with a shift that is not a multiple of
+// 8 rows each source tile is read by two destination tiles, and the second
+// read is served from the cache.
+template <typename E>
+__device__ __forceinline__ u32x4 load_stream(const E* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+
+template <typename E>
+__device__ __forceinline__ void store_stream(E* p, u32x4 x) {
+  __builtin_nontemporal_store(x, reinterpret_cast<u32x4*>(p));
+}
+
 __device__ __forceinline__ int64_t vt_index(int64_t row, int ch) {
   // element index of (row, channel) in the transposed 8-row value tiles
   return (row & ~int64_t(7)) * kHeadDim + ch * 8 + (row & 7);
@@ -153,7 +168,7 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
         const int j = j0 + row;
         if (u < kKUnits && j >= d0 && j < new_len) {
           const E* src = kpool + (region + src_of[row]) * kHeadDim + col * kEpu;
-          kbuf[q] = *reinterpret_cast<const u32x4*>(src);
+          kbuf[q] = load_stream(src);
         }
       }
 #pragma unroll
@@ -200,7 +215,7 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
         const int j = j0 + row;
         if (u < kKUnits && j >= d0 && j < new_len) {
           E* dst = kpool + (region + j) * kHeadDim + col * kEpu;
-          *reinterpret_cast<u32x4*>(dst) = kbuf[q];
+          store_stream(dst, kbuf[q]);
         }
       }
 #pragma unroll
@@ -213,7 +228,7 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
           E* dst = vpool + vt_index(region + j0 + tile * 8, ch) + part * kEpu;
           u32x4 w;
           __builtin_memcpy(&w, vbuf[q], 16);
-          *reinterpret_cast<u32x4*>(dst) = w;
+          store_stream(dst, w);
         }
       }
     }
