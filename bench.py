@@ -465,6 +465,10 @@ def main():
     ap.add_argument("--window-scorer", action="store_true",
                     help="also time the observation-window scoring pass (always on for "
                          "phi4-ragged)")
+    ap.add_argument("--full-run", action="store_true",
+                    help="time the whole generation from the prompt (steps 1..32768, no "
+                         "warm-up) instead of the steady-state window at its end; about "
+                         "four minutes on the Qwen3-14B shape")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device-to-device copy three times (the "
                          "known-size reference for the HBM byte counters)")
@@ -501,6 +505,11 @@ def main():
 
     w = WORKLOADS[args.workload]
     L, Hq, Hkv, Bsz, K = (w[k] for k in ("L", "Hq", "Hkv", "B", "K"))
+    if args.full_run:
+        if w["T"] is None:
+            print("--full-run needs a workload with one generation length", file=sys.stderr)
+            sys.exit(2)
+        args.warmup, args.steps = 0, w["T"]
     seed = SEEDS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -580,6 +589,8 @@ def main():
         # timed region) and each end-of-step call
         rec = []
         for i in range(first, first + n):
+            if timed and n > 4096 and (i - first) % 2048 == 0:
+                log("step %d of %d enqueued" % (i - first, n))
             j = i % RING
             lens = [B.ra_get_seq_info(h, b).len for b in range(Bsz)] if timed else None
             evs = []
