@@ -252,7 +252,8 @@ ra_status ra_end_step(ra_cache* cache, void* stream, int32_t* n_evicted);
 /* Run one eviction event on slot `seq` now, whatever the step count, if
  * its evictable rows exceed k_keep (otherwise a no-op).  Not allowed in
  * the middle of a step, nor with more than 1024 rows over k_keep (possible
- * only under RA_POLICY_EXTERNAL): RA_ERR_STATE.  The keys are Random
+ * only under RA_POLICY_EXTERNAL): RA_ERR_STATE; RA_ERR_UNSUPPORTED if such
+ * a pile-up makes more than 32768 candidate slots.  The keys are Random
  * Attention's (or the policy's). */
 ra_status ra_evict_now(ra_cache* cache, int32_t seq, void* stream);
 

@@ -457,6 +457,11 @@ ra_status ra_evict_now(ra_cache* c, int32_t seq, void* stream) {
   // the drop list of one event holds at most kMaxEvery rows (more can pile up
   // only when no end-of-step rule evicts, i.e. under the external policy)
   if (M.len - M.prompt_len - c->cfg.recent_r - M.k_keep > ra::kMaxEvery) return RA_ERR_STATE;
+  // the select holds every examined slot's key in registers: more slots than
+  // it supports (only reachable with rows piled up under the external policy)
+  if (M.len - M.prompt_len - (c->cfg.layout == RA_LAYOUT_HOLE_FILL ? 0 : c->cfg.recent_r) >
+      ra::kMaxCandidates)
+    return RA_ERR_UNSUPPORTED;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   RA_LAUNCH(ra::launch_plan_now(c->meta, seq, c->cfg.recent_r, s));
   for (int i = c->slot_lo; i < c->slot_hi; ++i) c->mirror[i].due = 0;

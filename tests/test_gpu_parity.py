@@ -169,6 +169,62 @@ def test_policy_large_select(policy, block, layout):
     run.close()
 
 
+@pytest.mark.parametrize("K,layout", [
+    (20000, B.RA_LAYOUT_CHRONOLOGICAL),
+    (20000, B.RA_LAYOUT_HOLE_FILL),
+    (32704, B.RA_LAYOUT_CHRONOLOGICAL),   # K + every = 32768 candidates, the largest
+    (32640, B.RA_LAYOUT_HOLE_FILL),       # K + every + r = 32768
+])
+def test_largest_select(K, layout):
+    """More than 16,384 candidates per head (the 1024-thread select with 32
+    keys per thread, up to the largest candidate count the library accepts):
+    kept sets after a positions-only fast forward through several events and
+    after an explicit event, with the rows compacted exactly."""
+    log("largest select K=%d layout=%d" % (K, layout))
+    run = Run(L=1, Hq=2, Hkv=2, K=K, lps=[129, 3], r=64, every=64, layout=layout,
+              seeds=[2**63 + 11, 5], rids=[2**40 + 1, 9])
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    n = K + 5 * 64 + 17
+    run.fast_forward(n)
+    for o in oracles:
+        o.advance(n)
+    assert oracles[0].rep.event >= 3
+    _check_heads(run, oracles, rows=False)
+    for s in range(run.n):
+        run.materialise(s)
+    for _ in range(5):
+        run.step()
+        for o in oracles:
+            o.rep.append()
+            o.rep.end_step()
+    for s in range(run.n):
+        B.ra_evict_now(run.h, s)
+        oracles[s].rep.evict_now()
+    _check_heads(run, oracles, rows=True)
+    run.close()
+
+
+def test_evict_now_rejects_oversize_selection():
+    """Under the external policy rows pile up past the budget; an explicit
+    event that would examine more than 32,768 slots is refused on the host
+    (nothing is launched) and leaves the state as it was."""
+    cfg = B.make_config(1, 2, 1, 32704, 64, 64, B.RA_BUDGET_EVICTABLE, B.RA_BF16, 1,
+                        policy=B.RA_POLICY_EXTERNAL)
+    cache = B.Cache(cfg, B.ra_seq_rows(cfg, 1))
+    h = cache.handle
+    B.ra_seq_begin(h, 0, 1, 3, 0, None, None)
+    info = B.ra_get_seq_info(h, 0)
+    B.ra_fast_forward(h, info.cap - info.len)
+    before = B.ra_get_seq_info(h, 0)
+    assert before.len == before.cap
+    with pytest.raises(B.RandAttnError) as err:
+        B.ra_evict_now(h, 0)
+    assert err.value.status == B.RA_ERR_UNSUPPORTED
+    after = B.ra_get_seq_info(h, 0)
+    assert (after.len, after.event) == (before.len, before.event)
+    cache.close()
+
+
 # (tag, KV heads, group, batch, K, wavefronts per item the plan must pick)
 PLAN_CASES = [
     ("12 wavefronts, 1 split", 8, 2, 25, 7600, 12),
