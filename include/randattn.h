@@ -180,6 +180,13 @@ int64_t ra_region_rows(const ra_config* cfg, int32_t prompt_len);
  * pool_rows int32.  Negative ra_status on error. */
 int64_t ra_seq_rows(const ra_config* cfg, int32_t prompt_len);
 
+/* Pool rows a batch of sequences occupies at once: the sum of ra_seq_rows
+ * over host_prompt_lens[0..n_seqs) (host memory).  The pool of
+ * ra_cache_create needs at least this many rows to hold them all.  Negative
+ * ra_status on error (bad config or argument, TOTAL mode with lp > K). */
+int64_t ra_required_slots(const ra_config* cfg, const int32_t* host_prompt_lens,
+                          int32_t n_seqs);
+
 /* Bytes of the persistent device metadata buffer (per-slot state).
  * 0 on a bad config. */
 size_t ra_meta_bytes(const ra_config* cfg);

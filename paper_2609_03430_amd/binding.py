@@ -36,7 +36,8 @@ RA_SCORER_SNAPKV, RA_SCORER_RKV, RA_SCORER_VASE = 0, 1, 2
 
 # Every entry point declared in include/randattn.h.
 EXPORTS = (
-    "ra_config_check", "ra_region_rows", "ra_seq_rows", "ra_meta_bytes",
+    "ra_config_check", "ra_region_rows", "ra_seq_rows", "ra_required_slots",
+    "ra_meta_bytes",
     "ra_workspace_bytes", "ra_cache_create", "ra_cache_destroy",
     "ra_seq_begin", "ra_seq_end", "ra_get_seq_info", "ra_decode_attention",
     "ra_end_step", "ra_evict_now", "ra_fast_forward", "ra_export_positions",
@@ -91,6 +92,7 @@ _SIGS = {
     "ra_config_check": (_I32, [_CFG]),
     "ra_region_rows": (_I64, [_CFG, _I32]),
     "ra_seq_rows": (_I64, [_CFG, _I32]),
+    "ra_required_slots": (_I64, [_CFG, ctypes.POINTER(ctypes.c_int32), _I32]),
     "ra_meta_bytes": (_SZ, [_CFG]),
     "ra_workspace_bytes": (_SZ, [_CFG]),
     "ra_cache_create": (_I32, [_CFG, _P, _P, _P, _I64, _P, _SZ, _P,
@@ -193,6 +195,12 @@ def ra_region_rows(cfg, prompt_len):
 
 def ra_seq_rows(cfg, prompt_len):
     return _lib().ra_seq_rows(ctypes.byref(cfg), int(prompt_len))
+
+
+def ra_required_slots(cfg, prompt_lens):
+    """Pool rows for a batch with these prompt lengths (a host list)."""
+    arr = (ctypes.c_int32 * len(prompt_lens))(*[int(x) for x in prompt_lens])
+    return _lib().ra_required_slots(ctypes.byref(cfg), arr, len(prompt_lens))
 
 
 def ra_meta_bytes(cfg):

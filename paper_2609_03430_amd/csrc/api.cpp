@@ -226,6 +226,19 @@ int64_t ra_seq_rows(const ra_config* c, int32_t prompt_len) {
   return rows * c->num_layers * c->num_kv_heads;
 }
 
+int64_t ra_required_slots(const ra_config* c, const int32_t* prompt_lens, int32_t n_seqs) {
+  if (!prompt_lens || n_seqs < 0) return RA_ERR_INVALID_ARG;
+  const ra_status st = ra_config_check(c);
+  if (st != RA_OK) return st;
+  int64_t total = 0;
+  for (int32_t i = 0; i < n_seqs; ++i) {
+    const int64_t rows = ra_seq_rows(c, prompt_lens[i]);
+    if (rows < 0) return rows;
+    total += rows;
+  }
+  return total;
+}
+
 size_t ra_meta_bytes(const ra_config* c) {
   if (ra_config_check(c) != RA_OK) return 0;
   const size_t metas = sizeof(SeqMeta) * static_cast<size_t>(c->max_seqs);

@@ -60,6 +60,10 @@ def test_region_sizes():
     assert B.ra_region_rows(t, 200) == 384               # 200 + 56 + 64 + 64
     assert B.ra_region_rows(t, 257) == B.RA_ERR_BUDGET
     assert B.ra_region_rows(t, -1) == B.RA_ERR_INVALID_ARG
+    assert B.ra_required_slots(c, [1024, 1, 0]) == sum(B.ra_seq_rows(c, lp) for lp in (1024, 1, 0))
+    assert B.ra_required_slots(c, []) == 0
+    assert B.ra_required_slots(t, [200, 257]) == B.RA_ERR_BUDGET
+    assert B.ra_required_slots(t, [200, -1]) == B.RA_ERR_INVALID_ARG
     assert B.ra_meta_bytes(c) >= 64 * 32
     assert B.ra_workspace_bytes(c) >= 32 * 8 * 64 * 5 * 130 * 4
 
