@@ -28,7 +28,7 @@ def _qwin(run, steps_done):
     return qw
 
 
-@pytest.mark.parametrize("Hq,Hkv", [(8, 2), (10, 2), (4, 4)])
+@pytest.mark.parametrize("Hq,Hkv", [(8, 2), (10, 2), (4, 4), (16, 2), (32, 2)])
 def test_window_scores_and_selection(Hq, Hkv):
     log("window scorer Hq=%d Hkv=%d" % (Hq, Hkv))
     L, K, r, every = 2, 200, 64, 64
