@@ -166,6 +166,9 @@ def evict_cost(B, torch, Workload, methods=("random", "snapkv")):
     stream = torch.cuda.current_stream()
     scorers = {"snapkv": B.RA_SCORER_SNAPKV, "rkv": B.RA_SCORER_RKV,
                "vase": B.RA_SCORER_VASE}
+    # "random-holefill": Random Attention's round with the hole-fill layout
+    # (the same kept sets; only the surviving rows of the last m slots move)
+    layouts = {"random-holefill": B.RA_LAYOUT_HOLE_FILL}
     res = {"metric": "eviction round ms per layer (scoring + selection + compaction)",
            "protocol": "1 sequence, K=1024 incl. prompt 300, r=64, every 64, 4096 "
                        "decode steps from the prompt, distinct rows every step, HIP events, "
@@ -195,10 +198,11 @@ def evict_cost(B, torch, Workload, methods=("random", "snapkv")):
             # each method first runs an untimed 1,024-step copy of the protocol
             # (4 rounds), so that no round pays a kernel's first-launch cost
             timed = run_steps == steps
-            scored = method != "random"
+            scored = method in scorers
             policy = B.RA_POLICY_EXTERNAL if scored else B.RA_POLICY_RANDOM
             cfg = B.make_config(L, Hq, Hkv, K, R, EVERY, B.RA_BUDGET_TOTAL, B.RA_BF16, 1,
-                                policy=policy)
+                                policy=policy,
+                                layout=layouts.get(method, B.RA_LAYOUT_CHRONOLOGICAL))
             cache = B.Cache(cfg, B.ra_seq_rows(cfg, lp), device=dev)
             h = cache.handle
             B.ra_seq_begin(h, 0, lp, 77, 0, kp, vp)
@@ -467,8 +471,9 @@ def main():
                          "(staggered compressions, requests finishing and replaced); "
                          "prints its own JSON line; --steps sets the window")
     ap.add_argument("--evict-cost-methods", default="random,snapkv",
-                    help="comma-separated rounds timed by --evict-cost: random and the "
-                         "score-based snapkv, rkv, vase")
+                    help="comma-separated rounds timed by --evict-cost: random, "
+                         "random-holefill (the hole-fill layout) and the score-based "
+                         "snapkv, rkv, vase")
     ap.add_argument("--window-scorer", action="store_true",
                     help="also time the observation-window scoring pass (always on for "
                          "phi4-ragged)")
