@@ -205,3 +205,27 @@ class OracleSeq:
 
 def max_abs(a, b):
     return float(np.max(np.abs(np.asarray(a, dtype=np.float64) - np.asarray(b, dtype=np.float64))))
+
+
+# Tolerances the workloads fix for attention against the fp64 oracle.
+TOL = {B.RA_BF16: 2e-2, B.RA_F32: 1e-5}
+
+
+def check_heads(run, oracles, rows=True):
+    """Kept positions equal the oracle's (as a sorted list in the hole-fill
+    layout, whose rows are unordered), and every row holds its position's
+    key and value."""
+    holefill = run.layout == B.RA_LAYOUT_HOLE_FILL
+    for o in oracles:
+        for (layer, g) in o.heads:
+            got = run.positions(o.slot, layer, g)
+            want = o.rep.P[(layer, g)]
+            if holefill:
+                assert len(set(got.tolist())) == len(got)
+                got = np.sort(got)
+            assert np.array_equal(got, want), (o.slot, layer, g, o.rep.step)
+            if rows:
+                k, v = run.rows(o.slot, layer, g, by_position=holefill)
+                kw, vw = o.rows(layer, g, want)
+                assert torch.equal(k, kw), (o.slot, layer, g)
+                assert torch.equal(v, vw), (o.slot, layer, g)

@@ -10,33 +10,11 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_harness import OracleSeq, Run, log, max_abs
+from gpu_harness import TOL, OracleSeq, Run, log, max_abs
+from gpu_harness import check_heads as _check_heads
 from paper_2609_03430_amd import binding as B
 
 pytestmark = pytest.mark.gpu
-
-TOL = {B.RA_BF16: 2e-2, B.RA_F32: 1e-5}
-
-
-def _check_heads(run, oracles, rows=True):
-    """Kept positions equal the oracle's (as a sorted list in the hole-fill
-    layout, whose rows are unordered), and every row holds its position's
-    key and value."""
-    holefill = run.layout == B.RA_LAYOUT_HOLE_FILL
-    for o in oracles:
-        for (layer, g) in o.heads:
-            got = run.positions(o.slot, layer, g)
-            want = o.rep.P[(layer, g)]
-            if holefill:
-                assert len(set(got.tolist())) == len(got)
-                got = np.sort(got)
-            assert np.array_equal(got, want), (o.slot, layer, g, o.rep.step)
-            if rows:
-                k, v = run.rows(o.slot, layer, g, by_position=holefill)
-                kw, vw = o.rows(layer, g, want)
-                assert torch.equal(k, kw), (o.slot, layer, g)
-                assert torch.equal(v, vw), (o.slot, layer, g)
-
 
 @pytest.mark.parametrize("layout", [B.RA_LAYOUT_CHRONOLOGICAL, B.RA_LAYOUT_HOLE_FILL])
 @pytest.mark.parametrize("dtype", [B.RA_BF16, B.RA_F32])
