@@ -25,6 +25,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -71,11 +72,25 @@ EVERY = 64
 RING = 64
 
 
-def kernel_source_hash():
+def code_of(text):
+    """Source text without comments and blank space: what the compiler sees
+    of it, so that a comment edit does not count as a kernel change."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
+def kernel_source_hash(read=None):
+    """Hash of the code of the attention and eviction kernels (the traffic
+    measured by rocprofv3 counters is reported only while it matches)."""
     h = hashlib.sha256()
     for name in ("attention.hip", "evict.hip"):
-        with open(os.path.join(ROOT, "paper_2609_03430_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        if read is None:
+            with open(os.path.join(ROOT, "paper_2609_03430_amd", "csrc", name)) as f:
+                text = f.read()
+        else:
+            text = read(name)
+        h.update(code_of(text).encode())
     return h.hexdigest()[:16]
 
 

@@ -3,15 +3,18 @@
 // alpha = softmax_i(q . k_i / sqrt(d)); Appendix F: the G query heads of a
 // group read their KV head's cache).
 //
-// Work decomposition: one wavefront per (sequence, KV head, split of
-// `split_keys` keys).  Each wavefront reads its keys and values exactly once
-// for all G query heads of the group, keeps an online softmax (running max
-// and sum, combined across lanes with wavefront shuffles), and writes an
-// unnormalised partial; a small second kernel merges the partials of each
-// head and writes the output.  The step's new key/value is read from the
-// input buffers by the wavefront that owns the last key, which also stores
-// it into the cache after its reads, so no wavefront of the launch reads a
-// row that is being written.
+// Work decomposition: one workgroup of W wavefronts per (sequence, KV head,
+// split of `split_keys` keys); wavefront v streams the v-th W-th of the
+// split.  Each wavefront reads its keys and values exactly once for all G
+// query heads of the group and keeps an online softmax (running max and sum,
+// combined across lanes with wavefront shuffles); the W states merge in LDS.
+// A head with one split writes its normalised output directly; otherwise
+// every split writes an unnormalised partial and a small second kernel
+// merges them.  The step's new key/value is read from the input buffers by
+// the wavefront that owns the last key, which also stores it into the cache
+// after its reads, so no wavefront of the launch reads a row that is being
+// written.  Value tiles are read with nontemporal loads, key rows with
+// ordinary ones.
 //
 // bf16 path (MFMA, v_mfma_f32_16x16x32_bf16, 16x16 output tiles):
 //   S^T[key][query] = K . Q^T   A = 16 key rows x 32 channels, B = Q^T with
