@@ -7,7 +7,7 @@
 //   1. every candidate slot (outside the prompt and the r most recent rows)
 //      gets its 64-bit Philox score, held in registers (KPT per thread, in
 //      slot order);
-//   2. an MSB-first radix select over the composite (score, candidate index)
+//   2. an MSB-first radix select over the composite (score, position)
 //      finds the m = |C| - k_keep smallest (select.h);
 //   3. a block scan turns the drop flags into the sorted drop list, stored as
 //      f[k] = d_k - k, so that destination row j receives source row
