@@ -131,10 +131,13 @@ struct Plan {
 };
 
 Plan attention_plan(const ra_cache* c) {
-  int cap_max = 32, n_active = 0;
+  // sized by the longest cache of this step (cached rows + the new one), so
+  // that while sequences are younger than their budget no wavefront or split
+  // is planned over rows that do not exist yet
+  int keys_max = 32, n_active = 0;
   for (int s = c->slot_lo; s < c->slot_hi; ++s) {
     if (!c->mirror[s].active) continue;
-    cap_max = std::max(cap_max, c->mirror[s].cap);
+    keys_max = std::max(keys_max, c->mirror[s].len + 1);
     ++n_active;
   }
   const int heads = std::max(1, n_active * c->cfg.num_kv_heads);
@@ -148,7 +151,7 @@ Plan attention_plan(const ra_cache* c) {
       p.waves = 4;
     } else {
       splits = std::max(1, (256 + heads / 2) / heads);
-      const int keys = (cap_max + splits - 1) / splits;
+      const int keys = (keys_max + splits - 1) / splits;
       p.waves = keys >= 12 * 640 ? 12 : keys >= 8 * 256 ? 8 : keys >= 4 * 128 ? 4 : 1;
       p.wide_regs = p.waves == 4;
     }
@@ -158,10 +161,10 @@ Plan attention_plan(const ra_cache* c) {
   splits = std::min(ra::kMaxSplits, splits);
   const int unit = 32 * p.waves;
   int sk = c->cfg.attn_split > 0 ? static_cast<int>(round_up(c->cfg.attn_split, unit))
-                                 : static_cast<int>(round_up((cap_max + splits - 1) / splits, unit));
-  sk = std::max<int>(sk, static_cast<int>(round_up((cap_max + ra::kMaxSplits - 1) / ra::kMaxSplits, unit)));
+                                 : static_cast<int>(round_up((keys_max + splits - 1) / splits, unit));
+  sk = std::max<int>(sk, static_cast<int>(round_up((keys_max + ra::kMaxSplits - 1) / ra::kMaxSplits, unit)));
   p.split_keys = sk;
-  p.max_splits = (cap_max + sk - 1) / sk;
+  p.max_splits = (keys_max + sk - 1) / sk;
   return p;
 }
 
