@@ -56,3 +56,22 @@ def test_vectorised_broadcasts_scalars():
     out = philox4x64_10_np(np.arange(5, dtype=np.uint64), 3, 2, 1, 99, 2**63 + 5)
     for i in range(5):
         assert tuple(int(o[i]) for o in out) == philox4x64_10((i, 3, 2, 1), (99, 2**63 + 5))
+
+
+@pytest.mark.parametrize("trial", range(6))
+def test_position_keys_follow_the_counter_layout(trial):
+    """The key of position p at event e, layer l, KV head g of request
+    (seed, request id) is word p mod 4 of the Philox4x64-10 block at counter
+    (p / 4, e, l, g) under key (seed, request id): checked word by word
+    against numpy's generator, so a wrong counter field, key order or word
+    choice fails here (the uniformity pins cannot see such a mistake)."""
+    from oracle.evict import position_keys
+    rng = np.random.default_rng(99 + trial)
+    seed = int(rng.integers(0, 2**63)) * 2 + trial % 2
+    rid = int(rng.integers(0, 2**40))
+    event, layer, head = int(rng.integers(0, 500)), int(rng.integers(0, 64)), int(rng.integers(0, 16))
+    p = np.sort(rng.choice(40000, 24, replace=False))
+    got = position_keys(p, seed, rid, event, layer, head)
+    for pi, key in zip(p.tolist(), got.tolist()):
+        block = _numpy_block((pi // 4, event, layer, head), (seed, rid))
+        assert key == block[pi % 4], (pi, event, layer, head)
