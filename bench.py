@@ -268,6 +268,57 @@ def evict_cost(B, torch, Workload, methods=("random", "snapkv")):
     return res
 
 
+def tiny_latency(B, torch, Workload):
+    """Per-step latency of the tiny case: 1 layer, 4 query / 2 KV heads,
+    head_dim 128, fp32 N(0,1) rows, prompt 128, r=64, K=256, eviction every
+    64 steps, 1024 decode steps from the pinned prompt (11 events).  A
+    latency case, not a roofline one: the cache is under 1 MB."""
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    L, Hq, Hkv, K, lp, T = 1, 4, 2, 256, 128, 1024
+    cfg = B.make_config(L, Hq, Hkv, K, R, EVERY, B.RA_BUDGET_EVICTABLE, B.RA_F32, 1)
+    wl = Workload(1000, L, Hq, Hkv, 128, torch.float32, False, device=dev)
+    ls = torch.arange(L, device=dev).view(-1, 1, 1)
+    gs = torch.arange(Hkv, device=dev).view(1, -1, 1)
+    ps = torch.arange(lp, device=dev).view(1, 1, -1)
+    kp = wl.k_rows(0, ls, gs, ps, lp).contiguous()
+    vp = wl.v_rows(0, ls, gs, ps, lp).contiguous()
+    zero = torch.zeros(T, dtype=torch.long, device=dev)
+    st = torch.arange(T, device=dev)
+    qs = wl.q_step(zero, 0, st)                                # [T][Hq][128]
+    ks, vs = wl.kv_step(zero, 0, lp + st, zero + lp)           # [T][Hkv][128]
+    out = torch.empty(1, Hq, 128, dtype=torch.float32, device=dev)
+    result = {}
+    for run in ("warm-up", "timed"):
+        cache = B.Cache(cfg, B.ra_seq_rows(cfg, lp), device=dev)
+        h = cache.handle
+        B.ra_seq_begin(h, 0, lp, 1000 * 1000003, 0, kp, vp)
+        torch.cuda.synchronize()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        events = 0
+        t0 = time.perf_counter()
+        e0.record(stream)
+        for t in range(T):
+            B.ra_decode_attention(h, 0, qs[t].unsqueeze(0), ks[t].unsqueeze(0),
+                                  vs[t].unsqueeze(0), out, cache.workspace, stream)
+            events += B.ra_end_step(h, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        cache.close()
+        result = {
+            "metric": "tiny-case decode step latency (append + attention + end of step)",
+            "config": {"workload": "1 layer, 4 Q / 2 KV heads, head_dim 128, fp32, prompt 128, "
+                                   "K=256, r=64, evict every 64, 1024 steps from the prompt"},
+            "steps": T,
+            "events": events,
+            "us_per_step_gpu": e0.elapsed_time(e1) * 1e3 / T,
+            "us_per_step_wall": wall * 1e6 / T,
+        }
+    return result
+
+
 def serving(B, torch, Workload, steps, log):
     """Continuous batching of a request stream (the paper's serving regime:
     staggered compressions, requests finishing and being replaced).
@@ -492,6 +543,9 @@ def main():
     ap.add_argument("--window-scorer", action="store_true",
                     help="also time the observation-window scoring pass (always on for "
                          "phi4-ragged)")
+    ap.add_argument("--tiny", action="store_true",
+                    help="per-step latency of the tiny fp32 case (1 layer, 4/2 heads, "
+                         "prompt 128, K=256, 1024 steps); prints its own JSON line")
     ap.add_argument("--full-run", action="store_true",
                     help="time the whole generation from the prompt (steps 1..32768, no "
                          "warm-up) instead of the steady-state window at its end; about "
@@ -528,6 +582,10 @@ def main():
     if args.evict_cost:
         print(json.dumps(evict_cost(B, torch, Workload, tuple(args.evict_cost_methods.split(",")))),
               flush=True)
+        return
+
+    if args.tiny:
+        print(json.dumps(tiny_latency(B, torch, Workload)), flush=True)
         return
 
     w = WORKLOADS[args.workload]
