@@ -1,0 +1,103 @@
+"""Protocol and argument errors of the C ABI on a live cache.
+
+Every call below is refused on the host, before any launch, with the status
+the header documents; afterwards the state is what it was (the host mirror
+and the device agree: a normal step still decodes to the oracle's output and
+keeps the oracle's positions).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+from gpu_harness import TOL, OracleSeq, Run, check_heads, log, max_abs
+from paper_2609_03430_amd import binding as B
+
+pytestmark = pytest.mark.gpu
+
+
+def _status(fn, *args, **kw):
+    try:
+        fn(*args, **kw)
+    except B.RandAttnError as e:
+        return e.status
+    return B.RA_OK
+
+
+def _infos(run):
+    return [(i.active, i.len, i.step, i.event) for i in
+            (B.ra_get_seq_info(run.h, s) for s in range(run.max_seqs))]
+
+
+def test_refused_calls_leave_the_state_unchanged():
+    log("protocol errors")
+    run = Run(L=2, Hq=4, Hkv=2, K=24, lps=[5, 9], r=8, every=8, max_seqs=3)
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    for t in range(30):
+        run.step()
+        for o in oracles:
+            o.rep.append()
+            o.rep.end_step()
+    before = _infos(run)
+    q, k, v = run.step_inputs(0)
+    out = torch.empty(run.max_seqs, run.Hq, 128, dtype=torch.bfloat16, device="cuda")
+    ws = run.cache.workspace
+
+    # between steps
+    assert _status(B.ra_end_step, run.h) == B.RA_ERR_STATE          # no layer appended
+    assert _status(B.ra_seq_begin, run.h, 0, 4, 1, 0) == B.RA_ERR_STATE   # slot active
+    assert _status(B.ra_seq_begin, run.h, 3, 4, 1, 0) == B.RA_ERR_INVALID_ARG  # slot range
+    assert _status(B.ra_seq_begin, run.h, 2, 10**6, 1, 0) == B.RA_ERR_CAPACITY  # no room
+    assert _status(B.ra_seq_end, run.h, 2) == B.RA_ERR_STATE         # slot not active
+    assert _status(B.ra_decode_attention, run.h, 2, q, k, v, out, ws) == B.RA_ERR_INVALID_ARG
+    assert _status(B.ra_decode_attention, run.h, 0, q, k, v, out, ws[:16]) == \
+        B.RA_ERR_INVALID_ARG                                         # workspace too small
+    assert _status(B.ra_read_positions, run.h, 0, 0, 0, 3) == B.RA_ERR_CAPACITY
+    assert _status(B.ra_window_select, run.h, 0, 2,
+                   torch.zeros(3, 2, 4, 64, 128, dtype=torch.bfloat16, device="cuda"),
+                   None, 0, None) == B.RA_ERR_STATE                 # fewer than 64 steps
+    assert _infos(run) == before
+
+    # inside an open step (layer 0 appended)
+    B.ra_decode_attention(run.h, 0, q, k, v, out, ws)
+    assert _status(B.ra_decode_attention, run.h, 0, q, k, v, out, ws) == B.RA_ERR_STATE
+    assert _status(B.ra_end_step, run.h) == B.RA_ERR_STATE          # layer 1 missing
+    assert _status(B.ra_seq_begin, run.h, 2, 4, 1, 0) == B.RA_ERR_STATE
+    assert _status(B.ra_seq_end, run.h, 0) == B.RA_ERR_STATE
+    assert _status(B.ra_evict_now, run.h, 0) == B.RA_ERR_STATE
+    assert _status(B.ra_fast_forward, run.h, 1) == B.RA_ERR_STATE
+    # finish the step normally: the outputs and positions are the oracle's
+    q1, k1, v1 = run.step_inputs(1)
+    out1 = torch.empty_like(out)
+    B.ra_decode_attention(run.h, 1, q1, k1, v1, out1, ws)
+    B.ra_end_step(run.h)
+    run.steps = [s + 1 for s in run.steps]
+    for o in oracles:
+        o.rep.append()
+        for layer, got in ((0, out), (1, out1)):
+            err = max_abs(got[o.slot].float().cpu(), o.attend(layer, 30))
+            assert err <= TOL[B.RA_BF16], (layer, o.slot, err)
+        o.rep.end_step()
+    check_heads(run, oracles)
+    run.close()
+
+
+def test_total_budget_refuses_a_prompt_longer_than_k():
+    cfg = B.make_config(1, 2, 1, 16, 8, 8, B.RA_BUDGET_TOTAL, B.RA_BF16, 2)
+    cache = B.Cache(cfg, B.ra_seq_rows(cfg, 16))
+    assert _status(B.ra_seq_begin, cache.handle, 0, 17, 1, 0) == B.RA_ERR_BUDGET
+    assert B.ra_get_seq_info(cache.handle, 0).active == 0
+    B.ra_seq_begin(cache.handle, 0, 16, 1, 0)           # k_keep = 0 is allowed
+    assert B.ra_get_seq_info(cache.handle, 0).k_keep == 0
+    cache.close()
+
+
+def test_window_select_needs_the_chronological_layout():
+    cfg = B.make_config(1, 2, 1, 16, 8, 8, B.RA_BUDGET_EVICTABLE, B.RA_BF16, 1,
+                        layout=B.RA_LAYOUT_HOLE_FILL)
+    cache = B.Cache(cfg, B.ra_seq_rows(cfg, 4))
+    B.ra_seq_begin(cache.handle, 0, 4, 1, 0)
+    qw = torch.zeros(1, 1, 2, 64, 128, dtype=torch.bfloat16, device="cuda")
+    assert _status(B.ra_window_select, cache.handle, 0, 1, qw, None, 0, None) == \
+        B.RA_ERR_UNSUPPORTED
+    cache.close()
