@@ -13,7 +13,7 @@
 //      f[k] = d_k - k, so that destination row j receives source row
 //      j + #{k : f[k] <= j};
 //   4. chronological layout (the paper's): the surviving rows are moved
-//      down in chunks of 128 destination rows:
+//      down in chunks of destination rows (512 for bf16 with 1,024 threads):
 //      every thread gathers its part of the chunk into registers, the block
 //      waits until all loads have returned and synchronises, then writes.
 //      Sources are never below destinations and a chunk's writes land below
@@ -30,7 +30,15 @@ namespace {
 
 using u32x4 = uint32_t __attribute__((ext_vector_type(4)));
 
-constexpr int kChunk = 128;   // destination rows moved per barrier round
+// Destination rows moved per barrier round: as many as give every thread 8
+// key units and 8 value units of 16 bytes in flight (512 rows of bf16 or 256
+// of fp32 for 1,024 threads).  Each round waits for all of its loads, so the
+// bytes in flight per workgroup set the move's rate (rounds of 128 rows ran
+// 9% slower on a full event of the Qwen3-14B shape).
+template <int NT, typename E>
+constexpr int chunk_rows() {
+  return NT * 8 / (kHeadDim * static_cast<int>(sizeof(E)) / 16);
+}
 
 // Number of f[k] <= x for the non-decreasing list f[0..m).
 __device__ __forceinline__ int count_le(const int* f, int m, int x) {
@@ -132,9 +140,9 @@ __device__ __forceinline__ u32x4 funnel8(u32x4 a, u32x4 b, int off) {
 // Order-preserving in-place compaction of one head's region: destination
 // row j < new_len (from the first drop d0 on) receives source row
 // j + #{k : f[k] <= j}, where f[k] = d_k - k for the ascending drop list d.
-// Chunks of kChunk destination rows: every thread gathers its part of the
-// chunk into registers, the block waits until all loads have returned and
-// synchronises, then writes.  Sources are never below destinations and a
+// Chunks of chunk_rows<NT, E>() destination rows: every thread gathers its
+// part of the chunk into registers, the block waits until all loads have
+// returned and synchronises, then writes.  Sources are never below destinations and a
 // chunk's writes land below the next chunk's sources, so the move is
 // race-free.  Called by every thread of the workgroup.
 template <int NT, typename E, bool POS_ONLY>
@@ -145,6 +153,8 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
   constexpr int kEpu = 16 / sizeof(E);            // elements per 16-byte unit
   constexpr int kKUnitsRow = kHeadDim / kEpu;     // 16-byte units per key row
   constexpr int kVUnitsCh = 8 / kEpu;             // units per (tile, channel)
+  constexpr int kChunk = chunk_rows<NT, E>();
+  static_assert(kChunk % 8 == 0 && kChunk <= NT, "a chunk is whole value tiles, one row per thread");
   constexpr int kKUnits = kChunk * kKUnitsRow;
   constexpr int kVUnits = (kChunk / 8) * kHeadDim * kVUnitsCh;
   constexpr int kKPer = (kKUnits + NT - 1) / NT;
@@ -328,7 +338,7 @@ __global__ __launch_bounds__(NT) void evict_kernel(
   }
 
   // 4. order-preserving in-place compaction of positions, keys and values
-  __shared__ int src_of[kChunk];
+  __shared__ int src_of[chunk_rows<NT, E>()];
   compact_rows<NT, E, POS_ONLY>(f, m, src_of, d0, new_len, old_len, region, kpool, vpool, P);
 }
 
@@ -342,7 +352,7 @@ __global__ __launch_bounds__(NT) void compact_drops_kernel(
     int32_t* __restrict__ pos, const int32_t* __restrict__ drops, int stride, int L,
     int Hkv, int slot_lo) {
   __shared__ int f[kMaxEvery];
-  __shared__ int src_of[kChunk];
+  __shared__ int src_of[chunk_rows<NT, E>()];
   const int per_seq = L * Hkv;
   const int slot = slot_lo + static_cast<int>(blockIdx.x) / per_seq;
   const int lg = static_cast<int>(blockIdx.x) % per_seq;
@@ -392,19 +402,21 @@ template <bool POS_ONLY>
 hipError_t launch_mode(const Shape& sh, const SeqMeta* meta, void* kpool,
                        void* vpool, int32_t* pos, int slot_lo, int slot_hi,
                        int max_candidates, hipStream_t s) {
-  if (max_candidates <= 512 * 1)
-    return launch_kpt<512, 1, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
-  if (max_candidates <= 512 * 2)
-    return launch_kpt<512, 2, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
-  if (max_candidates <= 512 * 4)
-    return launch_kpt<512, 4, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
-  if (max_candidates <= 512 * 8)
-    return launch_kpt<512, 8, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
-  if (max_candidates <= 512 * 16)
-    return launch_kpt<512, 16, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
-  // more than 16 scores per thread is kept for the largest budgets only: 32
-  // unrolled Philox evaluations exceed the compiler's unroll budget and the
-  // score array then lives in scratch memory
+  // 1,024 threads, KPT scores each: the smallest KPT that holds the
+  // candidates (C = K + 64 at the usual budgets: K = 1,024 -> 2, 2,048 -> 3,
+  // 4,096 -> 5, 8,192 -> 9).  More than 16 scores per thread is kept for the
+  // largest budgets only: 32 unrolled Philox evaluations exceed the
+  // compiler's unroll budget and the score array then lives in scratch memory.
+  if (max_candidates <= 1024 * 1)
+    return launch_kpt<1024, 1, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+  if (max_candidates <= 1024 * 2)
+    return launch_kpt<1024, 2, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+  if (max_candidates <= 1024 * 3)
+    return launch_kpt<1024, 3, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+  if (max_candidates <= 1024 * 5)
+    return launch_kpt<1024, 5, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+  if (max_candidates <= 1024 * 9)
+    return launch_kpt<1024, 9, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
   if (max_candidates <= 1024 * 16)
     return launch_kpt<1024, 16, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
   if (max_candidates <= kMaxCandidates)
@@ -420,11 +432,11 @@ hipError_t launch_compact_drops(const Shape& sh, const SeqMeta* meta, void* kpoo
   if (slot_hi <= slot_lo) return hipSuccess;
   const dim3 grid((slot_hi - slot_lo) * sh.L * sh.Hkv);
   if (sh.dtype == 1)
-    hipLaunchKernelGGL((compact_drops_kernel<512, uint16_t>), grid, dim3(512), 0, s, meta,
+    hipLaunchKernelGGL((compact_drops_kernel<1024, uint16_t>), grid, dim3(1024), 0, s, meta,
                        static_cast<uint16_t*>(kpool), static_cast<uint16_t*>(vpool), pos,
                        drops, stride, sh.L, sh.Hkv, slot_lo);
   else
-    hipLaunchKernelGGL((compact_drops_kernel<512, float>), grid, dim3(512), 0, s, meta,
+    hipLaunchKernelGGL((compact_drops_kernel<1024, float>), grid, dim3(1024), 0, s, meta,
                        static_cast<float*>(kpool), static_cast<float*>(vpool), pos,
                        drops, stride, sh.L, sh.Hkv, slot_lo);
   return hipGetLastError();
