@@ -94,15 +94,27 @@ def kernel_source_hash(read=None):
     return h.hexdigest()[:16]
 
 
-def read_traffic(workload):
-    """HBM traffic per attention launch measured with rocprofv3 counters, if a
-    summary for the current kernel sources exists under profiles/."""
-    path = os.path.join(ROOT, "profiles", "attention_traffic_%s.json" % workload)
+def run_signature(args):
+    """The settings that decide which launches a run times."""
+    return {"workload": args.workload, "steps": args.steps, "warmup": args.warmup,
+            "layout": args.layout, "policy": args.policy,
+            "block": args.block if args.policy == "block" else None,
+            "attn_split": args.attn_split}
+
+
+def read_traffic(signature):
+    """HBM traffic per attention launch measured with rocprofv3 counters (the
+    mean over the timed launches of one run), if a summary for the current
+    kernel sources and for a run with the same settings exists under
+    profiles/."""
+    path = os.path.join(ROOT, "profiles", "attention_traffic_%s.json" % signature["workload"])
     if not os.path.exists(path):
         return None
     with open(path) as f:
         d = json.load(f)
     if d.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    if d.get("run") != signature:
         return None
     return d.get("hbm_bytes_per_launch")
 
@@ -509,7 +521,7 @@ def time_window_scorer(B, torch, h, wl, cfg, Bsz, L, Hq, Hkv, stream, comp, log)
     return out
 
 
-def main():
+def build_parser():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=256)
@@ -553,7 +565,11 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device-to-device copy three times (the "
                          "known-size reference for the HBM byte counters)")
-    args = ap.parse_args()
+    return ap
+
+
+def main():
+    args = build_parser().parse_args()
 
     if args.gpus != 1:
         print("bench.py runs on one GPU only: the hot path has no cross-GPU step; "
@@ -674,7 +690,7 @@ def main():
         # timed region) and each end-of-step call
         rec = []
         for i in range(first, first + n):
-            if timed and n > 4096 and (i - first) % 2048 == 0:
+            if timed and (i - first) % (2048 if n > 4096 else 64) == 0:
                 log("step %d of %d enqueued" % (i - first, n))
             j = i % RING
             lens = [B.ra_get_seq_info(h, b).len for b in range(Bsz)] if timed else None
@@ -801,7 +817,7 @@ def main():
             "peak": PEAK_HBM_GBS,
             "unit": "GB/s",
             "frac": attn_gbs / PEAK_HBM_GBS,
-            "traffic": read_traffic(args.workload),
+            "traffic": read_traffic(run_signature(args)),
             "avg_launch_ms": attn_avg_ms,
             "avg_launch_note": "HIP events around each step's launches of all layers, "
                                "divided by the layer count (inter-kernel gaps included)",

@@ -1,5 +1,6 @@
 """bench.py's host-side contract, checked without a GPU."""
 
+import json
 import os
 import subprocess
 import sys
@@ -27,3 +28,25 @@ def test_ragged_plan_is_seeded_and_in_range():
     assert gens == sorted(gens, reverse=True)
     lps, starts = bench.sequence_plan("qwen3-14b", bench.WORKLOADS["qwen3-14b"], 320)
     assert lps == [1024] * 32 and starts == [32768 - 320] * 32
+
+
+def test_traffic_is_reported_only_for_the_profiled_run(monkeypatch):
+    """The stored counter traffic is the mean over the timed launches of one
+    run (the default bench line); a run with other settings, or kernels
+    changed since, reports none."""
+    sys.path.insert(0, ROOT)
+    import bench
+    with open(os.path.join(ROOT, "profiles", "attention_traffic_qwen3-14b.json")) as f:
+        stored = json.load(f)
+    default = bench.run_signature(bench.build_parser().parse_args([]))
+    assert stored["run"] == default
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda read=None: stored["kernel_source_hash"])
+    assert bench.read_traffic(default) == stored["hbm_bytes_per_launch"]
+    for key, other in [("steps", 2), ("warmup", 0), ("layout", "holefill"),
+                       ("policy", "shared"), ("attn_split", 4096)]:
+        assert bench.read_traffic(dict(default, **{key: other})) is None, key
+    full = bench.build_parser().parse_args(["--full-run"])
+    full.warmup, full.steps = 0, bench.WORKLOADS["qwen3-14b"]["T"]   # as main() sets them
+    assert bench.read_traffic(bench.run_signature(full)) is None
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda read=None: "0" * 16)
+    assert bench.read_traffic(default) is None
