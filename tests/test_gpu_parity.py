@@ -182,6 +182,36 @@ def test_largest_select(K, layout):
     run.close()
 
 
+@pytest.mark.parametrize("C,layout", [
+    (c, B.RA_LAYOUT_CHRONOLOGICAL) for c in
+    (1024, 1025, 2048, 2049, 3072, 3073, 5120, 5121, 9216, 9217, 16384, 16385)
+] + [(3073, B.RA_LAYOUT_HOLE_FILL), (16385, B.RA_LAYOUT_HOLE_FILL)])
+def test_select_size_boundaries(C, layout):
+    """An explicit event with exactly C candidates per head, on and just past
+    each boundary of the selection's scores-per-thread builds (1,024 threads
+    x 1, 2, 3, 5, 9, 16): kept sets and compacted rows as the oracle's.  With
+    a trigger period of 1,024 steps nothing is evicted during the positions-
+    only fast forward of C + r steps, so the event sees all C positions."""
+    log("select size boundary C=%d layout=%d" % (C, layout))
+    r = 64
+    run = Run(L=1, Hq=2, Hkv=2, K=C - 64, lps=[129, 3], r=r, every=1024, layout=layout,
+              seeds=[2**63 + 11, 5], rids=[2**40 + 1, 9])
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    run.fast_forward(C + r)
+    for o in oracles:
+        o.advance(C + r)
+        assert o.rep.event == 0
+    for s in range(run.n):
+        run.materialise(s)
+        info = B.ra_get_seq_info(run.h, s)
+        assert info.len - info.prompt_len - r == C
+    for s in range(run.n):
+        B.ra_evict_now(run.h, s)
+        oracles[s].rep.evict_now()
+    _check_heads(run, oracles, rows=True)
+    run.close()
+
+
 def test_evict_now_rejects_oversize_selection():
     """Under the external policy rows pile up past the budget; an explicit
     event that would examine more than 32,768 slots is refused on the host
