@@ -27,8 +27,11 @@
  * - Every call returns an ra_status.  Shapes, capacities, budgets and the
  *   step protocol are validated on the host mirror BEFORE any launch, so an
  *   error leaves device state untouched.  A failed launch returns
- *   RA_ERR_HIP (ra_last_hip_error gives the hipError_t).  Nothing throws
- *   across the ABI.
+ *   RA_ERR_HIP (ra_last_hip_error gives the hipError_t); after RA_ERR_HIP
+ *   from a call that launches several kernels (ra_seq_begin, ra_end_step,
+ *   ra_evict_now, ra_fast_forward, ra_scored_evict) the host mirror and the
+ *   device state may disagree, and the cache should be destroyed.  Nothing
+ *   throws across the ABI.
  * - head_dim must be 128; dtype f32 or bf16 (keys, values, queries and
  *   outputs all in that dtype); positions are int32.
  *
@@ -270,7 +273,10 @@ ra_status ra_evict_now(ra_cache* cache, int32_t seq, void* stream);
  * only: each step caches position lp + step and the periodic eviction runs
  * on the positions exactly as in a real decode, but no key/value rows are
  * written or moved (rows of newly cached positions are left stale).  Used
- * to reach a long-generation state quickly; follow with ra_write_rows. */
+ * to reach a long-generation state quickly; follow with ra_write_rows.
+ * RA_ERR_STATE inside an open step; RA_ERR_CAPACITY, before any launch, if
+ * some sequence would outgrow its region on the way (only possible under
+ * RA_POLICY_EXTERNAL, whose rows are evicted by explicit rounds only). */
 ra_status ra_fast_forward(ra_cache* cache, int32_t n_steps, void* stream);
 
 /* Copy slot `seq`'s cached positions, [L][Hkv][len] int32 row-major, to

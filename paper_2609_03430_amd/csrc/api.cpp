@@ -494,33 +494,47 @@ ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
   if (c->step_open()) return RA_ERR_STATE;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const int every = c->cfg.evict_every;
-  int remaining = n_steps;
-  while (remaining > 0 && c->slot_hi > c->slot_lo) {
-    int run = remaining;
-    for (int i = c->slot_lo; i < c->slot_hi; ++i)
-      if (c->mirror[i].active) run = std::min(run, every - c->mirror[i].step % every);
-    for (int i = c->slot_lo; i < c->slot_hi; ++i) {
-      const SeqMeta& M = c->mirror[i];
-      if (M.active && M.len + run > M.cap) return RA_ERR_CAPACITY;
+  // Runs of steps up to the next trigger of any sequence.  The first pass
+  // replays them on a copy of the mirror only, so that a capacity error (rows
+  // piling up under the external policy) is reported before any launch; the
+  // second pass launches and updates the mirror.
+  std::vector<SeqMeta> saved = c->mirror;
+  for (int pass = 0; pass < 2; ++pass) {
+    const bool launch = pass == 1;
+    if (launch) c->mirror = saved;
+    int remaining = n_steps;
+    while (remaining > 0 && c->slot_hi > c->slot_lo) {
+      int run = remaining;
+      for (int i = c->slot_lo; i < c->slot_hi; ++i)
+        if (c->mirror[i].active) run = std::min(run, every - c->mirror[i].step % every);
+      for (int i = c->slot_lo; i < c->slot_hi; ++i) {
+        const SeqMeta& M = c->mirror[i];
+        if (M.active && M.len + run > M.cap) {
+          c->mirror = saved;
+          return RA_ERR_CAPACITY;
+        }
+      }
+      if (launch) {
+        RA_LAUNCH(ra::launch_append_positions(c->meta, c->pos, c->slot_lo, c->slot_hi,
+                                              c->cfg.num_layers, c->cfg.num_kv_heads, run, s));
+        RA_LAUNCH(ra::launch_advance(c->meta, c->slot_lo, c->slot_hi, run, c->cfg.recent_r,
+                                     trigger_every(c->cfg), s));
+      }
+      int due = 0;
+      for (int i = c->slot_lo; i < c->slot_hi; ++i) {
+        SeqMeta& M = c->mirror[i];
+        if (!M.active) continue;
+        M.step += run;
+        M.len += run;
+        mirror_plan(M, c->cfg.recent_r, at_trigger(c->cfg, M.step));
+        due += M.due;
+      }
+      if (due && launch) {
+        RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos,
+                                   c->slot_lo, c->slot_hi, c->max_candidates_due(), true, s));
+      }
+      remaining -= run;
     }
-    RA_LAUNCH(ra::launch_append_positions(c->meta, c->pos, c->slot_lo, c->slot_hi,
-                                          c->cfg.num_layers, c->cfg.num_kv_heads, run, s));
-    RA_LAUNCH(ra::launch_advance(c->meta, c->slot_lo, c->slot_hi, run, c->cfg.recent_r,
-                                 trigger_every(c->cfg), s));
-    int due = 0;
-    for (int i = c->slot_lo; i < c->slot_hi; ++i) {
-      SeqMeta& M = c->mirror[i];
-      if (!M.active) continue;
-      M.step += run;
-      M.len += run;
-      mirror_plan(M, c->cfg.recent_r, at_trigger(c->cfg, M.step));
-      due += M.due;
-    }
-    if (due) {
-      RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos,
-                                 c->slot_lo, c->slot_hi, c->max_candidates_due(), true, s));
-    }
-    remaining -= run;
   }
   return RA_OK;
 }

@@ -101,3 +101,31 @@ def test_window_select_needs_the_chronological_layout():
     assert _status(B.ra_window_select, cache.handle, 0, 1, qw, None, 0, None) == \
         B.RA_ERR_UNSUPPORTED
     cache.close()
+
+
+def test_fast_forward_refuses_to_outgrow_a_region_before_any_launch():
+    """Under the external policy nothing is evicted at the end of a step, so
+    rows pile up: a fast forward that would outgrow the region is refused as
+    a whole, before any launch, and a shorter one still fills it exactly."""
+    log("fast forward capacity")
+    cfg = B.make_config(1, 2, 1, 16, 8, 8, B.RA_BUDGET_EVICTABLE, B.RA_BF16, 1,
+                        policy=B.RA_POLICY_EXTERNAL)
+    cache = B.Cache(cfg, B.ra_seq_rows(cfg, 4))
+    h = cache.handle
+    B.ra_seq_begin(h, 0, 4, 1, 0)
+    cap = B.ra_get_seq_info(h, 0).cap
+    B.ra_fast_forward(h, 5)
+    before = _infos_of(h, 1)
+    assert _status(B.ra_fast_forward, h, cap - 4 - 5 + 1) == B.RA_ERR_CAPACITY
+    assert _infos_of(h, 1) == before
+    assert list(B.ra_read_positions(h, 0, 0, 0, cap)) == list(range(9))
+    B.ra_fast_forward(h, cap - 4 - 5)
+    info = B.ra_get_seq_info(h, 0)
+    assert (info.len, info.step, info.event) == (cap, cap - 4, 0)
+    assert list(B.ra_read_positions(h, 0, 0, 0, cap)) == list(range(cap))
+    cache.close()
+
+
+def _infos_of(h, n):
+    return [(i.active, i.len, i.step, i.event) for i in
+            (B.ra_get_seq_info(h, s) for s in range(n))]
