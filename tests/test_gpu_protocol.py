@@ -129,3 +129,39 @@ def test_fast_forward_refuses_to_outgrow_a_region_before_any_launch():
 def _infos_of(h, n):
     return [(i.active, i.len, i.step, i.event) for i in
             (B.ra_get_seq_info(h, s) for s in range(n))]
+
+
+def test_no_active_sequence_and_gaps_between_slots():
+    """A step with no active sequence succeeds and writes nothing; with only
+    the middle one of three slots active, the other slots' output rows stay
+    untouched and the active one decodes as the oracle through its events."""
+    log("empty batch and slot gaps")
+    run = Run(L=2, Hq=4, Hkv=2, K=24, lps=[5, 9, 3], r=8, every=8, begin=False)
+    sentinel = 3.0
+    out = torch.full((run.max_seqs, run.Hq, 128), sentinel, dtype=torch.bfloat16,
+                     device="cuda")
+    for layer in range(run.L):
+        q, k, v = run.step_inputs(layer)
+        run.cache.decode(layer, q, k, v, out)
+    assert B.ra_end_step(run.h) == 0
+    assert bool((out == sentinel).all())
+    run.begin(1)
+    o = OracleSeq(run, 1)
+    events = 0
+    for t in range(56):          # events at steps 40, 48 and 56
+        outs = torch.full((run.L, run.max_seqs, run.Hq, 128), sentinel,
+                          dtype=torch.bfloat16, device="cuda")
+        for layer in range(run.L):
+            q, k, v = run.step_inputs(layer)
+            run.cache.decode(layer, q, k, v, outs[layer])
+        events += B.ra_end_step(run.h)
+        run.steps = [s + 1 for s in run.steps]
+        o.rep.append()
+        for layer in range(run.L):
+            err = max_abs(outs[layer, 1].float().cpu(), o.attend(layer, t))
+            assert err <= TOL[B.RA_BF16], (t, layer, err)
+        assert bool((outs[:, 0] == sentinel).all()) and bool((outs[:, 2] == sentinel).all())
+        o.rep.end_step()
+    assert events == 3
+    check_heads(run, [o])
+    run.close()
