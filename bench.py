@@ -280,7 +280,41 @@ def evict_cost(B, torch, Workload, methods=("random", "snapkv")):
     return res
 
 
-def tiny_latency(B, torch, Workload):
+def tiny_cpu_baseline(lp, K, T, Hq, Hkv, seed, rid):
+    """The CPU oracle, untuned, on the whole tiny run: the same 1024 steps and
+    eviction events, fp64 attention over the kept rows (rows resident in RAM
+    before timing)."""
+    import numpy as np
+    import torch
+    from oracle.attention import gqa_decode
+    from oracle.evict import SequenceReplay
+    from paper_2609_03430_amd.synth import Workload
+
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = 1
+    wl = Workload(1000, 1, Hq, Hkv, 128, torch.float32, False)
+    allp = torch.arange(lp + T)
+    k = [wl.k_rows(rid, 0, g, allp, lp).double().numpy() for g in range(Hkv)]
+    v = [wl.v_rows(rid, 0, g, allp, lp).double().numpy() for g in range(Hkv)]
+    qs = [wl.q_rows(rid, 0, torch.arange(Hq), t).double().numpy() for t in range(T)]
+    rep = SequenceReplay(lp, K, R, EVERY, seed, rid, [(0, g) for g in range(Hkv)])
+    t_start = time.perf_counter()
+    for t in range(T):
+        rep.append()
+        gqa_decode(qs[t], [k[g][rep.P[(0, g)]] for g in range(Hkv)],
+                   [v[g][rep.P[(0, g)]] for g in range(Hkv)])
+        rep.end_step()
+    seconds = time.perf_counter() - t_start
+    return {"value": seconds * 1e6 / T, "unit": "us/step", "cores": threads,
+            "kind": "oracle", "events": rep.event,
+            "sample": "the whole tiny run (%d steps from the prompt, every eviction event), "
+                      "numpy fp64" % T, "seconds": seconds}
+
+
+def tiny_latency(B, torch, Workload, with_cpu=True):
     """Per-step latency of the tiny case: 1 layer, 4 query / 2 KV heads,
     head_dim 128, fp32 N(0,1) rows, prompt 128, r=64, K=256, eviction every
     64 steps, 1024 decode steps from the pinned prompt (11 events).  A
@@ -327,7 +361,10 @@ def tiny_latency(B, torch, Workload):
             "events": events,
             "us_per_step_gpu": e0.elapsed_time(e1) * 1e3 / T,
             "us_per_step_wall": wall * 1e6 / T,
+            "higher_is_better": False,
         }
+    if with_cpu:
+        result["cpu_baseline"] = tiny_cpu_baseline(lp, K, T, Hq, Hkv, 1000 * 1000003, 0)
     return result
 
 
@@ -601,7 +638,7 @@ def main():
         return
 
     if args.tiny:
-        print(json.dumps(tiny_latency(B, torch, Workload)), flush=True)
+        print(json.dumps(tiny_latency(B, torch, Workload, not args.no_cpu_baseline)), flush=True)
         return
 
     w = WORKLOADS[args.workload]

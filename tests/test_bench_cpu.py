@@ -50,3 +50,13 @@ def test_traffic_is_reported_only_for_the_profiled_run(monkeypatch):
     assert bench.read_traffic(bench.run_signature(full)) is None
     monkeypatch.setattr(bench, "kernel_source_hash", lambda read=None: "0" * 16)
     assert bench.read_traffic(default) is None
+
+
+def test_tiny_cpu_baseline_replays_the_whole_run():
+    """--tiny's CPU baseline is the oracle on the whole tiny run: 1024 steps
+    from the prompt with all 11 eviction events."""
+    sys.path.insert(0, ROOT)
+    import bench
+    r = bench.tiny_cpu_baseline(128, 256, 1024, 4, 2, 1000 * 1000003, 0)
+    assert r["events"] == 11 and r["kind"] == "oracle" and r["unit"] == "us/step"
+    assert r["value"] > 0 and r["cores"] >= 1
