@@ -473,9 +473,13 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
 // fp32, VALU
 // ---------------------------------------------------------------------------
 
-__global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G,
+// GT: the group size when fixed at compile time (1, 2, 4, 8), 0 for any G.
+template <int GT>
+__global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G_rt,
                                                       int Hq, int Hkv,
                                                       float scale_log2) {
+  constexpr int kQ = GT > 0 ? GT : kMaxGroup;   // query slots in registers
+  const int G = GT > 0 ? GT : G_rt;
   __shared__ float qs[kMaxGroup][kHeadDim];
   __shared__ float ps[kMaxGroup][64];
   const Work w = locate(a.meta, a.layer, Hkv, a.split_keys);
@@ -492,34 +496,36 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G,
   for (int i = lane; i < G * kHeadDim; i += 64) qs[i / kHeadDim][i % kHeadDim] = qg[i];
   __syncthreads();
 
-  float m[kMaxGroup], l[kMaxGroup], acc[kMaxGroup][2];
+  float m[kQ], l[kQ], acc[kQ][2];
 #pragma unroll
-  for (int q = 0; q < kMaxGroup; ++q) {
+  for (int q = 0; q < kQ; ++q) {
     m[q] = kNegInf;
     l[q] = 0.f;
     acc[q][0] = acc[q][1] = 0.f;
   }
+  const float vn0 = vn[lane], vn1 = vn[lane + 64];
   for (int kb = w.k0; kb < w.k1; kb += 64) {
+    // scores: lanes own keys
     const int key = kb + lane;
     const bool valid = key < w.k1;
     const float* krow = key < w.len ? Kr + static_cast<int64_t>(key) * kHeadDim : kn;
-    float s[kMaxGroup];
+    float s[kQ];
 #pragma unroll
-    for (int q = 0; q < kMaxGroup; ++q) s[q] = 0.f;
+    for (int q = 0; q < kQ; ++q) s[q] = 0.f;
     if (valid) {
       for (int c = 0; c < kHeadDim; c += 4) {
         const float4 kv = *reinterpret_cast<const float4*>(krow + c);
 #pragma unroll
-        for (int q = 0; q < kMaxGroup; ++q) {
-          if (q < G)
+        for (int q = 0; q < kQ; ++q) {
+          if (GT > 0 || q < G)
             s[q] += kv.x * qs[q][c] + kv.y * qs[q][c + 1] + kv.z * qs[q][c + 2] +
                     kv.w * qs[q][c + 3];
         }
       }
     }
 #pragma unroll
-    for (int q = 0; q < kMaxGroup; ++q) {
-      if (q < G) {
+    for (int q = 0; q < kQ; ++q) {
+      if (GT > 0 || q < G) {
         const float x = valid ? s[q] * scale_log2 : kNegInf;
         const float mn = fmaxf(m[q], wave_max(x));
         const float alpha = exp2f(m[q] - mn);
@@ -532,23 +538,45 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G,
       }
     }
     __syncthreads();
+    // P.V: lanes own channels lane and lane + 64; a value tile holds the 8
+    // keys of a channel in 32 contiguous bytes, so a lane reads 8 keys with
+    // two 16-byte loads and the wavefront's reads are contiguous.  The
+    // chunk's tiles are all issued before any is used.  Rows at or past len
+    // are selected, not multiplied: the new value at len, zero above it.
     const int nk = min(64, w.k1 - kb);
-    for (int j = 0; j < nk; ++j) {
-      const int kj = kb + j;
-      float v0, v1;
-      if (kj < w.len) {
-        const float* vt = Vr + static_cast<int64_t>(kj & ~7) * kHeadDim + (kj & 7);
-        v0 = vt[lane * 8];
-        v1 = vt[(lane + 64) * 8];
-      } else {
-        v0 = vn[lane];
-        v1 = vn[lane + 64];
-      }
+    const int ntile = (nk + 7) >> 3;
+    float vv[8][2][8];
 #pragma unroll
-      for (int q = 0; q < kMaxGroup; ++q) {
-        if (q < G) {
-          acc[q][0] += ps[q][j] * v0;
-          acc[q][1] += ps[q][j] * v1;
+    for (int t = 0; t < 8; ++t) {
+      if (t < ntile) {
+        const int kt = kb + 8 * t;
+        const float* base = Vr + static_cast<int64_t>(kt) * kHeadDim;
+        const float4* s0 = reinterpret_cast<const float4*>(base + lane * 8);
+        const float4* s1 = reinterpret_cast<const float4*>(base + (lane + 64) * 8);
+        const float4 a0 = s0[0], a1 = s0[1], b0 = s1[0], b1 = s1[1];
+        const float ea[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        const float eb[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int kj = kt + e;
+          vv[t][0][e] = kj < w.len ? ea[e] : (kj == w.len ? vn0 : 0.f);
+          vv[t][1][e] = kj < w.len ? eb[e] : (kj == w.len ? vn1 : 0.f);
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      if (t < ntile) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+#pragma unroll
+          for (int q = 0; q < kQ; ++q) {
+            if (GT > 0 || q < G) {
+              const float p = ps[q][8 * t + e];
+              acc[q][0] += p * vv[t][0][e];
+              acc[q][1] += p * vv[t][1][e];
+            }
+          }
         }
       }
     }
@@ -564,8 +592,8 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G,
   const int head = w.slot * Hkv + w.g;
   const int64_t item = static_cast<int64_t>(head) * kMaxSplits + w.split;
 #pragma unroll
-  for (int q = 0; q < kMaxGroup; ++q) {
-    if (q < G) {
+  for (int q = 0; q < kQ; ++q) {
+    if (GT > 0 || q < G) {
       float* po = a.ws_o + (item * G + q) * kHeadDim;
       po[lane] = acc[q][0];
       po[lane + 64] = acc[q][1];
@@ -575,6 +603,13 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G,
       }
     }
   }
+}
+
+template <int GT>
+void launch_f32(const dim3& grid, hipStream_t s, const AttnLaunch& a, const Shape& sh,
+                float scale_log2) {
+  hipLaunchKernelGGL((attn_f32_kernel<GT>), grid, dim3(64), 0, s, a, sh.G, sh.Hq, sh.Hkv,
+                     scale_log2);
 }
 
 }  // namespace
@@ -606,8 +641,13 @@ hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s)
       hipLaunchKernelGGL(combine_kernel<uint16_t>, cgrid, dim3(256), 0, s, a, sh.G,
                          sh.Hq, sh.Hkv, true);
   } else {
-    hipLaunchKernelGGL(attn_f32_kernel, grid, dim3(64), 0, s, a, sh.G, sh.Hq,
-                       sh.Hkv, scale_log2);
+    switch (sh.G) {
+      case 1: launch_f32<1>(grid, s, a, sh, scale_log2); break;
+      case 2: launch_f32<2>(grid, s, a, sh, scale_log2); break;
+      case 4: launch_f32<4>(grid, s, a, sh, scale_log2); break;
+      case 8: launch_f32<8>(grid, s, a, sh, scale_log2); break;
+      default: launch_f32<0>(grid, s, a, sh, scale_log2); break;
+    }
     hipLaunchKernelGGL(combine_kernel<float>, cgrid, dim3(256), 0, s, a, sh.G,
                        sh.Hq, sh.Hkv, false);
   }
