@@ -119,6 +119,23 @@ def read_traffic(signature):
     return d.get("hbm_bytes_per_launch")
 
 
+def host_cpu():
+    """The host the CPU baseline ran on: CPUs this process may use, CPUs of
+    the machine, and the CPU model."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:  # pragma: no cover
+        pass
+    return {"cpus_usable": len(os.sched_getaffinity(0)), "nproc": os.cpu_count(),
+            "cpu_model": model,
+            "note": "cores = the BLAS threads the numpy oracle ran with"}
+
+
 def cpu_baseline(w, seed, lp, t0, steps):
     """The CPU oracle, untuned, on one sequence x one layer x all KV heads for
     `steps` steady-state decode steps (one eviction event included)."""
@@ -166,6 +183,7 @@ def cpu_baseline(w, seed, lp, t0, steps):
         "unit": "tokens/s",
         "cores": int(threads),
         "kind": "oracle",
+        "host": host_cpu(),
         "sample": ("1 sequence x 1 layer x %d KV heads (%d query heads), %d decode "
                    "steps at steps %d..%d incl. %d eviction event(s), numpy fp64; "
                    "tokens/s = steps / (time x %d layers), i.e. the oracle's rate on "
@@ -602,7 +620,81 @@ def build_parser():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device-to-device copy three times (the "
                          "known-size reference for the HBM byte counters)")
+    ap.add_argument("--traffic-summary", nargs=4,
+                    metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
+                    help="CPU only: read the rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE "
+                         "outputs of a bench run with the other arguments given here and "
+                         "of --calibrate-copy, and write "
+                         "profiles/attention_traffic_<workload>.json")
     return ap
+
+
+def _counter_rows(d):
+    """(dispatch id, kernel name, counter, value) rows of every rocprofv3
+    counter-collection CSV under directory d; values summed per dispatch and
+    counter."""
+    import csv
+    import glob
+    acc = {}
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit("no counter_collection.csv under %s" % d)
+    for path in files:
+        with open(path, newline="") as f:
+            for row in csv.DictReader(f):
+                key = (int(row["Dispatch_Id"]), row["Kernel_Name"], row["Counter_Name"])
+                acc[key] = acc.get(key, 0.0) + float(row["Counter_Value"])
+    return sorted((k[0], k[1], k[2], v) for k, v in acc.items())
+
+
+def traffic_summary(args):
+    """Copy-calibrated HBM bytes per attention launch (and per full eviction
+    event) of the timed region of one bench run, from two counter runs."""
+    fetch_dir, write_dir, cfetch_dir, cwrite_dir = args.traffic_summary
+    w = WORKLOADS[args.workload]
+
+    def per_dispatch(d, counter, match):
+        return [v for _, name, c, v in _counter_rows(d) if c == counter and match(name)]
+
+    def copy_kib(d, counter):
+        rows = [(v, name) for _, name, c, v in _counter_rows(d) if c == counter]
+        top = max(v for v, _ in rows)
+        big = [v for v, _ in rows if v > 0.5 * top]
+        return sum(big) / len(big)
+
+    copy_bytes = 1 << 30
+    cf, cw = copy_kib(cfetch_dir, "FETCH_SIZE"), copy_kib(cwrite_dir, "WRITE_SIZE")
+    fscale, wscale = copy_bytes / (cf * 1024), copy_bytes / (cw * 1024)
+    timed = args.steps * w["L"]
+    attn = lambda n: "attn_bf16_kernel" in n
+    full_evict = lambda n: "evict_kernel" in n and "false" in n
+    fa = per_dispatch(fetch_dir, "FETCH_SIZE", attn)[-timed:]
+    wa = per_dispatch(write_dir, "WRITE_SIZE", attn)[-timed:]
+    fe = per_dispatch(fetch_dir, "FETCH_SIZE", full_evict)
+    we = per_dispatch(write_dir, "WRITE_SIZE", full_evict)
+    fb = sum(fa) / len(fa) * 1024 * fscale
+    wb = sum(wa) / len(wa) * 1024 * wscale
+    out = {
+        "workload": args.workload,
+        "kernel": "attn_bf16_kernel",
+        "kernel_source_hash": kernel_source_hash(),
+        "copy_calibration": {"bytes": copy_bytes, "fetch_kib_per_dispatch": cf,
+                             "write_kib_per_dispatch": cw, "fetch_scale": fscale,
+                             "write_scale": wscale},
+        "fetch_bytes_per_launch": fb,
+        "write_bytes_per_launch": wb,
+        "hbm_bytes_per_launch": fb + wb,
+        "launches_sampled": len(fa),
+        "evict_full_events_sampled": len(fe),
+        "evict_full_event": ({"fetch_bytes": sum(fe) / len(fe) * 1024 * fscale,
+                              "write_bytes": sum(we) / len(we) * 1024 * wscale}
+                             if fe and we else None),
+        "run": run_signature(args),
+    }
+    path = os.path.join(ROOT, "profiles", "attention_traffic_%s.json" % args.workload)
+    with open(path, "w") as f:
+        json.dump(out, f, indent=1)
+    print(json.dumps(out))
 
 
 def main():
@@ -612,6 +704,10 @@ def main():
         print("bench.py runs on one GPU only: the hot path has no cross-GPU step; "
               "--gpus %d is not supported" % args.gpus, file=sys.stderr)
         sys.exit(2)
+
+    if args.traffic_summary:
+        traffic_summary(args)
+        return
 
     import torch
     from paper_2609_03430_amd import binding as B
@@ -814,6 +910,21 @@ def main():
                           "(key + value + position) x 2, plus candidate positions read",
         }
     total_bytes = sum(attn_bytes) + sum(ev_bytes)
+    # Steady-state rate: a window of `steps` steps holds round(steps / 64)
+    # end-of-step events only on average, so the raw value over a short
+    # window weighs the event by its position; the amortised figure charges
+    # every step the mean attention span, the mean end-of-step time of steps
+    # without events, and 1/64 of the mean event.
+    amortised = None
+    if ev_ms and len(set(starts)) == 1:
+        quiet = [x0.elapsed_time(x1) for _, _, (x0, x1), nev in rec if not nev]
+        step_ms = (sum(attn_ms) / len(attn_ms) + (sum(quiet) / len(quiet) if quiet else 0.0) +
+                   sum(ev_ms) / len(ev_ms) / EVERY)
+        amortised = {"value": Bsz / (step_ms * 1e-3), "unit": "tokens/s",
+                     "ms_per_step": step_ms,
+                     "note": "mean attention span per step + mean end-of-step time "
+                             "without an event + mean event / 64 (GPU time from HIP "
+                             "events; the raw value is wall time over the window)"}
     if len(set(starts)) == 1:
         window = ("decode steps %d..%d of %d (%d end-of-step eviction events)"
                   % (starts[0] + args.warmup + 1, starts[0] + total, starts[0] + total,
@@ -861,6 +972,7 @@ def main():
             "bytes_per_launch": sum(attn_bytes) / (len(attn_bytes) * L),
         },
         "compaction": comp,
+        "amortised": amortised,
         "end_to_end_gbs": total_bytes / wall / 1e9,
         "end_to_end_frac": total_bytes / wall / 1e9 / PEAK_HBM_GBS,
     }

@@ -260,7 +260,10 @@ ra_status ra_decode_attention(ra_cache* cache, int32_t layer, const void* q,
 ra_status ra_end_step(ra_cache* cache, void* stream, int32_t* n_evicted);
 
 /* Run one eviction event on slot `seq` now, whatever the step count, if
- * its evictable rows exceed k_keep (otherwise a no-op).  Not allowed in
+ * its evictable rows exceed k_keep (otherwise a no-op).  The event is the
+ * one of Eq. 1 with Section 3's scores (i.i.d. uniform per candidate, the
+ * top k_keep kept): the same keys, selection and compaction as a periodic
+ * event, with the next event index.  Not allowed in
  * the middle of a step, nor with more than 1024 rows over k_keep (possible
  * only under RA_POLICY_EXTERNAL): RA_ERR_STATE; RA_ERR_UNSUPPORTED if such
  * a pile-up makes more than 32768 candidate slots.  The keys are Random
@@ -297,7 +300,9 @@ ra_status ra_read_rows(ra_cache* cache, int32_t seq, int32_t layer,
                        void* stream);
 
 /* SYNCHRONOUS: copy one head's cached positions, in row order (ascending in
- * the chronological layout), to host memory; *n_out receives len.  RA_ERR_CAPACITY if host_cap < len (nothing
+ * the chronological layout), to host memory; *n_out receives len.  This is
+ * the keep-set of Appendix D's keep-log (the positions a head holds after
+ * each event), read one head at a time.  RA_ERR_CAPACITY if host_cap < len (nothing
  * copied).  Synchronizes `stream`. */
 ra_status ra_read_positions(ra_cache* cache, int32_t seq, int32_t layer,
                             int32_t kv_head, int32_t* host_out,

@@ -153,6 +153,40 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr())
 
 
+# Config of every live handle, for the tensor checks below (the C ABI takes
+# bare pointers and cannot see a buffer's size, dtype or layout).
+_CONFIGS = {}
+
+
+def _cfg_of(handle):
+    return _CONFIGS.get(getattr(handle, "value", handle))
+
+
+def _cache_dtype(cfg):
+    return torch.bfloat16 if cfg.dtype == RA_BF16 else torch.float32
+
+
+def _arg(t, where, name, dtype=None, numel=0):
+    """Refuse, before its pointer crosses the ABI, a tensor that the call
+    would read or write out of bounds or misread: not a contiguous device
+    tensor, another dtype than the call's, or fewer elements than it uses."""
+    if t is None:
+        return
+    why = None
+    if not isinstance(t, torch.Tensor):
+        why = "not a tensor"
+    elif not t.is_cuda:
+        why = "not on the GPU"
+    elif not t.is_contiguous():
+        why = "not contiguous"
+    elif dtype is not None and t.dtype != dtype:
+        why = "dtype %s, expected %s" % (t.dtype, dtype)
+    elif t.numel() < numel:
+        why = "%d elements, needs %d" % (t.numel(), numel)
+    if why:
+        raise RandAttnError(RA_ERR_INVALID_ARG, "%s (%s: %s)" % (where, name, why))
+
+
 def _stream(stream):
     if stream is None:
         stream = torch.cuda.current_stream()
@@ -212,21 +246,35 @@ def ra_workspace_bytes(cfg):
 
 
 def ra_cache_create(cfg, k_pool, v_pool, pos_pool, pool_rows, meta, stream=None):
+    where = "ra_cache_create"
+    if ra_config_check(cfg) == RA_OK:
+        rows = int(pool_rows) * cfg.head_dim
+        _arg(k_pool, where, "k_pool", _cache_dtype(cfg), rows)
+        _arg(v_pool, where, "v_pool", _cache_dtype(cfg), rows)
+        _arg(pos_pool, where, "pos_pool", torch.int32, int(pool_rows))
+        _arg(meta, where, "meta")
     out = ctypes.c_void_p()
     _check(_lib().ra_cache_create(ctypes.byref(cfg), _ptr(k_pool), _ptr(v_pool),
                                   _ptr(pos_pool), int(pool_rows), _ptr(meta),
                                   meta.numel() * meta.element_size(),
                                   _stream(stream), ctypes.byref(out)),
            "ra_cache_create")
+    _CONFIGS[out.value] = ra_config.from_buffer_copy(cfg)
     return out
 
 
 def ra_cache_destroy(handle):
     _check(_lib().ra_cache_destroy(handle), "ra_cache_destroy")
+    _CONFIGS.pop(getattr(handle, "value", handle), None)
 
 
 def ra_seq_begin(handle, seq, prompt_len, seed, request_id, k_prompt=None,
                  v_prompt=None, stream=None):
+    cfg = _cfg_of(handle)
+    if cfg is not None:
+        n = cfg.num_layers * cfg.num_kv_heads * max(0, int(prompt_len)) * cfg.head_dim
+        _arg(k_prompt, "ra_seq_begin", "k_prompt", _cache_dtype(cfg), n)
+        _arg(v_prompt, "ra_seq_begin", "v_prompt", _cache_dtype(cfg), n)
     _check(_lib().ra_seq_begin(handle, int(seq), int(prompt_len), int(seed),
                                int(request_id), _ptr(k_prompt), _ptr(v_prompt),
                                _stream(stream)), "ra_seq_begin")
@@ -243,8 +291,21 @@ def ra_get_seq_info(handle, seq):
     return info
 
 
+def _decode_args(handle, where, q, k_new, v_new, out):
+    cfg = _cfg_of(handle)
+    if cfg is None:
+        return
+    dt, n, d = _cache_dtype(cfg), cfg.max_seqs, cfg.head_dim
+    _arg(q, where, "q", dt, n * cfg.num_q_heads * d)
+    _arg(k_new, where, "k_new", dt, n * cfg.num_kv_heads * d)
+    _arg(v_new, where, "v_new", dt, n * cfg.num_kv_heads * d)
+    _arg(out, where, "out", dt, n * cfg.num_q_heads * d)
+
+
 def ra_decode_attention(handle, layer, q, k_new, v_new, out, workspace,
                         stream=None):
+    _decode_args(handle, "ra_decode_attention", q, k_new, v_new, out)
+    _arg(workspace, "ra_decode_attention", "workspace")
     _check(_lib().ra_decode_attention(handle, int(layer), _ptr(q), _ptr(k_new),
                                       _ptr(v_new), _ptr(out), _ptr(workspace),
                                       workspace.numel() * workspace.element_size(),
@@ -268,17 +329,36 @@ def ra_fast_forward(handle, n_steps, stream=None):
 
 
 def ra_export_positions(handle, seq, out, stream=None):
+    _arg(out, "ra_export_positions", "out", torch.int32)
     _check(_lib().ra_export_positions(handle, int(seq), _ptr(out), out.numel(),
                                       _stream(stream)), "ra_export_positions")
 
 
+def _rows_needed(handle, seq, per_head):
+    """(dtype, elements) of a row array of slot `seq`: all its heads, or one."""
+    cfg = _cfg_of(handle)
+    if cfg is None:
+        return None, 0
+    info = ra_seq_info()
+    if _lib().ra_get_seq_info(handle, int(seq), ctypes.byref(info)) != RA_OK:
+        return _cache_dtype(cfg), 0
+    heads = 1 if per_head else cfg.num_layers * cfg.num_kv_heads
+    return _cache_dtype(cfg), heads * info.len * cfg.head_dim
+
+
 def ra_write_rows(handle, seq, k_rows, v_rows, stream=None):
+    dt, n = _rows_needed(handle, seq, False)
+    _arg(k_rows, "ra_write_rows", "k_rows", dt, n)
+    _arg(v_rows, "ra_write_rows", "v_rows", dt, n)
     _check(_lib().ra_write_rows(handle, int(seq), _ptr(k_rows), _ptr(v_rows),
                                 _stream(stream)), "ra_write_rows")
 
 
 def ra_read_rows(handle, seq, layer, kv_head, k_out=None, v_out=None,
                  stream=None):
+    dt, n = _rows_needed(handle, seq, True)
+    _arg(k_out, "ra_read_rows", "k_out", dt, n)
+    _arg(v_out, "ra_read_rows", "v_out", dt, n)
     _check(_lib().ra_read_rows(handle, int(seq), int(layer), int(kv_head),
                                _ptr(k_out), _ptr(v_out), _stream(stream)),
            "ra_read_rows")
@@ -299,6 +379,13 @@ def ra_read_positions(handle, seq, layer, kv_head, cap, stream=None):
 def ra_window_select(handle, seq_lo, seq_hi, q_window, scores=None, scores_stride=0,
                      drops=None, stream=None):
     """Measurement only: the observation-window scoring pass (see the header)."""
+    cfg = _cfg_of(handle)
+    if cfg is not None:
+        heads = max(0, int(seq_hi) - int(seq_lo)) * cfg.num_layers * cfg.num_kv_heads
+        _arg(q_window, "ra_window_select", "q_window", torch.bfloat16,
+             cfg.max_seqs * cfg.num_layers * cfg.num_q_heads * 64 * cfg.head_dim)
+        _arg(scores, "ra_window_select", "scores", torch.float32, heads * int(scores_stride))
+        _arg(drops, "ra_window_select", "drops", torch.int32, heads * cfg.evict_every)
     _check(_lib().ra_window_select(handle, int(seq_lo), int(seq_hi), _ptr(q_window),
                                    _ptr(scores), int(scores_stride), _ptr(drops),
                                    _stream(stream)), "ra_window_select")
@@ -310,6 +397,11 @@ def ra_scored_scratch_bytes(cfg, max_prompt_len):
 
 def ra_scored_evict(handle, seq_lo, seq_hi, params, q_window, scratch, stream=None):
     """Measurement only: one score-based eviction round (see the header)."""
+    cfg = _cfg_of(handle)
+    if cfg is not None:
+        _arg(q_window, "ra_scored_evict", "q_window", torch.bfloat16,
+             cfg.max_seqs * cfg.num_layers * cfg.num_q_heads * 64 * cfg.head_dim)
+    _arg(scratch, "ra_scored_evict", "scratch")
     nbytes = scratch.numel() * scratch.element_size()
     _check(_lib().ra_scored_evict(handle, int(seq_lo), int(seq_hi), ctypes.byref(params),
                                   _ptr(q_window), _ptr(scratch), ctypes.c_size_t(nbytes),

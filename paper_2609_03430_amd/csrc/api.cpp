@@ -168,6 +168,52 @@ Plan attention_plan(const ra_cache* c) {
   return p;
 }
 
+// Host checks shared by both attention entry points; nothing is launched.
+ra_status check_decode(const ra_cache* c, int32_t layer, const void* q, const void* k_new,
+                       const void* v_new, const void* out) {
+  if (!c || layer < 0 || layer >= c->cfg.num_layers || !q || !k_new || !v_new || !out)
+    return RA_ERR_INVALID_ARG;
+  if (c->appended[layer]) return RA_ERR_STATE;
+  for (int s = c->slot_lo; s < c->slot_hi; ++s)
+    if (c->mirror[s].active && c->mirror[s].len + 1 > c->mirror[s].cap) return RA_ERR_CAPACITY;
+  return RA_OK;
+}
+
+// Marks the layer appended and launches its append + attention with the
+// given partials buffers (split_stride partial slots per head).
+ra_status launch_decode(ra_cache* c, int32_t layer, const void* q, const void* k_new,
+                        const void* v_new, void* out, const Plan& plan, float* ws_o,
+                        float* ws_ml, int split_stride, hipStream_t stream) {
+  c->appended[layer] = 1;
+  ++c->n_appended;
+  if (c->slot_hi <= c->slot_lo) return RA_OK;
+  ra::AttnLaunch a{};
+  a.meta = c->meta;
+  a.kpool = c->kpool;
+  a.vpool = c->vpool;
+  a.pos = c->pos;
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.out = out;
+  a.ws_o = ws_o;
+  a.ws_ml = ws_ml;
+  a.split_stride = split_stride;
+  a.layer = layer;
+  a.max_seqs = c->slot_hi;
+  a.split_keys = plan.split_keys;
+  a.max_splits = plan.max_splits;
+  a.waves = plan.waves;
+  a.wide_regs = plan.wide_regs;
+  const hipError_t e = ra::launch_attention(c->shape(), a, stream);
+  if (e != hipSuccess) {
+    c->appended[layer] = 0;
+    --c->n_appended;
+    return hip_fail(e);
+  }
+  return RA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -397,44 +443,14 @@ ra_status ra_decode_attention(ra_cache* c, int32_t layer, const void* q,
                               const void* k_new, const void* v_new, void* out,
                               void* workspace, size_t workspace_bytes,
                               void* stream) {
-  if (!c || layer < 0 || layer >= c->cfg.num_layers || !q || !k_new || !v_new ||
-      !out || !workspace)
-    return RA_ERR_INVALID_ARG;
-  if (workspace_bytes < ra_workspace_bytes(&c->cfg)) return RA_ERR_INVALID_ARG;
-  if (c->appended[layer]) return RA_ERR_STATE;
-  for (int s = c->slot_lo; s < c->slot_hi; ++s)
-    if (c->mirror[s].active && c->mirror[s].len + 1 > c->mirror[s].cap) return RA_ERR_CAPACITY;
-  c->appended[layer] = 1;
-  ++c->n_appended;
-  if (c->slot_hi <= c->slot_lo) return RA_OK;
-  const Plan plan = attention_plan(c);
-  const size_t G = static_cast<size_t>(c->G);
+  const ra_status st = check_decode(c, layer, q, k_new, v_new, out);
+  if (st != RA_OK) return st;
+  if (!workspace || workspace_bytes < ra_workspace_bytes(&c->cfg)) return RA_ERR_INVALID_ARG;
   const size_t items = static_cast<size_t>(c->cfg.max_seqs) * c->cfg.num_kv_heads * ra::kMaxSplits;
   float* ws = static_cast<float*>(workspace);
-  ra::AttnLaunch a{};
-  a.meta = c->meta;
-  a.kpool = c->kpool;
-  a.vpool = c->vpool;
-  a.pos = c->pos;
-  a.q = q;
-  a.k_new = k_new;
-  a.v_new = v_new;
-  a.out = out;
-  a.ws_o = ws;
-  a.ws_ml = ws + items * G * ra::kHeadDim;
-  a.layer = layer;
-  a.max_seqs = c->slot_hi;
-  a.split_keys = plan.split_keys;
-  a.max_splits = plan.max_splits;
-  a.waves = plan.waves;
-  a.wide_regs = plan.wide_regs;
-  const hipError_t e = ra::launch_attention(c->shape(), a, static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) {
-    c->appended[layer] = 0;
-    --c->n_appended;
-    return hip_fail(e);
-  }
-  return RA_OK;
+  return launch_decode(c, layer, q, k_new, v_new, out, attention_plan(c), ws,
+                       ws + items * c->G * ra::kHeadDim, ra::kMaxSplits,
+                       static_cast<hipStream_t>(stream));
 }
 
 ra_status ra_end_step(ra_cache* c, void* stream, int32_t* n_evicted) {

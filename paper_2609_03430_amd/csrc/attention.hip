@@ -129,8 +129,8 @@ __device__ __forceinline__ void append_row(const Work& w, const SeqMeta* meta,
 // workgroup per head, launched after the attention kernel (the kernel
 // boundary makes every partial visible; no device-scope fences are needed in
 // the streaming kernel).  Partial layout:
-//   ws_o[((head * kMaxSplits + split) * G + q) * 128 + c]  numerator / 2^m
-//   ws_ml[((head * kMaxSplits + split) * G + q) * 2 + {0,1}] = (m, l)
+//   ws_o[((head * split_stride + split) * G + q) * 128 + c]  numerator / 2^m
+//   ws_ml[((head * split_stride + split) * G + q) * 2 + {0,1}] = (m, l)
 // with m the running max of the scores in log2 units and l the sum of
 // 2^(s - m) over the split's keys.
 template <typename E>
@@ -148,8 +148,8 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnLaunch a, int G, int H
   // a head with one split was written directly by the attention kernel
   if (skip_single && nsplit == 1) return;
   const int head = slot * Hkv + g;
-  const float* ml = a.ws_ml + static_cast<int64_t>(head) * kMaxSplits * G * 2;
-  const float* po = a.ws_o + static_cast<int64_t>(head) * kMaxSplits * G * kHeadDim;
+  const float* ml = a.ws_ml + static_cast<int64_t>(head) * a.split_stride * G * 2;
+  const float* po = a.ws_o + static_cast<int64_t>(head) * a.split_stride * G * kHeadDim;
   for (int i = t; i < nsplit * G; i += blockDim.x) {
     sm[i] = ml[2 * i];
     sl[i] = ml[2 * i + 1];
@@ -408,7 +408,7 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
                          static_cast<uint16_t*>(a.vpool), a.pos);
 
   const int head = w.slot * Hkv + w.g;
-  const int64_t item = static_cast<int64_t>(head) * kMaxSplits + w.split;
+  const int64_t item = static_cast<int64_t>(head) * a.split_stride + w.split;
   uint16_t* out = static_cast<uint16_t*>(a.out);
   if constexpr (W == 1) {
     if (qi < G) {
@@ -590,7 +590,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G_rt,
                       static_cast<float*>(a.vpool), a.pos);
 
   const int head = w.slot * Hkv + w.g;
-  const int64_t item = static_cast<int64_t>(head) * kMaxSplits + w.split;
+  const int64_t item = static_cast<int64_t>(head) * a.split_stride + w.split;
 #pragma unroll
   for (int q = 0; q < kQ; ++q) {
     if (GT > 0 || q < G) {

@@ -83,8 +83,9 @@ struct AttnLaunch {
   const void* k_new;
   const void* v_new;
   void* out;
-  float* ws_o;         // [heads][kMaxSplits][G][128] partial numerators
-  float* ws_ml;        // [heads][kMaxSplits][G][2]  running max (log2), sum
+  float* ws_o;         // [heads][split_stride][G][128] partial numerators
+  float* ws_ml;        // [heads][split_stride][G][2]  running max (log2), sum
+  int split_stride;    // partial slots per head (>= max_splits)
   int layer;
   int max_seqs;
   int split_keys;

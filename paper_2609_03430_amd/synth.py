@@ -12,11 +12,13 @@ Distributions (the shapes of the measured workloads):
   unscaled N(0, 1) for the tiny fp32 case.
 
 Construction.  ``numpy.random.default_rng(seed)`` draws a pool of P rows of
-N(0,1) float32 and the scale tables.  The row for (kind, seq, layer, head, j)
-is pool[h mod P], where h is an integer hash of its arguments computed with
-int64 tensor operations that never overflow; the float32 product with the
-scale and the round-to-nearest-even cast to bfloat16 are IEEE-exact, so CPU
-and GPU produce bit-identical rows.
+N(0,1) float32 for keys and values, the scale tables, then a second pool of
+P rows for queries (so a query is never a copy of a cached key, which would
+make its attention collapse onto that one row).  The row for (kind, seq,
+layer, head, j) is pool[h mod P] of its kind's pool, where h is an integer
+hash of its arguments computed with int64 tensor operations that never
+overflow; the float32 product with the scale and the round-to-nearest-even
+cast to bfloat16 are IEEE-exact, so CPU and GPU produce bit-identical rows.
 
 ``j`` is the row id: a prompt position p < prompt_len uses j = p; a
 generated position p uses j = prompt_len + ((p - prompt_len) mod ring) when
@@ -67,7 +69,9 @@ class Workload:
         pool = rng.standard_normal((self.P, self.d)).astype(np.float32)
         sk = rng.uniform(0.5, 2.0, (self.L, self.Hkv, self.d)).astype(np.float32)
         sv = rng.uniform(0.5, 2.0, (self.L, self.Hkv, self.d)).astype(np.float32)
+        qpool = rng.standard_normal((self.P, self.d)).astype(np.float32)
         self.pool = torch.from_numpy(pool).to(self.device)
+        self.qpool = torch.from_numpy(qpool).to(self.device)
         self.scale_k = torch.from_numpy(sk).to(self.device)
         self.scale_v = torch.from_numpy(sv).to(self.device)
 
@@ -77,6 +81,7 @@ class Workload:
         w.__dict__.update(self.__dict__)
         w.device = torch.device(device)
         w.pool = self.pool.to(w.device)
+        w.qpool = self.qpool.to(w.device)
         w.scale_k = self.scale_k.to(w.device)
         w.scale_v = self.scale_v.to(w.device)
         return w
@@ -96,7 +101,7 @@ class Workload:
     def _rows(self, kind, seq, layer, head, j):
         seq, layer, head, j = (self._t(x) for x in (seq, layer, head, j))
         idx = _hash(kind, seq, layer, head, j) % self.P
-        x = self.pool[idx]
+        x = (self.qpool if kind == KIND_Q else self.pool)[idx]
         if self.scaled and kind != KIND_Q:
             table = self.scale_k if kind == KIND_K else self.scale_v
             lh = torch.broadcast_tensors(layer, head, idx)

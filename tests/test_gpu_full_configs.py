@@ -7,15 +7,18 @@ step 32768 of a 32k-token generation, materialises the kept rows from the
 seeded generator, then decodes the last steps, which include an eviction
 event.  Sampled (sequence, layer, KV head) sites are replayed by the oracle
 from the seeds alone: their kept positions must match bit-exactly after the
-event, and the sampled outputs of their query heads must be within 2e-2 of
-the fp64 oracle.
+event, and every query head of the sampled sites must be within 2e-2 of the
+fp64 oracle and within one bf16 half-ulp of it plus a small floor, element by
+element.  Every cached position has its own key and value row (no input
+ring), and queries come from their own pool, so no query meets a copy of
+itself among the keys.
 """
 
 import numpy as np
 import pytest
 import torch
 
-from gpu_harness import OracleSeq, Run, log, max_abs
+from gpu_harness import OracleSeq, Run, attn_err, log, note
 from paper_2609_03430_amd import binding as B
 
 pytestmark = pytest.mark.gpu
@@ -38,13 +41,14 @@ def test_full_size(name, layout):
         % (name, layout, L, Hq, Hkv, Bsz, lp, K))
     run = Run(L=L, Hq=Hq, Hkv=Hkv, K=K, lps=[lp] * Bsz, r=64, every=64,
               seeds=[seed * 1000003 + b for b in range(Bsz)], rids=list(range(Bsz)),
-              wl_seed=seed, ring=64, write_prompt=False, layout=layout)
+              wl_seed=seed, write_prompt=False, layout=layout)
     t0 = T - WINDOW
     run.fast_forward(t0)
     for b in range(Bsz):
         run.materialise(b)
     log("  state at step %d materialised" % t0)
-    sites = [(0, 0, 0), (Bsz - 1, L - 1, Hkv - 1), (Bsz // 2, L // 2, 1)]
+    sites = [(0, 0, 0), (Bsz - 1, L - 1, Hkv - 1), (Bsz // 2, L // 2, 1),
+             (1, L - 2, Hkv // 2), (Bsz - 2, 3, Hkv - 2), (Bsz // 3, L // 3, 3)]
     heads = {}
     for b, l, g in sites:
         heads.setdefault(b, []).append((l, g))
@@ -63,9 +67,8 @@ def test_full_size(name, layout):
                 o = oracles[b]
                 want = o.attend_group(l, g, t0 + i)
                 got = outs[l, b, g * run.G:(g + 1) * run.G].float().cpu()
-                err = max_abs(got, want)
+                err = attn_err(got, want, B.RA_BF16, (name, i, b, l, g))
                 worst = max(worst, err)
-                assert err <= 2e-2, (name, i, b, l, g, err)
         for o in oracles.values():
             o.rep.end_step()
     for b, l, g in sites:
@@ -73,6 +76,7 @@ def test_full_size(name, layout):
         want = oracles[b].rep.P[(l, g)]
         assert np.array_equal(got, want), (name, b, l, g)
     assert oracles[0].rep.event >= 2
+    note("events", oracles[0].rep.event)
     log("  %s ok: worst %.3g, events %d" % (name, worst, oracles[0].rep.event))
     run.close()
     torch.cuda.empty_cache()
@@ -92,7 +96,7 @@ def test_full_size_phi4_ragged():
     log("phi4 ragged: prompts %d..%d, generated %d..%d" % (min(lps), max(lps), gens[-1], gens[0]))
     run = Run(L=L, Hq=Hq, Hkv=Hkv, K=K, lps=lps, r=64, every=64,
               seeds=[seed * 1000003 + b for b in range(Bsz)], rids=list(range(Bsz)),
-              wl_seed=seed, ring=64, write_prompt=False, begin=False)
+              wl_seed=seed, write_prompt=False, begin=False)
     for b in range(Bsz):
         run.begin(b)
         nxt = gens[b + 1] if b + 1 < Bsz else 0
@@ -102,7 +106,8 @@ def test_full_size_phi4_ragged():
     for b in range(Bsz):
         run.materialise(b)
     log("  snapshot materialised")
-    sites = [(0, 0, 0), (Bsz - 1, L - 1, Hkv - 1), (Bsz // 2, 7, 5), (31, L - 1, 0)]
+    sites = [(0, 0, 0), (Bsz - 1, L - 1, Hkv - 1), (Bsz // 2, 7, 5), (31, L - 1, 0),
+             (100, 20, 9), (77, 1, 3)]
     heads = {}
     for b, l, g in sites:
         heads.setdefault(b, []).append((l, g))
@@ -122,8 +127,7 @@ def test_full_size_phi4_ragged():
             for b, l, g in sites:
                 want = oracles[b].attend_group(l, g, gens[b] + i)
                 got = outs[l, b, g * run.G:(g + 1) * run.G].float().cpu()
-                err = max_abs(got, want)
-                assert err <= 2e-2, ("phi4", i, b, l, g, err)
+                attn_err(got, want, B.RA_BF16, ("phi4", i, b, l, g))
         for o in oracles.values():
             o.rep.end_step()
     for b, l, g in sites:

@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_harness import TOL, OracleSeq, Run, log, max_abs
+from gpu_harness import TOL, attn_err, OracleSeq, Run, log, max_abs
 from gpu_harness import check_heads as _check_heads
 from paper_2609_03430_amd import binding as B
 
@@ -34,9 +34,8 @@ def test_small_decode_parity(dtype, layout):
             o.rep.append()
             for layer in range(run.L):
                 want = o.attend(layer, t)
-                err = max_abs(outs[layer, o.slot], want)
+                err = attn_err(outs[layer, o.slot], want, dtype, (t, o.slot, layer,))
                 worst = max(worst, err)
-                assert err <= TOL[dtype], (t, o.slot, layer, err)
             o.rep.end_step()
         if ev:
             events += 1
@@ -107,9 +106,8 @@ def test_policy_decode_parity(policy, block, layout):
         for o in oracles:
             o.rep.append()
             for layer in range(run.L):
-                err = max_abs(outs[layer, o.slot], o.attend(layer, t))
+                err = attn_err(outs[layer, o.slot], o.attend(layer, t), B.RA_BF16, (t, o.slot, layer,))
                 worst = max(worst, err)
-                assert err <= TOL[B.RA_BF16], (t, o.slot, layer, err)
             o.rep.end_step()
         if ev:
             events += 1
@@ -276,9 +274,8 @@ def test_attention_plans(tag, Hkv, G, Bsz, K, waves):
         for b, o in enumerate(oracles):
             o.rep.append()
             if check:
-                err = max_abs(outs[0, b], o.attend(0, gens[b] + i))
+                err = attn_err(outs[0, b], o.attend(0, gens[b] + i), B.RA_BF16, (tag, i, b,))
                 worst = max(worst, err)
-                assert err <= TOL[B.RA_BF16], (tag, i, b, err)
             o.rep.end_step()
     log("  worst %.3g" % worst)
     run.close()
@@ -321,21 +318,24 @@ def test_attention_shapes(dtype, Hq, Hkv, split):
         for o in oracles:
             o.rep.append()
             if t in (0, 1, 2, 31, 32, 47, 69):
-                err = max_abs(outs[0, o.slot], o.attend(0, t))
-                assert err <= TOL[dtype], (t, o.slot, err)
+                err = attn_err(outs[0, o.slot], o.attend(0, t), dtype, (t, o.slot,))
                 checked += 1
             o.rep.end_step()
     assert checked == 7 * len(lps)
     run.close()
 
 
-def test_tiny_config_full_run():
+@pytest.mark.parametrize("every,n_events", [(64, 11), (1, 704)])
+def test_tiny_config_full_run(every, n_events):
     """The tiny single-layer case in full: 1 sequence, 4 query / 2 KV heads,
-    fp32, prompt 128, r=64, K=256, 1024 decode steps, evicting every 64 steps
-    once over budget.  Every output of every step within 1e-5 of the fp64
-    oracle; kept sets bit-exact after each of the 11 events."""
-    log("tiny config full run")
-    run = Run(L=1, Hq=4, Hkv=2, K=256, lps=[128], r=64, every=64, dtype=B.RA_F32,
+    fp32, prompt 128, r=64, K=256, 1024 decode steps, evicting once over
+    budget -- at every 64th step (the paper's periodic trigger, the headline
+    reading: 11 events) or at every step (the case's own "whenever the
+    evictable entries exceed K": 704 events, from step 321 on).  Every output
+    of every step within 1e-5 of the fp64 oracle; kept sets and rows
+    bit-exact after every event."""
+    log("tiny config full run, trigger every %d" % every)
+    run = Run(L=1, Hq=4, Hkv=2, K=256, lps=[128], r=64, every=every, dtype=B.RA_F32,
               scaled=False, seeds=[1000], rids=[0])
     o = OracleSeq(run, 0)
     worst = 0.0
@@ -343,15 +343,14 @@ def test_tiny_config_full_run():
     for t in range(1024):
         outs, ev = run.step()
         o.rep.append()
-        err = max_abs(outs[0, 0].cpu(), o.attend(0, t))
+        err = attn_err(outs[0, 0].cpu(), o.attend(0, t), B.RA_F32, (t,))
         worst = max(worst, err)
-        assert err <= 1e-5, (t, err)
         o.rep.end_step()
         if ev:
             events += 1
             _check_heads(run, [o])
     log("  events=%d worst=%.3g" % (events, worst))
-    assert events == 11
+    assert events == n_events
     run.close()
 
 

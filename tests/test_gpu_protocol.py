@@ -10,7 +10,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_harness import TOL, OracleSeq, Run, check_heads, log, max_abs
+from gpu_harness import TOL, attn_err, OracleSeq, Run, check_heads, log, max_abs
 from paper_2609_03430_amd import binding as B
 
 pytestmark = pytest.mark.gpu
@@ -75,8 +75,7 @@ def test_refused_calls_leave_the_state_unchanged():
     for o in oracles:
         o.rep.append()
         for layer, got in ((0, out), (1, out1)):
-            err = max_abs(got[o.slot].float().cpu(), o.attend(layer, 30))
-            assert err <= TOL[B.RA_BF16], (layer, o.slot, err)
+            err = attn_err(got[o.slot].float().cpu(), o.attend(layer, 30), B.RA_BF16, (layer, o.slot,))
         o.rep.end_step()
     check_heads(run, oracles)
     run.close()
@@ -158,10 +157,45 @@ def test_no_active_sequence_and_gaps_between_slots():
         run.steps = [s + 1 for s in run.steps]
         o.rep.append()
         for layer in range(run.L):
-            err = max_abs(outs[layer, 1].float().cpu(), o.attend(layer, t))
-            assert err <= TOL[B.RA_BF16], (t, layer, err)
+            err = attn_err(outs[layer, 1].float().cpu(), o.attend(layer, t), B.RA_BF16, (t, layer,))
         assert bool((outs[:, 0] == sentinel).all()) and bool((outs[:, 2] == sentinel).all())
         o.rep.end_step()
     assert events == 3
     check_heads(run, [o])
+    run.close()
+
+
+def test_binding_refuses_tensors_the_call_would_misread():
+    """The binding checks every tensor before its pointer crosses the ABI: a
+    host tensor, a non-contiguous view, another dtype than the cache's, or
+    fewer elements than the call reads or writes is refused with
+    RA_ERR_INVALID_ARG and nothing is launched; the step then runs normally."""
+    log("binding tensor checks")
+    run = Run(L=1, Hq=4, Hkv=2, K=16, lps=[5, 9], r=8, every=8)
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    q, k, v = run.step_inputs(0)
+    out = torch.zeros(run.max_seqs, run.Hq, 128, dtype=torch.bfloat16, device="cuda")
+    ws = run.cache.workspace
+    bad = [
+        (q.cpu(), k, v, out),                                   # host memory
+        (q.transpose(0, 1), k, v, out),                         # non-contiguous view
+        (q.float(), k, v, out),                                 # fp32 into a bf16 cache
+        (q, k[:1], v, out),                                     # too few rows
+        (q, k, v, out.view(-1)[:-1]),                           # output one element short
+    ]
+    for args in bad:
+        assert _status(B.ra_decode_attention, run.h, 0, *args, ws) == B.RA_ERR_INVALID_ARG
+    kr = torch.zeros(run.L * run.Hkv * 5 * 128 - 1, dtype=torch.bfloat16, device="cuda")
+    assert _status(B.ra_write_rows, run.h, 0, kr, kr) == B.RA_ERR_INVALID_ARG
+    ko = torch.zeros(8, 128, dtype=torch.float32, device="cuda")
+    assert _status(B.ra_read_rows, run.h, 1, 0, 0, ko, None) == B.RA_ERR_INVALID_ARG
+    torch.cuda.synchronize()
+    assert float(out.float().abs().max()) == 0.0
+    run.cache.decode(0, q, k, v, out)
+    B.ra_end_step(run.h)
+    for o in oracles:
+        o.rep.append()
+        err = attn_err(out[o.slot].float().cpu(), o.attend(0, 0), B.RA_BF16, (o.slot,))
+        o.rep.end_step()
+    check_heads(run, oracles)
     run.close()

@@ -13,7 +13,7 @@ eighth event and at the end.
 import numpy as np
 import pytest
 
-from gpu_harness import TOL, OracleSeq, Run, check_heads, log, max_abs
+from gpu_harness import OracleSeq, Run, attn_err, check_heads, log
 from paper_2609_03430_amd import binding as B
 
 pytestmark = pytest.mark.gpu
@@ -56,7 +56,6 @@ def test_random_config_parity(case):
               seeds=[case * 7919 + s for s in range(len(c["lps"]))],
               rids=[case * 31 + s for s in range(len(c["lps"]))], wl_seed=500 + case)
     oracles = [OracleSeq(run, s) for s in range(run.n)]
-    tol = TOL[c["dtype"]]
     worst, events = 0.0, 0
     for t in range(c["T"]):
         outs, ev = run.step()
@@ -64,9 +63,8 @@ def test_random_config_parity(case):
         for o in oracles:
             o.rep.append()
             for layer in range(run.L):
-                err = max_abs(outs[layer, o.slot], o.attend(layer, t))
+                err = attn_err(outs[layer, o.slot], o.attend(layer, t), c["dtype"], (case, t, o.slot, layer,))
                 worst = max(worst, err)
-                assert err <= tol, (case, t, o.slot, layer, err)
             o.rep.end_step()
         if ev:
             events += 1

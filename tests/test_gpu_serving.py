@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_harness import OracleSeq, Run, log, max_abs
+from gpu_harness import OracleSeq, Run, attn_err, log
 from paper_2609_03430_amd import binding as B
 
 pytestmark = pytest.mark.gpu
@@ -64,9 +64,9 @@ def test_requests_finish_and_are_replaced(layout):
             o.rep.append()
             if check:
                 for layer in range(run.L):
-                    err = max_abs(outs[layer, s], o.attend(layer, o.rep.step - 1))
+                    err = attn_err(outs[layer, s], o.attend(layer, o.rep.step - 1),
+                                   B.RA_BF16, (s, o.rid, layer))
                     worst = max(worst, err)
-                    assert err <= 2e-2, (s, o.rid, layer, err)
             if o.rep.end_step():
                 _check_sets(run, o)
         for s in list(live):

@@ -41,8 +41,16 @@ def test_window_scores_and_selection(Hq, Hkv):
         for o in oracles:
             o.rep.append()
             o.rep.end_step()
+    _select_and_check(run, oracles, n_steps, stride=1024)
+    run.close()
+
+
+def _select_and_check(run, oracles, n_steps, stride):
+    """Run the scorer on every slot of `run` after `n_steps` decode steps and
+    check its raw scores against the fp64 oracle and its drops as a valid
+    lowest-m selection of the oracle's pooled scores."""
+    L, Hkv, r, every = run.L, run.Hkv, run.r, run.every
     qw = _qwin(run, n_steps)
-    stride = 1024
     scores = torch.zeros(run.n, L, Hkv, stride, dtype=torch.float32, device="cuda")
     drops = torch.full((run.n, L, Hkv, every), -1, dtype=torch.int32, device="cuda")
     B.ra_window_select(run.h, 0, run.n, qw, scores, stride, drops)
@@ -74,4 +82,27 @@ def test_window_scores_and_selection(Hq, Hkv):
                 kept = np.setdiff1d(np.arange(n - r), d)
                 assert np.all(pooled[d] <= thr + tol), (b, l, g)
                 assert np.all(pooled[kept] >= thr - tol), (b, l, g)
+
+
+@pytest.mark.parametrize("K,lps,steps,Hq,Hkv", [
+    (4096, [1024, 300], 4190, 8, 2),       # 5,214 rows: the 16-keys-per-thread build
+    (8192, [2048, 100], 8300, 8, 2),       # 10,348 rows: the 32-keys-per-thread build
+    (8192, [2048, 100], 8300, 10, 2),      #   the same with G = 5 (three tiles per wave)
+])
+def test_window_select_large_caches(K, lps, steps, Hq, Hkv):
+    """Caches of the Phi-4-shaped batch's size (prompts up to 2,048, K = 8,192):
+    the selection holds 16 or 32 keys per thread.  The state is reached by a
+    positions-only fast forward to a step before the next trigger, so the
+    rows over budget (steps - r - K) are fewer than evict_every, and the
+    cached rows are materialised from the generator."""
+    log("window scorer large caches K=%d lps=%s steps=%d Hq=%d" % (K, lps, steps, Hq))
+    run = Run(L=2, Hq=Hq, Hkv=Hkv, K=K, lps=lps, r=64, every=64, write_prompt=False,
+              wl_seed=1004)
+    run.fast_forward(steps)
+    for b in range(run.n):
+        run.materialise(b)
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    for o in oracles:
+        o.advance(steps)
+    _select_and_check(run, oracles, steps, stride=16384)
     run.close()
