@@ -22,7 +22,8 @@
  *   marked synchronous.
  * - The library never allocates device memory.  The caller owns the pools,
  *   the metadata buffer and the workspace and must keep them alive until
- *   ra_cache_destroy.  One ra_cache must be driven from one stream (calls
+ *   ra_cache_destroy.  (The one fixed device array the library holds, that
+ *   of ra_decode_attention_noalloc, comes with its code object.)  One ra_cache must be driven from one stream (calls
  *   are stream-ordered); it is not thread-safe.
  * - Every call returns an ra_status.  Shapes, capacities, budgets and the
  *   step protocol are validated on the host mirror BEFORE any launch, so an
@@ -250,6 +251,25 @@ ra_status ra_decode_attention(ra_cache* cache, int32_t layer, const void* q,
                               const void* k_new, const void* v_new, void* out,
                               void* workspace, size_t workspace_bytes,
                               void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * append + attention as ra_decode_attention, with the same arguments minus
+ * the workspace.  The split partial results go to a file-scope device array
+ * of RA_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on
+ * until the process ends (its address is looked up once per device, at
+ * ra_cache_create).  The call allocates nothing and calls no allocating
+ * routine.  It needs (slots up to the highest active one) * Hkv * splits * G
+ * * 130 * 4 bytes of that array when the launch has more than one split per
+ * head (always for f32; see ra_attention_plan), and returns RA_ERR_CAPACITY,
+ * before any launch, when that exceeds RA_NOALLOC_SCRATCH_BYTES.  Every call
+ * on one GPU shares the array, from any cache: calls that overlap on one GPU
+ * (other streams, other threads) race on it and must be serialised by the
+ * caller.  Nothing in the array needs to start at zero. */
+#define RA_NOALLOC_SCRATCH_BYTES (8u << 20)
+ra_status ra_decode_attention_noalloc(ra_cache* cache, int32_t layer, const void* q,
+                                      const void* k_new, const void* v_new, void* out,
+                                      void* stream);
 
 /* End the decode step of every active sequence: step += 1, then run the
  * periodic eviction (Eq. 1 with Random Attention's scores, Appendix F

@@ -33,6 +33,7 @@ RA_LAYOUT_CHRONOLOGICAL, RA_LAYOUT_HOLE_FILL = 0, 1
 RA_POLICY_RANDOM, RA_POLICY_SHARED, RA_POLICY_BLOCK, RA_POLICY_RECENCY = 0, 1, 2, 3
 RA_POLICY_EXTERNAL = 4
 RA_SCORER_SNAPKV, RA_SCORER_RKV, RA_SCORER_VASE = 0, 1, 2
+RA_NOALLOC_SCRATCH_BYTES = 8 << 20
 
 # Every entry point declared in include/randattn.h.
 EXPORTS = (
@@ -40,6 +41,7 @@ EXPORTS = (
     "ra_meta_bytes",
     "ra_workspace_bytes", "ra_cache_create", "ra_cache_destroy",
     "ra_seq_begin", "ra_seq_end", "ra_get_seq_info", "ra_decode_attention",
+    "ra_decode_attention_noalloc",
     "ra_end_step", "ra_evict_now", "ra_fast_forward", "ra_export_positions",
     "ra_write_rows", "ra_read_rows", "ra_read_positions", "ra_status_string",
     "ra_last_hip_error", "ra_attention_plan", "ra_window_select",
@@ -102,6 +104,7 @@ _SIGS = {
     "ra_seq_end": (_I32, [_P, _I32, _P]),
     "ra_get_seq_info": (_I32, [_P, _I32, ctypes.POINTER(ra_seq_info)]),
     "ra_decode_attention": (_I32, [_P, _I32, _P, _P, _P, _P, _P, _SZ, _P]),
+    "ra_decode_attention_noalloc": (_I32, [_P, _I32, _P, _P, _P, _P, _P]),
     "ra_end_step": (_I32, [_P, _P, ctypes.POINTER(_I32)]),
     "ra_evict_now": (_I32, [_P, _I32, _P]),
     "ra_fast_forward": (_I32, [_P, _I32, _P]),
@@ -312,6 +315,15 @@ def ra_decode_attention(handle, layer, q, k_new, v_new, out, workspace,
                                       _stream(stream)), "ra_decode_attention")
 
 
+def ra_decode_attention_noalloc(handle, layer, q, k_new, v_new, out, stream=None):
+    """ra_decode_attention with the split partials in the library's fixed
+    device array (no workspace; see the header for its limit)."""
+    _decode_args(handle, "ra_decode_attention_noalloc", q, k_new, v_new, out)
+    _check(_lib().ra_decode_attention_noalloc(handle, int(layer), _ptr(q), _ptr(k_new),
+                                              _ptr(v_new), _ptr(out), _stream(stream)),
+           "ra_decode_attention_noalloc")
+
+
 def ra_end_step(handle, stream=None):
     n = ctypes.c_int32(0)
     _check(_lib().ra_end_step(handle, _stream(stream), ctypes.byref(n)),
@@ -456,3 +468,6 @@ class Cache:
     def decode(self, layer, q, k_new, v_new, out, stream=None):
         ra_decode_attention(self.handle, layer, q, k_new, v_new, out,
                             self.workspace, stream)
+
+    def decode_noalloc(self, layer, q, k_new, v_new, out, stream=None):
+        ra_decode_attention_noalloc(self.handle, layer, q, k_new, v_new, out, stream)

@@ -20,6 +20,9 @@
 
 using ra::SeqMeta;
 
+static_assert(RA_NOALLOC_SCRATCH_BYTES == ra::kNoAllocScratchBytes,
+              "the header's no-alloc limit is the size of the device array");
+
 namespace {
 
 std::atomic<int32_t> g_last_hip_error{0};
@@ -69,6 +72,7 @@ struct ra_cache {
   std::vector<uint8_t> appended;         // layers appended in the open step
   int n_appended = 0;
   int slot_lo = 0, slot_hi = 0;          // range covering the active slots
+  void* scratch = nullptr;               // device address of the no-alloc partials
 
   ra::Shape shape() const {
     return ra::Shape{cfg.num_layers, cfg.num_q_heads, cfg.num_kv_heads, G,
@@ -336,6 +340,13 @@ ra_status ra_cache_create(const ra_config* cfg, void* k_pool, void* v_pool,
     delete c;
     return hip_fail(e);
   }
+  // the allocation-free attention's partials: this device's copy of the
+  // library's static array (looked up once per device, with it current)
+  const hipError_t es = ra::scratch_address(&c->scratch);
+  if (es != hipSuccess) {
+    delete c;
+    return hip_fail(es);
+  }
   *out = c;
   return RA_OK;
 }
@@ -451,6 +462,24 @@ ra_status ra_decode_attention(ra_cache* c, int32_t layer, const void* q,
   return launch_decode(c, layer, q, k_new, v_new, out, attention_plan(c), ws,
                        ws + items * c->G * ra::kHeadDim, ra::kMaxSplits,
                        static_cast<hipStream_t>(stream));
+}
+
+ra_status ra_decode_attention_noalloc(ra_cache* c, int32_t layer, const void* q,
+                                      const void* k_new, const void* v_new, void* out,
+                                      void* stream) {
+  const ra_status st = check_decode(c, layer, q, k_new, v_new, out);
+  if (st != RA_OK) return st;
+  if (!c->scratch) return RA_ERR_STATE;
+  // partial slots only for the splits this launch has, packed per head
+  const Plan plan = attention_plan(c);
+  const size_t items = static_cast<size_t>(c->slot_hi) * c->cfg.num_kv_heads * plan.max_splits;
+  const size_t floats = items * c->G * ra::kHeadDim;
+  const bool partials = c->cfg.dtype == RA_F32 || plan.max_splits > 1;
+  if (partials && (floats + items * c->G * 2) * sizeof(float) > ra::kNoAllocScratchBytes)
+    return RA_ERR_CAPACITY;
+  float* ws = static_cast<float*>(c->scratch);
+  return launch_decode(c, layer, q, k_new, v_new, out, plan, ws, ws + floats,
+                       std::max(1, plan.max_splits), static_cast<hipStream_t>(stream));
 }
 
 ra_status ra_end_step(ra_cache* c, void* stream, int32_t* n_evicted) {

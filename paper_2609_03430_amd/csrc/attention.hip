@@ -30,6 +30,8 @@
 // row 4a+i holds key 8a+4t+i), so no data moves between lanes except the
 // two shuffles of the row maximum.
 // fp32 path (VALU): lanes own keys for the scores and channels for P.V.
+#include <mutex>
+
 #include "ra_internal.h"
 
 namespace ra {
@@ -652,6 +654,30 @@ hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s)
                        sh.Hq, sh.Hkv, false);
   }
   return hipGetLastError();
+}
+
+// Partials of the allocation-free attention entry point.  Every GPU the
+// library runs on holds its own copy until the process ends.  In host code
+// `scratch` names a host-side stand-in, not device memory: host code uses
+// only the address scratch_address returns.
+static __device__ __align__(256) float scratch[kNoAllocScratchBytes / sizeof(float)];
+
+hipError_t scratch_address(void** out) {
+  static std::mutex mu;
+  static void* addr[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return hipSuccess;
 }
 
 }  // namespace ra

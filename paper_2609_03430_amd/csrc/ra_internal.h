@@ -95,6 +95,12 @@ struct AttnLaunch {
 };
 hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s);
 
+// The allocation-free attention's partials: a file-scope device array of
+// kNoAllocScratchBytes (attention.hip).  scratch_address returns its device
+// address on the current device, looked up once per device.
+constexpr size_t kNoAllocScratchBytes = size_t(8) << 20;
+hipError_t scratch_address(void** out);
+
 // Score-based rounds (measurement only): compaction from given drop lists,
 // and the plan rule applied to a slot range.
 hipError_t launch_compact_drops(const Shape& sh, const SeqMeta* meta, void* kpool,
