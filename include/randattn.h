@@ -97,15 +97,34 @@ typedef struct {
   int32_t layout;         /* ra_layout: row order kept in each region */
   int32_t policy;         /* ra_policy: which candidates an eviction keeps */
   int32_t policy_block;   /* RA_POLICY_BLOCK: tokens per block (>= 1) */
+  int32_t page_rows;      /* RA_LAYOUT_PAGED: rows per page, a power of two in
+                             [32, 1024] (ignored by the other layouts) */
+  int32_t max_prompt_len; /* RA_LAYOUT_PAGED: longest prompt ra_seq_begin
+                             accepts; sizes the block tables (ignored by the
+                             other layouts) */
 } ra_config;
 
 typedef enum {
   RA_LAYOUT_CHRONOLOGICAL = 0, /* rows in position order; an eviction shifts every
                                   survivor after the first drop (Appendix F: keep
                                   sets sorted chronologically, gather compaction) */
-  RA_LAYOUT_HOLE_FILL = 1      /* an eviction moves only the surviving rows of the
+  RA_LAYOUT_HOLE_FILL = 1,     /* an eviction moves only the surviving rows of the
                                   last m slots into the holes; rows are unordered
                                   (positions travel with them); the same kept sets */
+  RA_LAYOUT_PAGED = 2          /* rows in position order in fixed pages of page_rows
+                                  rows mapped by a block table per sequence (Appendix
+                                  G: physical eviction under paging rewrites each
+                                  request's surviving KV into its blocks, frees the
+                                  tail and keeps positions logical).  The pool is a
+                                  sequence of page groups of L * Hkv pages, one per
+                                  (layer, KV head): every head of a sequence holds
+                                  the same number of rows, so one table entry maps
+                                  one group.  A group is taken from the pool's free
+                                  list when an append needs a new page and returned
+                                  when an eviction or ra_seq_end releases it; an
+                                  event keeps the chronological order (the same
+                                  shift as RA_LAYOUT_CHRONOLOGICAL through the
+                                  table) and frees the pages past the new length */
 } ra_layout;
 
 typedef enum {
@@ -175,11 +194,14 @@ typedef struct {
 ra_status ra_config_check(const ra_config* cfg);
 
 /* Row capacity of one (layer, KV head) region for a prompt of prompt_len:
- * lp + k_keep + recent_r + evict_every rounded up to a multiple of 32.
- * Negative ra_status on error (bad config, TOTAL mode with lp > K). */
+ * lp + k_keep + recent_r + evict_every rounded up to a multiple of 32 (of
+ * page_rows in the paged layout, where it is the most rows a head of such a
+ * sequence ever holds).  Negative ra_status on error (bad config, TOTAL mode
+ * with lp > K, a paged prompt longer than max_prompt_len). */
 int64_t ra_region_rows(const ra_config* cfg, int32_t prompt_len);
 
-/* Pool rows one sequence occupies: L * Hkv * ra_region_rows.  The K and V
+/* Pool rows one sequence occupies: L * Hkv * ra_region_rows (in the paged
+ * layout, at most: it holds pages only for the rows it has).  The K and V
  * pools hold pool_rows * head_dim elements each, the position pool
  * pool_rows int32.  Negative ra_status on error. */
 int64_t ra_seq_rows(const ra_config* cfg, int32_t prompt_len);
@@ -191,8 +213,9 @@ int64_t ra_seq_rows(const ra_config* cfg, int32_t prompt_len);
 int64_t ra_required_slots(const ra_config* cfg, const int32_t* host_prompt_lens,
                           int32_t n_seqs);
 
-/* Bytes of the persistent device metadata buffer (per-slot state).
- * 0 on a bad config. */
+/* Bytes of the persistent device metadata buffer (per-slot state; in the
+ * paged layout also the block tables, max_seqs * ceil((max_prompt_len +
+ * k_keep + recent_r + evict_every) / page_rows) int32).  0 on a bad config. */
 size_t ra_meta_bytes(const ra_config* cfg);
 
 /* Bytes of the attention workspace (split partial results) that
@@ -205,9 +228,12 @@ size_t ra_workspace_bytes(const ra_config* cfg);
  *   k_pool, v_pool: pool_rows * head_dim elements of cfg->dtype each;
  *   pos_pool:       pool_rows int32;
  *   meta:           ra_meta_bytes(cfg) bytes (zeroed here on `stream`).
- * Keys are stored row-major per region; values in tiles of 8 rows stored
- * transposed ([row/8][head_dim][8]); positions row-major.  Sequences are
- * placed by a first-fit allocator over the pool at ra_seq_begin. */
+ * pool_rows is a multiple of 32 (of L * Hkv * page_rows, one page group, in
+ * the paged layout).  Keys are stored row-major; values in tiles of 8 rows
+ * stored transposed ([row/8][head_dim][8]); positions row-major.  Contiguous
+ * layouts place each sequence's regions by a first-fit allocator over the
+ * pool at ra_seq_begin; the paged layout hands out page groups from a free
+ * list as rows are appended. */
 ra_status ra_cache_create(const ra_config* cfg, void* k_pool, void* v_pool,
                           int32_t* pos_pool, int64_t pool_rows, void* meta,
                           size_t meta_bytes, void* stream, ra_cache** out);
@@ -216,13 +242,20 @@ ra_status ra_cache_destroy(ra_cache* cache);
 
 /* ---- sequences ----------------------------------------------------------- */
 
+/* Pool occupancy (host mirror, no device access): rows in use by sequences
+ * and rows free (contiguous layouts: the first-fit free list, whose largest
+ * hole bounds the next admission; paged: free page groups * L * Hkv *
+ * page_rows).  Either output may be NULL. */
+ra_status ra_pool_info(const ra_cache* cache, int64_t* used_rows, int64_t* free_rows);
+
 /* Pin a prompt into slot `seq` (Section 3: the prompt is never evicted).
  * dev_k_prompt / dev_v_prompt: [L][Hkv][prompt_len][head_dim] row-major, or
  * both NULL to leave the prompt rows unwritten (positions are still set;
  * the rows are then expected from ra_write_rows).  `seed` and `request_id`
  * key every eviction draw of this sequence.  Errors: RA_ERR_STATE if the
  * slot is active, RA_ERR_BUDGET (TOTAL mode, lp > K), RA_ERR_CAPACITY if
- * the pool has no room. */
+ * the pool has no room (paged: for the prompt's pages) or a paged prompt is
+ * longer than max_prompt_len. */
 ra_status ra_seq_begin(ra_cache* cache, int32_t seq, int32_t prompt_len,
                        uint64_t seed, uint64_t request_id,
                        const void* dev_k_prompt, const void* dev_v_prompt,
@@ -246,7 +279,10 @@ ra_status ra_get_seq_info(const ra_cache* cache, int32_t seq, ra_seq_info* out);
  * KV head of `layer`, and query head h attends, with softmax over
  * q.k/sqrt(d), to every cached pair of KV head h / G, the new one included.
  * Each layer must be called once per step (RA_ERR_STATE otherwise) and
- * RA_ERR_CAPACITY is returned before a region would overflow. */
+ * RA_ERR_CAPACITY is returned before a region would overflow.  In the paged
+ * layout the first layer of a step takes a page group for every sequence
+ * whose new row starts a page; RA_ERR_CAPACITY, before any launch, if the
+ * pool has too few free groups (ending a sequence frees its groups). */
 ra_status ra_decode_attention(ra_cache* cache, int32_t layer, const void* q,
                               const void* k_new, const void* v_new, void* out,
                               void* workspace, size_t workspace_bytes,

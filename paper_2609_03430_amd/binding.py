@@ -29,7 +29,7 @@ RA_ERR_HIP = -5
 RA_ERR_STATE = -6
 RA_F32, RA_BF16 = 0, 1
 RA_BUDGET_EVICTABLE, RA_BUDGET_TOTAL = 0, 1
-RA_LAYOUT_CHRONOLOGICAL, RA_LAYOUT_HOLE_FILL = 0, 1
+RA_LAYOUT_CHRONOLOGICAL, RA_LAYOUT_HOLE_FILL, RA_LAYOUT_PAGED = 0, 1, 2
 RA_POLICY_RANDOM, RA_POLICY_SHARED, RA_POLICY_BLOCK, RA_POLICY_RECENCY = 0, 1, 2, 3
 RA_POLICY_EXTERNAL = 4
 RA_SCORER_SNAPKV, RA_SCORER_RKV, RA_SCORER_VASE = 0, 1, 2
@@ -40,7 +40,7 @@ EXPORTS = (
     "ra_config_check", "ra_region_rows", "ra_seq_rows", "ra_required_slots",
     "ra_meta_bytes",
     "ra_workspace_bytes", "ra_cache_create", "ra_cache_destroy",
-    "ra_seq_begin", "ra_seq_end", "ra_get_seq_info", "ra_decode_attention",
+    "ra_pool_info", "ra_seq_begin", "ra_seq_end", "ra_get_seq_info", "ra_decode_attention",
     "ra_decode_attention_noalloc",
     "ra_end_step", "ra_evict_now", "ra_fast_forward", "ra_export_positions",
     "ra_write_rows", "ra_read_rows", "ra_read_positions", "ra_status_string",
@@ -62,7 +62,8 @@ class ra_config(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in (
         "num_layers", "num_q_heads", "num_kv_heads", "head_dim", "budget_k",
         "recent_r", "evict_every", "budget_mode", "dtype", "max_seqs",
-        "attn_split", "layout", "policy", "policy_block")]
+        "attn_split", "layout", "policy", "policy_block", "page_rows",
+        "max_prompt_len")]
 
 
 class ra_scorer_params(ctypes.Structure):
@@ -100,6 +101,7 @@ _SIGS = {
     "ra_cache_create": (_I32, [_CFG, _P, _P, _P, _I64, _P, _SZ, _P,
                                ctypes.POINTER(_P)]),
     "ra_cache_destroy": (_I32, [_P]),
+    "ra_pool_info": (_I32, [_P, ctypes.POINTER(_I64), ctypes.POINTER(_I64)]),
     "ra_seq_begin": (_I32, [_P, _I32, _I32, _U64, _U64, _P, _P, _P]),
     "ra_seq_end": (_I32, [_P, _I32, _P]),
     "ra_get_seq_info": (_I32, [_P, _I32, ctypes.POINTER(ra_seq_info)]),
@@ -202,10 +204,12 @@ def make_config(num_layers, num_q_heads, num_kv_heads, budget_k, recent_r=64,
                 evict_every=64, budget_mode=RA_BUDGET_EVICTABLE, dtype=RA_BF16,
                 max_seqs=1, head_dim=128, attn_split=0,
                 layout=RA_LAYOUT_CHRONOLOGICAL, policy=RA_POLICY_RANDOM,
-                policy_block=1):
+                policy_block=1, page_rows=64, max_prompt_len=0):
+    """page_rows and max_prompt_len apply to RA_LAYOUT_PAGED only."""
     return ra_config(num_layers, num_q_heads, num_kv_heads, head_dim, budget_k,
                      recent_r, evict_every, budget_mode, dtype, max_seqs,
-                     attn_split, layout, policy, policy_block)
+                     attn_split, layout, policy, policy_block, page_rows,
+                     max_prompt_len)
 
 
 # ---- one wrapper per C entry point ------------------------------------------
@@ -269,6 +273,14 @@ def ra_cache_create(cfg, k_pool, v_pool, pos_pool, pool_rows, meta, stream=None)
 def ra_cache_destroy(handle):
     _check(_lib().ra_cache_destroy(handle), "ra_cache_destroy")
     _CONFIGS.pop(getattr(handle, "value", handle), None)
+
+
+def ra_pool_info(handle):
+    """(used_rows, free_rows) of the cache's pool (host mirror)."""
+    used, free = ctypes.c_int64(0), ctypes.c_int64(0)
+    _check(_lib().ra_pool_info(handle, ctypes.byref(used), ctypes.byref(free)),
+           "ra_pool_info")
+    return used.value, free.value
 
 
 def ra_seq_begin(handle, seq, prompt_len, seed, request_id, k_prompt=None,

@@ -56,6 +56,31 @@ int64_t keep_rows(const ra_config& c, int32_t lp) {
   return static_cast<int64_t>(c.budget_k) - lp;
 }
 
+bool paged(const ra_config& c) { return c.layout == RA_LAYOUT_PAGED; }
+
+int log2_exact(int x) {
+  int k = 0;
+  while ((1 << k) < x) ++k;
+  return (1 << k) == x ? k : -1;
+}
+
+// Most rows a head of the paged layout ever holds, over the prompts it
+// accepts: lp + k_keep + r + R (the prompt counts against K in TOTAL mode).
+int64_t paged_rows_max(const ra_config& c) {
+  const int64_t held = c.budget_mode == RA_BUDGET_TOTAL
+                           ? static_cast<int64_t>(c.budget_k)
+                           : static_cast<int64_t>(c.max_prompt_len) + c.budget_k;
+  return held + c.recent_r + c.evict_every;
+}
+
+int64_t pages_per_seq(const ra_config& c) {
+  return (paged_rows_max(c) + c.page_rows - 1) / c.page_rows;
+}
+
+size_t meta_records_bytes(const ra_config& c) {
+  return static_cast<size_t>(round_up(static_cast<int64_t>(sizeof(SeqMeta)) * c.max_seqs, 256));
+}
+
 }  // namespace
 
 struct ra_cache {
@@ -72,12 +97,47 @@ struct ra_cache {
   std::vector<uint8_t> appended;         // layers appended in the open step
   int n_appended = 0;
   int slot_lo = 0, slot_hi = 0;          // range covering the active slots
+  // paged layout
+  ra::Paging pg{};                       // device tables and page geometry
+  int page_rows = 0;
+  int64_t n_groups = 0;                  // page groups in the pool
+  std::vector<int32_t> free_groups;      // stack: the next group is back()
+  std::vector<std::vector<int32_t>> groups;   // per slot: its table, in order
   void* scratch = nullptr;               // device address of the no-alloc partials
 
   ra::Shape shape() const {
     return ra::Shape{cfg.num_layers, cfg.num_q_heads, cfg.num_kv_heads, G,
                      cfg.recent_r, cfg.evict_every, cfg.dtype, cfg.layout,
-                     cfg.policy, std::max(1, cfg.policy_block)};
+                     cfg.policy, std::max(1, cfg.policy_block), pg};
+  }
+  bool is_paged() const { return cfg.layout == RA_LAYOUT_PAGED; }
+  int64_t pages_for(int64_t rows) const { return (rows + page_rows - 1) / page_rows; }
+  // paged: page groups slot `s` must add to hold `rows` rows
+  // paged: whether `rows` rows fit the block table of one sequence (rows
+  // pile up past lp + k_keep + r + R only under the external policy)
+  bool fits_table(int64_t rows) const { return pages_for(rows) <= pg.pages_per_seq; }
+  int64_t groups_short(int s, int64_t rows) const {
+    return std::max<int64_t>(0, pages_for(rows) - static_cast<int64_t>(groups[s].size()));
+  }
+  // paged: take groups from the free list until slot `s` holds `rows` rows;
+  // the new table entries are appended to `out` (the caller checked that
+  // enough groups are free)
+  void grow(int s, int64_t rows, std::vector<ra::TableEntry>& out) {
+    while (static_cast<int64_t>(groups[s].size()) < pages_for(rows)) {
+      const int32_t g = free_groups.back();
+      free_groups.pop_back();
+      out.push_back(ra::TableEntry{s, static_cast<int32_t>(groups[s].size()), g});
+      groups[s].push_back(g);
+    }
+    mirror[s].cap = static_cast<int32_t>(groups[s].size()) * page_rows;
+  }
+  // paged: return the groups past the first pages_for(rows) to the free list
+  void shrink(int s, int64_t rows) {
+    while (static_cast<int64_t>(groups[s].size()) > pages_for(rows)) {
+      free_groups.push_back(groups[s].back());
+      groups[s].pop_back();
+    }
+    mirror[s].cap = static_cast<int32_t>(groups[s].size()) * page_rows;
   }
   bool step_open() const { return n_appended != 0; }
   void update_range() {
@@ -178,6 +238,17 @@ ra_status check_decode(const ra_cache* c, int32_t layer, const void* q, const vo
   if (!c || layer < 0 || layer >= c->cfg.num_layers || !q || !k_new || !v_new || !out)
     return RA_ERR_INVALID_ARG;
   if (c->appended[layer]) return RA_ERR_STATE;
+  if (c->is_paged()) {
+    // the step's new rows may start pages: enough free groups for all of them
+    int64_t short_groups = 0;
+    for (int s = c->slot_lo; s < c->slot_hi; ++s) {
+      if (!c->mirror[s].active) continue;
+      if (!c->fits_table(c->mirror[s].len + 1)) return RA_ERR_CAPACITY;
+      short_groups += c->groups_short(s, c->mirror[s].len + 1);
+    }
+    if (short_groups > static_cast<int64_t>(c->free_groups.size())) return RA_ERR_CAPACITY;
+    return RA_OK;
+  }
   for (int s = c->slot_lo; s < c->slot_hi; ++s)
     if (c->mirror[s].active && c->mirror[s].len + 1 > c->mirror[s].cap) return RA_ERR_CAPACITY;
   return RA_OK;
@@ -188,6 +259,17 @@ ra_status check_decode(const ra_cache* c, int32_t layer, const void* q, const vo
 ra_status launch_decode(ra_cache* c, int32_t layer, const void* q, const void* k_new,
                         const void* v_new, void* out, const Plan& plan, float* ws_o,
                         float* ws_ml, int split_stride, hipStream_t stream) {
+  if (c->is_paged()) {
+    // pages for the rows this step appends (the first layer of the step)
+    std::vector<ra::TableEntry> te;
+    for (int s = c->slot_lo; s < c->slot_hi; ++s)
+      if (c->mirror[s].active) c->grow(s, c->mirror[s].len + 1, te);
+    if (!te.empty()) {
+      const hipError_t e = ra::launch_table_set(c->shape(), te.data(),
+                                                static_cast<int>(te.size()), stream);
+      if (e != hipSuccess) return hip_fail(e);
+    }
+  }
   c->appended[layer] = 1;
   ++c->n_appended;
   if (c->slot_hi <= c->slot_lo) return RA_OK;
@@ -245,11 +327,19 @@ ra_status ra_config_check(const ra_config* c) {
       c->max_seqs > 65536 || c->attn_split < 0 || c->attn_split % 32 != 0 ||
       (c->budget_mode != RA_BUDGET_EVICTABLE && c->budget_mode != RA_BUDGET_TOTAL) ||
       (c->dtype != RA_F32 && c->dtype != RA_BF16) || c->num_layers > 4096 ||
-      (c->layout != RA_LAYOUT_CHRONOLOGICAL && c->layout != RA_LAYOUT_HOLE_FILL) ||
+      (c->layout != RA_LAYOUT_CHRONOLOGICAL && c->layout != RA_LAYOUT_HOLE_FILL &&
+       c->layout != RA_LAYOUT_PAGED) ||
       c->policy < RA_POLICY_RANDOM || c->policy > RA_POLICY_EXTERNAL ||
       (c->policy == RA_POLICY_BLOCK && c->policy_block < 1) ||
       c->num_kv_heads > 4096)
     return RA_ERR_INVALID_ARG;
+  if (paged(*c)) {
+    if (c->page_rows < 32 || c->page_rows > 1024 || log2_exact(c->page_rows) < 0 ||
+        c->max_prompt_len < 0 ||
+        (c->budget_mode == RA_BUDGET_TOTAL && c->max_prompt_len > c->budget_k))
+      return RA_ERR_INVALID_ARG;
+    if (pages_per_seq(*c) > (int64_t(1) << 20)) return RA_ERR_UNSUPPORTED;
+  }
   if (c->head_dim != ra::kHeadDim) return RA_ERR_UNSUPPORTED;
   if (c->num_q_heads / c->num_kv_heads > ra::kMaxGroup) return RA_ERR_UNSUPPORTED;
   if (c->evict_every > ra::kMaxEvery) return RA_ERR_UNSUPPORTED;
@@ -267,8 +357,10 @@ int64_t ra_region_rows(const ra_config* c, int32_t prompt_len) {
   if (prompt_len < 0) return RA_ERR_INVALID_ARG;
   const int64_t k = keep_rows(*c, prompt_len);
   if (k < 0) return RA_ERR_BUDGET;
+  if (paged(*c) && prompt_len > c->max_prompt_len) return RA_ERR_CAPACITY;
   const int64_t rows = round_up(static_cast<int64_t>(prompt_len) + k + c->recent_r +
-                                    c->evict_every, ra::kRegionAlign);
+                                    c->evict_every,
+                                paged(*c) ? c->page_rows : ra::kRegionAlign);
   if (rows > (int64_t(1) << 30)) return RA_ERR_UNSUPPORTED;
   return rows;
 }
@@ -294,8 +386,11 @@ int64_t ra_required_slots(const ra_config* c, const int32_t* prompt_lens, int32_
 
 size_t ra_meta_bytes(const ra_config* c) {
   if (ra_config_check(c) != RA_OK) return 0;
-  const size_t metas = sizeof(SeqMeta) * static_cast<size_t>(c->max_seqs);
-  return round_up(static_cast<int64_t>(metas), 256);
+  size_t bytes = meta_records_bytes(*c);
+  if (paged(*c))
+    bytes += static_cast<size_t>(round_up(
+        static_cast<int64_t>(sizeof(int32_t)) * c->max_seqs * pages_per_seq(*c), 256));
+  return bytes;
 }
 
 size_t ra_workspace_bytes(const ra_config* c) {
@@ -315,6 +410,11 @@ ra_status ra_cache_create(const ra_config* cfg, void* k_pool, void* v_pool,
   if (!k_pool || !v_pool || !pos_pool || !meta || pool_rows <= 0 ||
       pool_rows % ra::kRegionAlign != 0 || meta_bytes < ra_meta_bytes(cfg))
     return RA_ERR_INVALID_ARG;
+  const int64_t group_rows = paged(*cfg) ? static_cast<int64_t>(cfg->num_layers) *
+                                               cfg->num_kv_heads * cfg->page_rows
+                                         : 0;
+  if (paged(*cfg) && (pool_rows % group_rows != 0 || pool_rows / group_rows > INT32_MAX))
+    return RA_ERR_INVALID_ARG;
   const auto misaligned = [](const void* p) {
     return (reinterpret_cast<uintptr_t>(p) & 15u) != 0;
   };
@@ -333,6 +433,19 @@ ra_status ra_cache_create(const ra_config* cfg, void* k_pool, void* v_pool,
   c->mirror.assign(cfg->max_seqs, SeqMeta{});
   c->free_rows[0] = pool_rows;
   c->appended.assign(cfg->num_layers, 0);
+  if (paged(*cfg)) {
+    c->page_rows = cfg->page_rows;
+    c->n_groups = pool_rows / group_rows;
+    c->pg.tables = reinterpret_cast<const int32_t*>(static_cast<char*>(meta) +
+                                                    meta_records_bytes(*cfg));
+    c->pg.pages_per_seq = static_cast<int>(pages_per_seq(*cfg));
+    c->pg.page_shift = log2_exact(cfg->page_rows);
+    c->pg.group_rows = group_rows;
+    c->free_groups.resize(c->n_groups);
+    for (int64_t i = 0; i < c->n_groups; ++i)
+      c->free_groups[i] = static_cast<int32_t>(c->n_groups - 1 - i);   // 0 first
+    c->groups.assign(cfg->max_seqs, {});
+  }
   const hipError_t e = ra::launch_zero_words(static_cast<uint32_t*>(meta),
                                              static_cast<int64_t>(ra_meta_bytes(cfg) / 4),
                                              static_cast<hipStream_t>(stream));
@@ -381,6 +494,19 @@ ra_status ra_attention_plan(const ra_cache* c, int32_t* split_keys, int32_t* max
   return RA_OK;
 }
 
+ra_status ra_pool_info(const ra_cache* c, int64_t* used_rows, int64_t* free_rows) {
+  if (!c) return RA_ERR_INVALID_ARG;
+  int64_t free = 0;
+  if (c->is_paged()) {
+    free = static_cast<int64_t>(c->free_groups.size()) * c->pg.group_rows;
+  } else {
+    for (const auto& kv : c->free_rows) free += kv.second;
+  }
+  if (used_rows) *used_rows = c->pool_rows - free;
+  if (free_rows) *free_rows = free;
+  return RA_OK;
+}
+
 ra_status ra_seq_begin(ra_cache* c, int32_t seq, int32_t prompt_len, uint64_t seed,
                        uint64_t request_id, const void* dev_k_prompt,
                        const void* dev_v_prompt, void* stream) {
@@ -391,6 +517,29 @@ ra_status ra_seq_begin(ra_cache* c, int32_t seq, int32_t prompt_len, uint64_t se
   if (c->mirror[seq].active) return RA_ERR_STATE;
   const int64_t cap = ra_region_rows(&c->cfg, prompt_len);
   if (cap < 0) return static_cast<ra_status>(cap);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (c->is_paged()) {
+    // pages for the prompt rows; the first append takes the next page
+    if (c->groups_short(seq, prompt_len) > static_cast<int64_t>(c->free_groups.size()))
+      return RA_ERR_CAPACITY;
+    SeqMeta M{};
+    M.prompt_len = prompt_len;
+    M.len = prompt_len;
+    M.k_keep = static_cast<int32_t>(keep_rows(c->cfg, prompt_len));
+    M.seed = seed;
+    M.rid = request_id;
+    M.active = 1;
+    std::vector<ra::TableEntry> te;
+    c->grow(seq, prompt_len, te);
+    M.cap = c->mirror[seq].cap;
+    RA_LAUNCH(ra::launch_table_set(c->shape(), te.data(), static_cast<int>(te.size()), s));
+    RA_LAUNCH(ra::launch_write_rows(c->shape(), M, seq, prompt_len, dev_k_prompt,
+                                    dev_v_prompt, nullptr, c->kpool, c->vpool, c->pos, s));
+    RA_LAUNCH(ra::launch_seq_set(c->meta, seq, M, s));
+    c->mirror[seq] = M;
+    c->update_range();
+    return RA_OK;
+  }
   const int64_t need = cap * c->cfg.num_layers * c->cfg.num_kv_heads;
   auto it = c->free_rows.begin();
   for (; it != c->free_rows.end(); ++it)
@@ -407,10 +556,9 @@ ra_status ra_seq_begin(ra_cache* c, int32_t seq, int32_t prompt_len, uint64_t se
   M.seed = seed;
   M.rid = request_id;
   M.active = 1;
-  const hipStream_t s = static_cast<hipStream_t>(stream);
   // rows first, then the metadata that makes the slot active: a failed launch
   // leaves the slot inactive on the device as in the mirror
-  RA_LAUNCH(ra::launch_write_rows(c->shape(), base, M.cap, prompt_len, dev_k_prompt,
+  RA_LAUNCH(ra::launch_write_rows(c->shape(), M, seq, prompt_len, dev_k_prompt,
                                   dev_v_prompt, nullptr, c->kpool, c->vpool, c->pos, s));
   RA_LAUNCH(ra::launch_seq_set(c->meta, seq, M, s));
   const int64_t rest = it->second - need;
@@ -428,6 +576,12 @@ ra_status ra_seq_end(ra_cache* c, int32_t seq, void* stream) {
   if (!M.active) return RA_ERR_STATE;
   SeqMeta off{};
   RA_LAUNCH(ra::launch_seq_set(c->meta, seq, off, static_cast<hipStream_t>(stream)));
+  if (c->is_paged()) {
+    c->shrink(seq, 0);
+    M = SeqMeta{};
+    c->update_range();
+    return RA_OK;
+  }
   int64_t base = M.base;
   int64_t rows = static_cast<int64_t>(M.cap) * c->cfg.num_layers * c->cfg.num_kv_heads;
   // return the rows to the free list, merging with neighbours
@@ -501,6 +655,9 @@ ra_status ra_end_step(ra_cache* c, void* stream, int32_t* n_evicted) {
     M.len += 1;
     mirror_plan(M, c->cfg.recent_r, at_trigger(c->cfg, M.step));
     due += M.due;
+    // the pages past the new length are free once the event (launched below,
+    // ahead of any later use of them on this stream) has moved their rows
+    if (M.due && c->is_paged()) c->shrink(i, M.len);
   }
   if (due) {
     RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos,
@@ -528,6 +685,7 @@ ra_status ra_evict_now(ra_cache* c, int32_t seq, void* stream) {
   for (int i = c->slot_lo; i < c->slot_hi; ++i) c->mirror[i].due = 0;
   mirror_plan(M, c->cfg.recent_r, true);
   if (M.due) {
+    if (c->is_paged()) c->shrink(seq, M.len);
     RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos, seq,
                                seq + 1, c->span(M), false, s));
   }
@@ -544,24 +702,51 @@ ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
   // piling up under the external policy) is reported before any launch; the
   // second pass launches and updates the mirror.
   std::vector<SeqMeta> saved = c->mirror;
+  const std::vector<int32_t> saved_free = c->free_groups;
+  const std::vector<std::vector<int32_t>> saved_groups = c->groups;
+  auto restore = [&]() {
+    c->mirror = saved;
+    c->free_groups = saved_free;
+    c->groups = saved_groups;
+  };
   for (int pass = 0; pass < 2; ++pass) {
     const bool launch = pass == 1;
-    if (launch) c->mirror = saved;
+    if (launch) restore();
     int remaining = n_steps;
     while (remaining > 0 && c->slot_hi > c->slot_lo) {
       int run = remaining;
       for (int i = c->slot_lo; i < c->slot_hi; ++i)
         if (c->mirror[i].active) run = std::min(run, every - c->mirror[i].step % every);
-      for (int i = c->slot_lo; i < c->slot_hi; ++i) {
-        const SeqMeta& M = c->mirror[i];
-        if (M.active && M.len + run > M.cap) {
-          c->mirror = saved;
+      if (c->is_paged()) {
+        // pages for the run's rows
+        int64_t short_groups = 0;
+        bool fits = true;
+        for (int i = c->slot_lo; i < c->slot_hi; ++i) {
+          if (!c->mirror[i].active) continue;
+          fits = fits && c->fits_table(c->mirror[i].len + run);
+          short_groups += c->groups_short(i, c->mirror[i].len + run);
+        }
+        if (!fits || short_groups > static_cast<int64_t>(c->free_groups.size())) {
+          restore();
           return RA_ERR_CAPACITY;
+        }
+        std::vector<ra::TableEntry> te;
+        for (int i = c->slot_lo; i < c->slot_hi; ++i)
+          if (c->mirror[i].active) c->grow(i, c->mirror[i].len + run, te);
+        if (launch && !te.empty())
+          RA_LAUNCH(ra::launch_table_set(c->shape(), te.data(), static_cast<int>(te.size()), s));
+      } else {
+        for (int i = c->slot_lo; i < c->slot_hi; ++i) {
+          const SeqMeta& M = c->mirror[i];
+          if (M.active && M.len + run > M.cap) {
+            restore();
+            return RA_ERR_CAPACITY;
+          }
         }
       }
       if (launch) {
-        RA_LAUNCH(ra::launch_append_positions(c->meta, c->pos, c->slot_lo, c->slot_hi,
-                                              c->cfg.num_layers, c->cfg.num_kv_heads, run, s));
+        RA_LAUNCH(ra::launch_append_positions(c->shape(), c->meta, c->pos, c->slot_lo,
+                                              c->slot_hi, run, s));
         RA_LAUNCH(ra::launch_advance(c->meta, c->slot_lo, c->slot_hi, run, c->cfg.recent_r,
                                      trigger_every(c->cfg), s));
       }
@@ -573,6 +758,7 @@ ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
         M.len += run;
         mirror_plan(M, c->cfg.recent_r, at_trigger(c->cfg, M.step));
         due += M.due;
+        if (M.due && c->is_paged()) c->shrink(i, M.len);
       }
       if (due && launch) {
         RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos,
@@ -592,7 +778,7 @@ ra_status ra_export_positions(ra_cache* c, int32_t seq, int32_t* dev_out,
   if (!M.active) return RA_ERR_STATE;
   if (out_elems < static_cast<int64_t>(M.len) * c->cfg.num_layers * c->cfg.num_kv_heads)
     return RA_ERR_CAPACITY;
-  RA_LAUNCH(ra::launch_export_positions(c->shape(), M.base, M.cap, M.len, c->pos, dev_out,
+  RA_LAUNCH(ra::launch_export_positions(c->shape(), M, seq, M.len, c->pos, dev_out,
                                         static_cast<hipStream_t>(stream)));
   return RA_OK;
 }
@@ -604,7 +790,7 @@ ra_status ra_write_rows(ra_cache* c, int32_t seq, const void* dev_k, const void*
   const SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
   // positions are left as they are: pass the region's own positions through
-  RA_LAUNCH(ra::launch_write_rows(c->shape(), M.base, M.cap, M.len, dev_k, dev_v, nullptr,
+  RA_LAUNCH(ra::launch_write_rows(c->shape(), M, seq, M.len, dev_k, dev_v, nullptr,
                                   c->kpool, c->vpool, nullptr, static_cast<hipStream_t>(stream)));
   return RA_OK;
 }
@@ -617,9 +803,9 @@ ra_status ra_read_rows(ra_cache* c, int32_t seq, int32_t layer, int32_t kv_head,
   if (c->step_open()) return RA_ERR_STATE;
   const SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
-  const int64_t region = M.base + static_cast<int64_t>(layer * c->cfg.num_kv_heads + kv_head) * M.cap;
-  RA_LAUNCH(ra::launch_read_rows(c->shape(), region, M.len, c->kpool, c->vpool, dev_k_out,
-                                 dev_v_out, static_cast<hipStream_t>(stream)));
+  RA_LAUNCH(ra::launch_read_rows(c->shape(), M, seq, layer * c->cfg.num_kv_heads + kv_head,
+                                 M.len, c->kpool, c->vpool, dev_k_out, dev_v_out,
+                                 static_cast<hipStream_t>(stream)));
   return RA_OK;
 }
 
@@ -732,9 +918,19 @@ ra_status ra_read_positions(ra_cache* c, int32_t seq, int32_t layer, int32_t kv_
   if (!M.active) return RA_ERR_STATE;
   *n_out = M.len;
   if (host_cap < M.len) return RA_ERR_CAPACITY;
-  const int64_t region = M.base + static_cast<int64_t>(layer * c->cfg.num_kv_heads + kv_head) * M.cap;
+  const int lg = layer * c->cfg.num_kv_heads + kv_head;
   const hipStream_t s = static_cast<hipStream_t>(stream);
-  if (M.len > 0) {
+  if (c->is_paged()) {
+    // one copy per page of the head
+    for (int64_t k = 0; k * c->page_rows < M.len; ++k) {
+      const int64_t first = static_cast<int64_t>(c->groups[seq][k]) * c->pg.group_rows +
+                            static_cast<int64_t>(lg) * c->page_rows;
+      const int64_t n = std::min<int64_t>(c->page_rows, M.len - k * c->page_rows);
+      RA_LAUNCH(hipMemcpyAsync(host_out + k * c->page_rows, c->pos + first,
+                               sizeof(int32_t) * n, hipMemcpyDeviceToHost, s));
+    }
+  } else if (M.len > 0) {
+    const int64_t region = M.base + static_cast<int64_t>(lg) * M.cap;
     RA_LAUNCH(hipMemcpyAsync(host_out, c->pos + region, sizeof(int32_t) * M.len,
                              hipMemcpyDeviceToHost, s));
   }

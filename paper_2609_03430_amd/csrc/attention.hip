@@ -87,12 +87,12 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float x) {
 struct Work {
   int slot, g, split;
   int len, n_keys, k0, k1, nsplit;
-  int64_t region;  // first row of the (slot, layer, g) region
+  RowMap rm;       // where the rows of the (slot, layer, g) cache live
   bool valid;
 };
 
 __device__ __forceinline__ Work locate(const SeqMeta* meta, int layer, int Hkv,
-                                       int split_keys) {
+                                       int split_keys, const Paging& pg) {
   Work w;
   w.split = blockIdx.x;
   w.g = blockIdx.y;
@@ -106,20 +106,20 @@ __device__ __forceinline__ Work locate(const SeqMeta* meta, int layer, int Hkv,
   if (w.k0 >= w.n_keys) return w;
   w.k1 = min(w.k0 + split_keys, w.n_keys);
   w.nsplit = (w.n_keys + split_keys - 1) / split_keys;
-  w.region = M.base + static_cast<int64_t>(layer * Hkv + w.g) * M.cap;
+  w.rm = row_map(M, w.slot, layer * Hkv + w.g, pg);
   w.valid = true;
   return w;
 }
 
-// Store the step's new pair into the cache (row `len` of the region).
-template <typename E>
+// Store the step's new pair into the cache (row `len` of the head).
+template <typename E, bool PAGED>
 __device__ __forceinline__ void append_row(const Work& w, const SeqMeta* meta,
                                            int Hkv, const E* k_new,
                                            const E* v_new, E* kpool, E* vpool,
                                            int32_t* pos) {
   const int lane = threadIdx.x & 63;   // called by one whole wavefront
   const int64_t src = (static_cast<int64_t>(w.slot) * Hkv + w.g) * kHeadDim;
-  const int64_t row = w.region + w.len;
+  const int64_t row = pool_row<PAGED>(w.rm, w.len);
   for (int c = lane; c < kHeadDim; c += 64) {
     kpool[row * kHeadDim + c] = k_new[src + c];
     vpool[(row & ~int64_t(7)) * kHeadDim + c * 8 + (row & 7)] = v_new[src + c];
@@ -219,16 +219,17 @@ __device__ __forceinline__ LaneMap lane_map() {
   return m;
 }
 
-__device__ __forceinline__ void load_block(BlockRegs& b, const uint16_t* Kr,
-                                           const uint16_t* Vr, int kb,
-                                           const LaneMap& lm) {
+// Kb, Vb: the block's first key row and first value tile (32 consecutive
+// rows, within one page in the paged layout).
+__device__ __forceinline__ void load_block(BlockRegs& b, const uint16_t* Kb,
+                                           const uint16_t* Vb, const LaneMap& lm) {
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
-    const uint16_t* row = Kr + static_cast<int64_t>(kb + lm.krow[t]) * kHeadDim + lm.kcol;
+    const uint16_t* row = Kb + lm.krow[t] * kHeadDim + lm.kcol;
 #pragma unroll
     for (int s = 0; s < 4; ++s) b.k[t][s] = ld16(row + 32 * s);
   }
-  const uint16_t* vt = Vr + static_cast<int64_t>(kb + lm.vrow) * kHeadDim + lm.vch * 8;
+  const uint16_t* vt = Vb + lm.vrow * kHeadDim + lm.vch * 8;
 #pragma unroll
   for (int u = 0; u < 8; ++u) b.v[u] = ld16_stream(vt + 16 * 8 * u);
 }
@@ -298,20 +299,22 @@ __device__ __forceinline__ void compute_block(Softmax& st, const BlockRegs& b,
 // itself and no merge kernel runs.  MINW is the number of wavefronts per
 // SIMD the build must allow (1 lets the accumulators live in the
 // accumulation registers, 2 keeps each wavefront within 256 registers).
-template <int W, int MINW>
+template <int W, int MINW, bool PAGED>
 __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
-    AttnLaunch a, int G, int Hq, int Hkv, float scale_log2) {
+    AttnLaunch a, Paging pg, int G, int Hq, int Hkv, float scale_log2) {
   constexpr int kNBuf = 2;   // register buffers (3 or 4 measured no faster)
   __shared__ float s_m[W][kMaxGroup];
   __shared__ float s_l[W][kMaxGroup];
   __shared__ float s_o[W > 1 ? W : 1][kMaxGroup][kHeadDim];
-  const Work w = locate(a.meta, a.layer, Hkv, a.split_keys);
+  const Work w = locate(a.meta, a.layer, Hkv, a.split_keys, pg);
   if (!w.valid) return;
   const int wave = threadIdx.x >> 6;
   const int lane = threadIdx.x & 63, qi = lane & 15, grp = lane >> 4;
   const LaneMap lm = lane_map();
-  const uint16_t* Kr = static_cast<const uint16_t*>(a.kpool) + w.region * kHeadDim;
-  const uint16_t* Vr = static_cast<const uint16_t*>(a.vpool) + w.region * kHeadDim;
+  const uint16_t* kpool = static_cast<const uint16_t*>(a.kpool);
+  const uint16_t* vpool = static_cast<const uint16_t*>(a.vpool);
+  // the first row of key block kb (a multiple of 32) in the pools
+  auto block_row = [&](int kb) -> int64_t { return pool_row<PAGED>(w.rm, kb); };
   const uint16_t* kn = static_cast<const uint16_t*>(a.k_new) +
                        (static_cast<int64_t>(w.slot) * Hkv + w.g) * kHeadDim;
   const uint16_t* vn = static_cast<const uint16_t*>(a.v_new) +
@@ -354,13 +357,17 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
     const int last = nfull - 1;
     BlockRegs buf[kNBuf];
 #pragma unroll
-    for (int j = 0; j < kNBuf; ++j) load_block(buf[j], Kr, Vr, k0 + 32 * min(j, last), lm);
+    for (int j = 0; j < kNBuf; ++j) {
+      const int64_t br = block_row(k0 + 32 * min(j, last));
+      load_block(buf[j], kpool + br * kHeadDim, vpool + br * kHeadDim, lm);
+    }
     int i = 0;
     for (; i + kNBuf - 1 < nfull; i += kNBuf) {
 #pragma unroll
       for (int j = 0; j < kNBuf; ++j) {
         compute_block(st, buf[j], qop, scale_log2, 32);
-        load_block(buf[j], Kr, Vr, k0 + 32 * min(i + kNBuf + j, last), lm);
+        const int64_t br = block_row(k0 + 32 * min(i + kNBuf + j, last));
+        load_block(buf[j], kpool + br * kHeadDim, vpool + br * kHeadDim, lm);
       }
     }
 #pragma unroll
@@ -371,12 +378,17 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
     // tail block: cached rows below len, the new pair at len, masked above
     const int kb = k0 + 32 * nfull;
     const int limit = w.n_keys - kb;       // 1..32 valid keys
+    // rows below len of this block lie in its page (the page of row len may
+    // not be mapped yet when len is a multiple of 32: only rows < len are read)
+    const int64_t br = kb < w.len ? block_row(kb) : 0;
+    const uint16_t* Kb = kpool + br * kHeadDim;
+    const uint16_t* Vb = vpool + br * kHeadDim;
     BlockRegs b;
     const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const int key = kb + lm.krow[t];
-      const uint16_t* row = key < w.len ? Kr + static_cast<int64_t>(key) * kHeadDim : kn;
+      const uint16_t* row = key < w.len ? Kb + lm.krow[t] * kHeadDim : kn;
 #pragma unroll
       for (int s = 0; s < 4; ++s)
         b.k[t][s] = key <= w.len ? ld16(row + lm.kcol + 32 * s) : z;
@@ -385,7 +397,7 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int ch = 16 * u + lm.vch;
-      u32x4 v = key0 < w.len ? ld16(Vr + static_cast<int64_t>(key0) * kHeadDim + ch * 8) : z;
+      u32x4 v = key0 < w.len ? ld16(Vb + lm.vrow * kHeadDim + ch * 8) : z;
       uint16_t e8[8];
       __builtin_memcpy(e8, &v, 16);
 #pragma unroll
@@ -404,7 +416,7 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
   st.l += __shfl_xor(st.l, 32, 64);
 
   if (owns_last)
-    append_row<uint16_t>(w, a.meta, Hkv, static_cast<const uint16_t*>(a.k_new),
+    append_row<uint16_t, PAGED>(w, a.meta, Hkv, static_cast<const uint16_t*>(a.k_new),
                          static_cast<const uint16_t*>(a.v_new),
                          static_cast<uint16_t*>(a.kpool),
                          static_cast<uint16_t*>(a.vpool), a.pos);
@@ -476,19 +488,19 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
 // ---------------------------------------------------------------------------
 
 // GT: the group size when fixed at compile time (1, 2, 4, 8), 0 for any G.
-template <int GT>
-__global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G_rt,
+template <int GT, bool PAGED>
+__global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, Paging pg, int G_rt,
                                                       int Hq, int Hkv,
                                                       float scale_log2) {
   constexpr int kQ = GT > 0 ? GT : kMaxGroup;   // query slots in registers
   const int G = GT > 0 ? GT : G_rt;
   __shared__ float qs[kMaxGroup][kHeadDim];
   __shared__ float ps[kMaxGroup][64];
-  const Work w = locate(a.meta, a.layer, Hkv, a.split_keys);
+  const Work w = locate(a.meta, a.layer, Hkv, a.split_keys, pg);
   if (!w.valid) return;
   const int lane = threadIdx.x;
-  const float* Kr = static_cast<const float*>(a.kpool) + w.region * kHeadDim;
-  const float* Vr = static_cast<const float*>(a.vpool) + w.region * kHeadDim;
+  const float* kpool = static_cast<const float*>(a.kpool);
+  const float* vpool = static_cast<const float*>(a.vpool);
   const float* kn = static_cast<const float*>(a.k_new) +
                     (static_cast<int64_t>(w.slot) * Hkv + w.g) * kHeadDim;
   const float* vn = static_cast<const float*>(a.v_new) +
@@ -510,7 +522,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G_rt,
     // scores: lanes own keys
     const int key = kb + lane;
     const bool valid = key < w.k1;
-    const float* krow = key < w.len ? Kr + static_cast<int64_t>(key) * kHeadDim : kn;
+    const float* krow = key < w.len ? kpool + pool_row<PAGED>(w.rm, key) * kHeadDim : kn;
     float s[kQ];
 #pragma unroll
     for (int q = 0; q < kQ; ++q) s[q] = 0.f;
@@ -552,7 +564,9 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G_rt,
     for (int t = 0; t < 8; ++t) {
       if (t < ntile) {
         const int kt = kb + 8 * t;
-        const float* base = Vr + static_cast<int64_t>(kt) * kHeadDim;
+        // a tile of 8 rows lies in one page; only tiles holding a row below
+        // len are read from the pool (the others hold the new value or zero)
+        const float* base = vpool + (kt < w.len ? pool_row<PAGED>(w.rm, kt) : 0) * kHeadDim;
         const float4* s0 = reinterpret_cast<const float4*>(base + lane * 8);
         const float4* s1 = reinterpret_cast<const float4*>(base + (lane + 64) * 8);
         const float4 a0 = s0[0], a1 = s0[1], b0 = s1[0], b1 = s1[1];
@@ -586,7 +600,7 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G_rt,
   }
 
   if (w.k1 == w.n_keys)
-    append_row<float>(w, a.meta, Hkv, static_cast<const float*>(a.k_new),
+    append_row<float, PAGED>(w, a.meta, Hkv, static_cast<const float*>(a.k_new),
                       static_cast<const float*>(a.v_new),
                       static_cast<float*>(a.kpool),
                       static_cast<float*>(a.vpool), a.pos);
@@ -607,36 +621,35 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, int G_rt,
   }
 }
 
-template <int GT>
+template <int GT, bool PAGED>
 void launch_f32(const dim3& grid, hipStream_t s, const AttnLaunch& a, const Shape& sh,
                 float scale_log2) {
-  hipLaunchKernelGGL((attn_f32_kernel<GT>), grid, dim3(64), 0, s, a, sh.G, sh.Hq, sh.Hkv,
-                     scale_log2);
+  hipLaunchKernelGGL((attn_f32_kernel<GT, PAGED>), grid, dim3(64), 0, s, a, sh.pg, sh.G,
+                     sh.Hq, sh.Hkv, scale_log2);
 }
 
-}  // namespace
-
-hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s) {
+template <bool PAGED>
+hipError_t launch_attention_t(const Shape& sh, const AttnLaunch& a, hipStream_t s) {
   const dim3 grid(a.max_splits, sh.Hkv, a.max_seqs);
   // scores in log2 units: q.k / sqrt(d) * log2(e)
   const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(kHeadDim));
   const dim3 cgrid(sh.Hkv, a.max_seqs);
   if (sh.dtype == 1) {
     if (a.waves == 12)
-      hipLaunchKernelGGL((attn_bf16_kernel<12, 1>), grid, dim3(768), 0, s, a, sh.G, sh.Hq,
-                         sh.Hkv, scale_log2);
+      hipLaunchKernelGGL((attn_bf16_kernel<12, 1, PAGED>), grid, dim3(768), 0, s, a, sh.pg,
+                         sh.G, sh.Hq, sh.Hkv, scale_log2);
     else if (a.waves == 8)
-      hipLaunchKernelGGL((attn_bf16_kernel<8, 1>), grid, dim3(512), 0, s, a, sh.G, sh.Hq,
-                         sh.Hkv, scale_log2);
+      hipLaunchKernelGGL((attn_bf16_kernel<8, 1, PAGED>), grid, dim3(512), 0, s, a, sh.pg,
+                         sh.G, sh.Hq, sh.Hkv, scale_log2);
     else if (a.waves == 4 && a.wide_regs)
-      hipLaunchKernelGGL((attn_bf16_kernel<4, 1>), grid, dim3(256), 0, s, a, sh.G, sh.Hq,
-                         sh.Hkv, scale_log2);
+      hipLaunchKernelGGL((attn_bf16_kernel<4, 1, PAGED>), grid, dim3(256), 0, s, a, sh.pg,
+                         sh.G, sh.Hq, sh.Hkv, scale_log2);
     else if (a.waves == 4)
-      hipLaunchKernelGGL((attn_bf16_kernel<4, 2>), grid, dim3(256), 0, s, a, sh.G, sh.Hq,
-                         sh.Hkv, scale_log2);
+      hipLaunchKernelGGL((attn_bf16_kernel<4, 2, PAGED>), grid, dim3(256), 0, s, a, sh.pg,
+                         sh.G, sh.Hq, sh.Hkv, scale_log2);
     else if (a.waves == 1)
-      hipLaunchKernelGGL((attn_bf16_kernel<1, 2>), grid, dim3(64), 0, s, a, sh.G, sh.Hq,
-                         sh.Hkv, scale_log2);
+      hipLaunchKernelGGL((attn_bf16_kernel<1, 2, PAGED>), grid, dim3(64), 0, s, a, sh.pg,
+                         sh.G, sh.Hq, sh.Hkv, scale_log2);
     else
       return hipErrorInvalidConfiguration;
     if (a.max_splits > 1)
@@ -644,16 +657,22 @@ hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s)
                          sh.Hq, sh.Hkv, true);
   } else {
     switch (sh.G) {
-      case 1: launch_f32<1>(grid, s, a, sh, scale_log2); break;
-      case 2: launch_f32<2>(grid, s, a, sh, scale_log2); break;
-      case 4: launch_f32<4>(grid, s, a, sh, scale_log2); break;
-      case 8: launch_f32<8>(grid, s, a, sh, scale_log2); break;
-      default: launch_f32<0>(grid, s, a, sh, scale_log2); break;
+      case 1: launch_f32<1, PAGED>(grid, s, a, sh, scale_log2); break;
+      case 2: launch_f32<2, PAGED>(grid, s, a, sh, scale_log2); break;
+      case 4: launch_f32<4, PAGED>(grid, s, a, sh, scale_log2); break;
+      case 8: launch_f32<8, PAGED>(grid, s, a, sh, scale_log2); break;
+      default: launch_f32<0, PAGED>(grid, s, a, sh, scale_log2); break;
     }
     hipLaunchKernelGGL(combine_kernel<float>, cgrid, dim3(256), 0, s, a, sh.G,
                        sh.Hq, sh.Hkv, false);
   }
   return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s) {
+  return sh.pg.tables ? launch_attention_t<true>(sh, a, s) : launch_attention_t<false>(sh, a, s);
 }
 
 // Partials of the allocation-free attention entry point.  Every GPU the

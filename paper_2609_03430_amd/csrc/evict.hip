@@ -145,11 +145,12 @@ __device__ __forceinline__ u32x4 funnel8(u32x4 a, u32x4 b, int off) {
 // returned and synchronises, then writes.  Sources are never below destinations and a
 // chunk's writes land below the next chunk's sources, so the move is
 // race-free.  Called by every thread of the workgroup.
-template <int NT, typename E, bool POS_ONLY>
+template <int NT, typename E, bool POS_ONLY, bool PAGED>
 __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, int d0,
-                                             int new_len, int old_len, int64_t region,
+                                             int new_len, int old_len, const RowMap& rm,
                                              E* __restrict__ kpool, E* __restrict__ vpool,
-                                             int32_t* __restrict__ P) {
+                                             int32_t* __restrict__ pos) {
+  auto row = [&](int j) -> int64_t { return pool_row<PAGED>(rm, j); };
   constexpr int kEpu = 16 / sizeof(E);            // elements per 16-byte unit
   constexpr int kKUnitsRow = kHeadDim / kEpu;     // 16-byte units per key row
   constexpr int kVUnitsCh = 8 / kEpu;             // units per (tile, channel)
@@ -167,17 +168,17 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
 
     int pval = 0;
     const bool pos_mine = t < kChunk && j0 + t >= d0 && j0 + t < new_len;
-    if (pos_mine) pval = P[src_of[t]];
+    if (pos_mine) pval = pos[row(src_of[t])];
     u32x4 kbuf[POS_ONLY ? 1 : kKPer];
     E vbuf[POS_ONLY ? 1 : kVPer][kEpu];
     if constexpr (!POS_ONLY) {
 #pragma unroll
       for (int q = 0; q < kKPer; ++q) {
         const int u = t + q * NT;
-        const int row = u / kKUnitsRow, col = u % kKUnitsRow;
-        const int j = j0 + row;
+        const int r = u / kKUnitsRow, col = u % kKUnitsRow;
+        const int j = j0 + r;
         if (u < kKUnits && j >= d0 && j < new_len) {
-          const E* src = kpool + (region + src_of[row]) * kHeadDim + col * kEpu;
+          const E* src = kpool + row(src_of[r]) * kHeadDim + col * kEpu;
           kbuf[q] = load_stream(src);
         }
       }
@@ -195,18 +196,21 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
             // consecutive rows, i.e. one or two adjacent source tiles (the
             // offset is the same for the whole wavefront, so the branch and
             // the switch in funnel8 do not diverge)
-            const E* a = vpool + vt_index(region + (s0 & ~7), ch);
+            const E* a = vpool + vt_index(row(s0 & ~7), ch);
             const u32x4 va = *reinterpret_cast<const u32x4*>(a);
             const int off = s0 & 7;
             u32x4 vb = va;
-            if (off) vb = *reinterpret_cast<const u32x4*>(a + 8 * kHeadDim);
+            // the next tile may lie in another page of the paged layout
+            if (off)
+              vb = *reinterpret_cast<const u32x4*>(
+                  PAGED ? vpool + vt_index(row((s0 & ~7) + 8), ch) : a + 8 * kHeadDim);
             const u32x4 r = funnel8(va, vb, off);
             __builtin_memcpy(vbuf[q], &r, 16);
           } else {
 #pragma unroll
             for (int e = 0; e < kEpu; ++e) {
               const int sj = src_of[jt + e - j0];
-              vbuf[q][e] = sj < old_len ? vpool[vt_index(region + sj, ch)] : zero_e;
+              vbuf[q][e] = sj < old_len ? vpool[vt_index(row(sj), ch)] : zero_e;
             }
           }
         }
@@ -216,15 +220,15 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
 
-    if (pos_mine) P[j0 + t] = pval;
+    if (pos_mine) pos[row(j0 + t)] = pval;
     if constexpr (!POS_ONLY) {
 #pragma unroll
       for (int q = 0; q < kKPer; ++q) {
         const int u = t + q * NT;
-        const int row = u / kKUnitsRow, col = u % kKUnitsRow;
-        const int j = j0 + row;
+        const int r = u / kKUnitsRow, col = u % kKUnitsRow;
+        const int j = j0 + r;
         if (u < kKUnits && j >= d0 && j < new_len) {
-          E* dst = kpool + (region + j) * kHeadDim + col * kEpu;
+          E* dst = kpool + row(j) * kHeadDim + col * kEpu;
           store_stream(dst, kbuf[q]);
         }
       }
@@ -235,7 +239,7 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
         const int rem = u % (kHeadDim * kVUnitsCh);
         const int ch = rem / kVUnitsCh, part = rem % kVUnitsCh;
         if (u < kVUnits && j0 + tile * 8 < new_len) {
-          E* dst = vpool + vt_index(region + j0 + tile * 8, ch) + part * kEpu;
+          E* dst = vpool + vt_index(row(j0 + tile * 8), ch) + part * kEpu;
           u32x4 w;
           __builtin_memcpy(&w, vbuf[q], 16);
           store_stream(dst, w);
@@ -245,11 +249,13 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
   }
 }
 
+// LAYOUT: 0 chronological, 1 hole-fill, 2 chronological in pages.
 template <int NT, int KPT, typename E, bool POS_ONLY, int LAYOUT>
 __global__ __launch_bounds__(NT) void evict_kernel(
     const SeqMeta* __restrict__ meta, E* __restrict__ kpool,
     E* __restrict__ vpool, int32_t* __restrict__ pos, int L, int Hkv, int r,
-    int slot_lo, int policy, int block) {
+    int slot_lo, int policy, int block, Paging pg) {
+  constexpr bool PAGED = LAYOUT == 2;
   static_assert(KPT <= 32, "drop flags live in one 32-bit mask");
   __shared__ SelectShared sel_sh;
   __shared__ int f[kMaxEvery];
@@ -268,12 +274,13 @@ __global__ __launch_bounds__(NT) void evict_kernel(
   if (m <= 0) return;                      // recent ones (positions < thr)
   const int thr = lp + Mref.step - r;
   const int new_len = old_len - m;
-  // slots that can hold candidates: all of them in the chronological layout
+  // slots that can hold candidates: all of them in the chronological layouts
   // are [lp, old_len - r); after hole-fill events the recent rows may sit
   // anywhere above the prompt, so every slot from lp is examined
-  const int span = LAYOUT == 0 ? C : old_len - lp;
-  const int64_t region = Mref.base + static_cast<int64_t>(lg) * Mref.cap;
-  int32_t* P = pos + region;
+  const int span = LAYOUT == 1 ? old_len - lp : C;
+  const RowMap rm = row_map(Mref, slot, lg, pg);
+  const int64_t region = rm.region;
+  int32_t* P = pos + region;     // hole-fill (contiguous) only
   const int t = threadIdx.x;
 
   // 1. scores of this thread's KPT consecutive slots; ties by position
@@ -286,7 +293,7 @@ __global__ __launch_bounds__(NT) void evict_kernel(
     score[i] = 0;
     tie[i] = 0;
     if (c < span) {
-      const int p = P[lp + c];
+      const int p = pos[pool_row<PAGED>(rm, lp + c)];
       if (p < thr) {
         score[i] = policy_key(policy, block, p, lp, event, layer, g, seed, rid);
         tie[i] = static_cast<uint32_t>(p);
@@ -339,7 +346,8 @@ __global__ __launch_bounds__(NT) void evict_kernel(
 
   // 4. order-preserving in-place compaction of positions, keys and values
   __shared__ int src_of[chunk_rows<NT, E>()];
-  compact_rows<NT, E, POS_ONLY>(f, m, src_of, d0, new_len, old_len, region, kpool, vpool, P);
+  compact_rows<NT, E, POS_ONLY, PAGED>(f, m, src_of, d0, new_len, old_len, rm, kpool, vpool,
+                                       pos);
 }
 
 // Compaction of a score-based round: each due head's drop list comes from
@@ -363,9 +371,9 @@ __global__ __launch_bounds__(NT) void compact_drops_kernel(
   const int32_t* d = drops + static_cast<int64_t>(blockIdx.x) * stride;
   for (int k = threadIdx.x; k < m; k += NT) f[k] = d[k] - k;
   __syncthreads();
-  const int64_t region = M.base + static_cast<int64_t>(lg) * M.cap;
-  compact_rows<NT, E, false>(f, m, src_of, f[0], new_len, old_len, region, kpool, vpool,
-                             pos + region);
+  const RowMap rm = row_map(M, slot, lg, Paging{});
+  compact_rows<NT, E, false, false>(f, m, src_of, f[0], new_len, old_len, rm, kpool, vpool,
+                                    pos);
 }
 
 template <int NT, int KPT, bool POS_ONLY, int LAYOUT>
@@ -377,12 +385,12 @@ hipError_t launch_layout(const Shape& sh, const SeqMeta* meta, void* kpool,
     hipLaunchKernelGGL((evict_kernel<NT, KPT, uint16_t, POS_ONLY, LAYOUT>), grid,
                        dim3(NT), 0, s, meta, static_cast<uint16_t*>(kpool),
                        static_cast<uint16_t*>(vpool), pos, sh.L, sh.Hkv, sh.r,
-                       slot_lo, sh.policy, sh.block);
+                       slot_lo, sh.policy, sh.block, sh.pg);
   } else {
     hipLaunchKernelGGL((evict_kernel<NT, KPT, float, POS_ONLY, LAYOUT>), grid,
                        dim3(NT), 0, s, meta, static_cast<float*>(kpool),
                        static_cast<float*>(vpool), pos, sh.L, sh.Hkv, sh.r,
-                       slot_lo, sh.policy, sh.block);
+                       slot_lo, sh.policy, sh.block, sh.pg);
   }
   return hipGetLastError();
 }
@@ -393,6 +401,9 @@ hipError_t launch_kpt(const Shape& sh, const SeqMeta* meta, void* kpool,
                       hipStream_t s) {
   if (sh.layout == 1)
     return launch_layout<NT, KPT, POS_ONLY, 1>(sh, meta, kpool, vpool, pos, slot_lo,
+                                               slot_hi, s);
+  if (sh.layout == 2)
+    return launch_layout<NT, KPT, POS_ONLY, 2>(sh, meta, kpool, vpool, pos, slot_lo,
                                                slot_hi, s);
   return launch_layout<NT, KPT, POS_ONLY, 0>(sh, meta, kpool, vpool, pos, slot_lo,
                                              slot_hi, s);

@@ -7,9 +7,17 @@
 //                                     one channel (the MFMA operand shape of
 //                                     the P.V product)
 //   pos     [pool_rows]               int32 token position of each row
-// A sequence owns L * Hkv consecutive regions of `cap` rows (cap a multiple
-// of 32); region (l, g) starts at row base + (l * Hkv + g) * cap.  Rows
-// [0, len) of a region are cached, in chronological order.
+// Contiguous layouts: a sequence owns L * Hkv consecutive regions of `cap`
+// rows (cap a multiple of 32); region (l, g) starts at row base + (l * Hkv +
+// g) * cap.  Rows [0, len) of a region are cached, in chronological order
+// (or, in the hole-fill layout, in no particular order).
+// Paged layout: the pool is a sequence of page groups of L * Hkv pages of
+// page_rows rows each (page (l, g) of group p starts at row (p * L * Hkv +
+// l * Hkv + g) * page_rows).  A sequence's block table lists its groups in
+// order; row j of its head (l, g) lives in page (l, g) of group table[j /
+// page_rows], at offset j mod page_rows.  Every head of a sequence holds the
+// same number of rows, so one table serves all of them.  Rows stay in
+// chronological order across the pages.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -43,12 +51,50 @@ struct SeqMeta {
 };
 static_assert(sizeof(SeqMeta) == 64, "SeqMeta must stay 64 bytes");
 
+// Block tables of the paged layout (null tables: a contiguous layout).
+struct Paging {
+  const int32_t* tables = nullptr;  // [max_seqs][pages_per_seq] page groups
+  int pages_per_seq = 0;            // table entries per sequence
+  int page_shift = 0;               // log2(page_rows)
+  int64_t group_rows = 0;           // rows of one page group: L * Hkv * page_rows
+};
+
 struct Shape {
   int L, Hq, Hkv, G, r, every, dtype;  // dtype: 0 f32, 1 bf16
-  int layout;                          // 0 chronological, 1 hole-fill
+  int layout;                          // 0 chronological, 1 hole-fill, 2 paged
   int policy;                          // ra_policy
   int block;                           // tokens per block (block policy)
+  Paging pg;                           // the paged layout's tables
 };
+
+// Pool row of row j of one (sequence, layer, KV head) cache.
+struct RowMap {
+  int64_t region;          // contiguous: first pool row of the head's region
+  const int32_t* table;    // paged: the sequence's block table
+  int64_t group_rows;      // paged: rows of one page group
+  int64_t head_off;        // paged: (layer * Hkv + g) * page_rows
+  int page_shift;          // paged: log2(page_rows)
+};
+
+__device__ __host__ inline RowMap row_map(const SeqMeta& M, int slot, int lg, const Paging& pg) {
+  RowMap m;
+  m.region = M.base + static_cast<int64_t>(lg) * M.cap;
+  m.table = pg.tables ? pg.tables + static_cast<int64_t>(slot) * pg.pages_per_seq : nullptr;
+  m.group_rows = pg.group_rows;
+  m.head_off = static_cast<int64_t>(lg) << pg.page_shift;
+  m.page_shift = pg.page_shift;
+  return m;
+}
+
+template <bool PAGED>
+__device__ __forceinline__ int64_t pool_row(const RowMap& m, int j) {
+  if constexpr (PAGED) {
+    const int64_t page = m.table[j >> m.page_shift];
+    return page * m.group_rows + m.head_off + (j & ((1 << m.page_shift) - 1));
+  } else {
+    return m.region + j;
+  }
+}
 
 // ---- launch wrappers (defined in the .hip files) ----------------------------
 
@@ -57,22 +103,32 @@ hipError_t launch_seq_set(SeqMeta* meta, int slot, const SeqMeta& v, hipStream_t
 hipError_t launch_advance(SeqMeta* meta, int slot_lo, int slot_hi, int n_steps,
                           int r, int every, hipStream_t s);
 hipError_t launch_plan_now(SeqMeta* meta, int slot, int r, hipStream_t s);
-hipError_t launch_append_positions(const SeqMeta* meta, int32_t* pos, int slot_lo,
-                                   int slot_hi, int L, int Hkv, int run,
-                                   hipStream_t s);
+hipError_t launch_append_positions(const Shape& sh, const SeqMeta* meta, int32_t* pos,
+                                   int slot_lo, int slot_hi, int run, hipStream_t s);
 hipError_t launch_evict(const Shape& sh, const SeqMeta* meta, void* kpool,
                         void* vpool, int32_t* pos, int slot_lo, int slot_hi,
                         int max_candidates, bool positions_only, hipStream_t s);
-hipError_t launch_write_rows(const Shape& sh, int64_t base, int cap, int len,
+// Rows [0, len) of every head of slot `slot` (host mirror M) from row-major
+// sources [L * Hkv][len][128] (positions: pos_src, or 0..len-1 if null).
+hipError_t launch_write_rows(const Shape& sh, const SeqMeta& M, int slot, int len,
                              const void* k_src, const void* v_src,
                              const int32_t* pos_src, void* kpool, void* vpool,
                              int32_t* pos, hipStream_t s);
-hipError_t launch_read_rows(const Shape& sh, int64_t region_row, int len,
+// Rows [0, len) of head lg = layer * Hkv + g of slot `slot` to row-major outputs.
+hipError_t launch_read_rows(const Shape& sh, const SeqMeta& M, int slot, int lg, int len,
                             const void* kpool, const void* vpool, void* k_out,
                             void* v_out, hipStream_t s);
-hipError_t launch_export_positions(const Shape& sh, int64_t base, int cap,
-                                   int len, const int32_t* pos, int32_t* out,
-                                   hipStream_t s);
+// Positions of rows [0, len) of every head of slot `slot`: [L * Hkv][len].
+hipError_t launch_export_positions(const Shape& sh, const SeqMeta& M, int slot, int len,
+                                   const int32_t* pos, int32_t* out, hipStream_t s);
+
+// Paged layout: table entries set by the host (slot, index, page group).
+struct TableEntry {
+  int32_t slot, index, group;
+};
+constexpr int kTableBatch = 64;   // entries per table-update launch
+hipError_t launch_table_set(const Shape& sh, const TableEntry* entries, int n,
+                            hipStream_t s);
 
 struct AttnLaunch {
   const SeqMeta* meta;

@@ -67,21 +67,26 @@ __global__ void plan_now_kernel(SeqMeta* meta, int slot, int r) {
 }
 
 // Positions lp+step .. lp+step+run-1 into rows len .. len+run-1 of every
-// region of every active slot (rows themselves are not touched).
-__global__ void append_positions_kernel(const SeqMeta* meta, int32_t* pos,
-                                        int lo, int run) {
-  const SeqMeta& M = meta[lo + blockIdx.x];
+// head of every active slot (rows themselves are not touched).
+// Grid: (slots, L * Hkv).
+template <bool PAGED>
+__global__ void append_positions_kernel(const SeqMeta* meta, int32_t* pos, int lo,
+                                        int run, Paging pg) {
+  const int slot = lo + blockIdx.x;
+  const SeqMeta& M = meta[slot];
   if (!M.active) return;
-  const int64_t region = M.base + static_cast<int64_t>(blockIdx.y) * M.cap;
+  const RowMap rm = row_map(M, slot, blockIdx.y, pg);
   for (int i = threadIdx.x; i < run; i += blockDim.x)
-    pos[region + M.len + i] = M.prompt_len + M.step + i;
+    pos[pool_row<PAGED>(rm, M.len + i)] = M.prompt_len + M.step + i;
 }
 
 // Row-major source rows [L*Hkv][len][128] into the cache layout of rows
-// [0, len) of each region; rows of a partly filled last value tile are
-// zeroed.  Grid: (ceil(len/64), L*Hkv).
-template <typename E>
-__global__ void write_rows_kernel(int64_t base, int cap, int len,
+// [0, len) of each head; rows of a partly filled last value tile are
+// zeroed.  Grid: (ceil(len/64), L*Hkv).  A 64-row chunk may straddle two
+// pages of 32 rows, so rows are mapped one by one (value tiles of 8 rows
+// never straddle a page).
+template <typename E, bool PAGED>
+__global__ void write_rows_kernel(SeqMeta M, int slot, int len, Paging pg,
                                   const E* __restrict__ k_src,
                                   const E* __restrict__ v_src,
                                   const int32_t* __restrict__ pos_src,
@@ -90,12 +95,12 @@ __global__ void write_rows_kernel(int64_t base, int cap, int len,
   constexpr int kEpu = 16 / sizeof(E);
   const int lg = blockIdx.y;
   const int j0 = blockIdx.x * 64;
-  const int64_t region = base + static_cast<int64_t>(lg) * cap;
+  const RowMap rm = row_map(M, slot, lg, pg);
   const int64_t src0 = static_cast<int64_t>(lg) * len;
   if (pos) {
     for (int i = threadIdx.x; i < 64; i += blockDim.x) {
       const int j = j0 + i;
-      if (j < len) pos[region + j] = pos_src ? pos_src[src0 + j] : j;
+      if (j < len) pos[pool_row<PAGED>(rm, j)] = pos_src ? pos_src[src0 + j] : j;
     }
   }
   if (!k_src) return;
@@ -103,7 +108,7 @@ __global__ void write_rows_kernel(int64_t base, int cap, int len,
   for (int u = threadIdx.x; u < 64 * kUnitsRow; u += blockDim.x) {
     const int j = j0 + u / kUnitsRow, col = u % kUnitsRow;
     if (j < len)
-      *reinterpret_cast<u32x4*>(kpool + (region + j) * kHeadDim + col * kEpu) =
+      *reinterpret_cast<u32x4*>(kpool + pool_row<PAGED>(rm, j) * kHeadDim + col * kEpu) =
           *reinterpret_cast<const u32x4*>(k_src + (src0 + j) * kHeadDim + col * kEpu);
   }
   // values: each output 16-byte unit holds kEpu consecutive rows of one channel
@@ -122,21 +127,23 @@ __global__ void write_rows_kernel(int64_t base, int cap, int len,
     }
     u32x4 w;
     __builtin_memcpy(&w, e, 16);
-    *reinterpret_cast<u32x4*>(vpool + (region + jt) * kHeadDim + ch * 8 + part * kEpu) = w;
+    *reinterpret_cast<u32x4*>(vpool + pool_row<PAGED>(rm, jt) * kHeadDim + ch * 8 +
+                              part * kEpu) = w;
   }
 }
 
-// Rows [0, len) of one region to row-major outputs.  Grid: ceil(len/64).
-template <typename E>
-__global__ void read_rows_kernel(int64_t region, int len,
+// Rows [0, len) of one head to row-major outputs.  Grid: ceil(len/64).
+template <typename E, bool PAGED>
+__global__ void read_rows_kernel(SeqMeta M, int slot, int lg, int len, Paging pg,
                                  const E* __restrict__ kpool,
                                  const E* __restrict__ vpool,
                                  E* __restrict__ k_out, E* __restrict__ v_out) {
+  const RowMap rm = row_map(M, slot, lg, pg);
   const int j0 = blockIdx.x * 64;
   for (int u = threadIdx.x; u < 64 * kHeadDim; u += blockDim.x) {
     const int j = j0 + u / kHeadDim, ch = u % kHeadDim;
     if (j >= len) continue;
-    const int64_t row = region + j;
+    const int64_t row = pool_row<PAGED>(rm, j);
     if (k_out) k_out[static_cast<int64_t>(j) * kHeadDim + ch] = kpool[row * kHeadDim + ch];
     if (v_out)
       v_out[static_cast<int64_t>(j) * kHeadDim + ch] =
@@ -144,13 +151,25 @@ __global__ void read_rows_kernel(int64_t region, int len,
   }
 }
 
-__global__ void export_positions_kernel(int64_t base, int cap, int len,
+template <bool PAGED>
+__global__ void export_positions_kernel(SeqMeta M, int slot, int len, Paging pg,
                                         const int32_t* __restrict__ pos,
                                         int32_t* __restrict__ out) {
   const int lg = blockIdx.y;
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
-  if (j < len)
-    out[static_cast<int64_t>(lg) * len + j] = pos[base + static_cast<int64_t>(lg) * cap + j];
+  const RowMap rm = row_map(M, slot, lg, pg);
+  if (j < len) out[static_cast<int64_t>(lg) * len + j] = pos[pool_row<PAGED>(rm, j)];
+}
+
+struct TableBatch {
+  TableEntry e[kTableBatch];
+};
+
+// Block-table entries chosen by the host's page allocator.
+__global__ void table_set_kernel(int32_t* tables, int pages_per_seq, TableBatch b, int n) {
+  const int i = threadIdx.x;
+  if (i < n)
+    tables[static_cast<int64_t>(b.e[i].slot) * pages_per_seq + b.e[i].index] = b.e[i].group;
 }
 
 }  // namespace
@@ -189,61 +208,99 @@ hipError_t launch_plan_range(SeqMeta* meta, int slot_lo, int slot_hi, int r, hip
   return hipGetLastError();
 }
 
-hipError_t launch_append_positions(const SeqMeta* meta, int32_t* pos, int slot_lo,
-                                   int slot_hi, int L, int Hkv, int run,
-                                   hipStream_t s) {
+hipError_t launch_append_positions(const Shape& sh, const SeqMeta* meta, int32_t* pos,
+                                   int slot_lo, int slot_hi, int run, hipStream_t s) {
   if (slot_hi <= slot_lo || run <= 0) return hipSuccess;
-  hipLaunchKernelGGL(append_positions_kernel, dim3(slot_hi - slot_lo, L * Hkv),
-                     dim3(256), 0, s, meta, pos, slot_lo, run);
+  const dim3 grid(slot_hi - slot_lo, sh.L * sh.Hkv);
+  if (sh.pg.tables)
+    hipLaunchKernelGGL(append_positions_kernel<true>, grid, dim3(256), 0, s, meta, pos,
+                       slot_lo, run, sh.pg);
+  else
+    hipLaunchKernelGGL(append_positions_kernel<false>, grid, dim3(256), 0, s, meta, pos,
+                       slot_lo, run, sh.pg);
   return hipGetLastError();
 }
 
-hipError_t launch_write_rows(const Shape& sh, int64_t base, int cap, int len,
+template <typename E>
+void write_rows_t(const Shape& sh, const SeqMeta& M, int slot, int len, const void* k_src,
+                  const void* v_src, const int32_t* pos_src, void* kpool, void* vpool,
+                  int32_t* pos, hipStream_t s) {
+  const dim3 grid((len + 63) / 64, sh.L * sh.Hkv);
+  const E* k = static_cast<const E*>(k_src);
+  const E* v = static_cast<const E*>(v_src);
+  if (sh.pg.tables)
+    hipLaunchKernelGGL((write_rows_kernel<E, true>), grid, dim3(256), 0, s, M, slot, len,
+                       sh.pg, k, v, pos_src, static_cast<E*>(kpool), static_cast<E*>(vpool),
+                       pos);
+  else
+    hipLaunchKernelGGL((write_rows_kernel<E, false>), grid, dim3(256), 0, s, M, slot, len,
+                       sh.pg, k, v, pos_src, static_cast<E*>(kpool), static_cast<E*>(vpool),
+                       pos);
+}
+
+hipError_t launch_write_rows(const Shape& sh, const SeqMeta& M, int slot, int len,
                              const void* k_src, const void* v_src,
                              const int32_t* pos_src, void* kpool, void* vpool,
                              int32_t* pos, hipStream_t s) {
   if (len <= 0) return hipSuccess;
-  const dim3 grid((len + 63) / 64, sh.L * sh.Hkv);
-  if (sh.dtype == 1) {
-    hipLaunchKernelGGL(write_rows_kernel<uint16_t>, grid, dim3(256), 0, s, base,
-                       cap, len, static_cast<const uint16_t*>(k_src),
-                       static_cast<const uint16_t*>(v_src), pos_src,
-                       static_cast<uint16_t*>(kpool), static_cast<uint16_t*>(vpool), pos);
-  } else {
-    hipLaunchKernelGGL(write_rows_kernel<float>, grid, dim3(256), 0, s, base, cap,
-                       len, static_cast<const float*>(k_src),
-                       static_cast<const float*>(v_src), pos_src,
-                       static_cast<float*>(kpool), static_cast<float*>(vpool), pos);
-  }
+  if (sh.dtype == 1)
+    write_rows_t<uint16_t>(sh, M, slot, len, k_src, v_src, pos_src, kpool, vpool, pos, s);
+  else
+    write_rows_t<float>(sh, M, slot, len, k_src, v_src, pos_src, kpool, vpool, pos, s);
   return hipGetLastError();
 }
 
-hipError_t launch_read_rows(const Shape& sh, int64_t region_row, int len,
+template <typename E>
+void read_rows_t(const Shape& sh, const SeqMeta& M, int slot, int lg, int len,
+                 const void* kpool, const void* vpool, void* k_out, void* v_out,
+                 hipStream_t s) {
+  const dim3 grid((len + 63) / 64);
+  const E* k = static_cast<const E*>(kpool);
+  const E* v = static_cast<const E*>(vpool);
+  if (sh.pg.tables)
+    hipLaunchKernelGGL((read_rows_kernel<E, true>), grid, dim3(256), 0, s, M, slot, lg, len,
+                       sh.pg, k, v, static_cast<E*>(k_out), static_cast<E*>(v_out));
+  else
+    hipLaunchKernelGGL((read_rows_kernel<E, false>), grid, dim3(256), 0, s, M, slot, lg, len,
+                       sh.pg, k, v, static_cast<E*>(k_out), static_cast<E*>(v_out));
+}
+
+hipError_t launch_read_rows(const Shape& sh, const SeqMeta& M, int slot, int lg, int len,
                             const void* kpool, const void* vpool, void* k_out,
                             void* v_out, hipStream_t s) {
   if (len <= 0) return hipSuccess;
-  const dim3 grid((len + 63) / 64);
-  if (sh.dtype == 1) {
-    hipLaunchKernelGGL(read_rows_kernel<uint16_t>, grid, dim3(256), 0, s,
-                       region_row, len, static_cast<const uint16_t*>(kpool),
-                       static_cast<const uint16_t*>(vpool),
-                       static_cast<uint16_t*>(k_out), static_cast<uint16_t*>(v_out));
-  } else {
-    hipLaunchKernelGGL(read_rows_kernel<float>, grid, dim3(256), 0, s, region_row,
-                       len, static_cast<const float*>(kpool),
-                       static_cast<const float*>(vpool), static_cast<float*>(k_out),
-                       static_cast<float*>(v_out));
-  }
+  if (sh.dtype == 1)
+    read_rows_t<uint16_t>(sh, M, slot, lg, len, kpool, vpool, k_out, v_out, s);
+  else
+    read_rows_t<float>(sh, M, slot, lg, len, kpool, vpool, k_out, v_out, s);
   return hipGetLastError();
 }
 
-hipError_t launch_export_positions(const Shape& sh, int64_t base, int cap,
-                                   int len, const int32_t* pos, int32_t* out,
-                                   hipStream_t s) {
+hipError_t launch_export_positions(const Shape& sh, const SeqMeta& M, int slot, int len,
+                                   const int32_t* pos, int32_t* out, hipStream_t s) {
   if (len <= 0) return hipSuccess;
-  hipLaunchKernelGGL(export_positions_kernel, dim3((len + 255) / 256, sh.L * sh.Hkv),
-                     dim3(256), 0, s, base, cap, len, pos, out);
+  const dim3 grid((len + 255) / 256, sh.L * sh.Hkv);
+  if (sh.pg.tables)
+    hipLaunchKernelGGL(export_positions_kernel<true>, grid, dim3(256), 0, s, M, slot, len,
+                       sh.pg, pos, out);
+  else
+    hipLaunchKernelGGL(export_positions_kernel<false>, grid, dim3(256), 0, s, M, slot, len,
+                       sh.pg, pos, out);
   return hipGetLastError();
+}
+
+hipError_t launch_table_set(const Shape& sh, const TableEntry* entries, int n,
+                            hipStream_t s) {
+  for (int i0 = 0; i0 < n; i0 += kTableBatch) {
+    TableBatch b{};
+    const int k = std::min(kTableBatch, n - i0);
+    for (int i = 0; i < k; ++i) b.e[i] = entries[i0 + i];
+    hipLaunchKernelGGL(table_set_kernel, dim3(1), dim3(kTableBatch), 0, s,
+                       const_cast<int32_t*>(sh.pg.tables), sh.pg.pages_per_seq, b, k);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace ra

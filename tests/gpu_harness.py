@@ -32,7 +32,7 @@ class Run:
                  scaled=True, wl_seed=1000, ring=None, attn_split=0,
                  max_seqs=None, write_prompt=True, begin=True,
                  layout=B.RA_LAYOUT_CHRONOLOGICAL, policy=B.RA_POLICY_RANDOM,
-                 block=1, pool_rows=None):
+                 block=1, pool_rows=None, page_rows=32, max_prompt_len=None):
         self.L, self.Hq, self.Hkv, self.K, self.r, self.every = L, Hq, Hkv, K, r, every
         self.G = Hq // Hkv
         self.lps = list(lps)
@@ -47,7 +47,9 @@ class Run:
         self.policy, self.block = policy, block
         self.cfg = B.make_config(L, Hq, Hkv, K, r, every, mode, dtype, self.max_seqs,
                                  attn_split=attn_split, layout=layout, policy=policy,
-                                 policy_block=block)
+                                 policy_block=block, page_rows=page_rows,
+                                 max_prompt_len=(max(self.lps, default=0)
+                                                 if max_prompt_len is None else max_prompt_len))
         rows = pool_rows or sum(B.ra_seq_rows(self.cfg, lp) for lp in self.lps)
         self.cache = B.Cache(self.cfg, rows)
         self.h = self.cache.handle

@@ -34,8 +34,13 @@ def test_config_validation():
     bad = [
         dict(num_q_heads=41), dict(num_layers=0), dict(budget_k=-1),
         dict(recent_r=-1), dict(evict_every=0), dict(max_seqs=0),
-        dict(attn_split=33), dict(budget_mode=7), dict(dtype=9), dict(layout=2),
+        dict(attn_split=33), dict(budget_mode=7), dict(dtype=9), dict(layout=3),
         dict(policy=5), dict(policy=-1), dict(policy=2, policy_block=0),
+        # paged layout: pages a power of two in [32, 1024], a prompt bound >= 0
+        # that a TOTAL budget can hold
+        dict(layout=2, page_rows=48), dict(layout=2, page_rows=16),
+        dict(layout=2, page_rows=2048), dict(layout=2, max_prompt_len=-1),
+        dict(layout=2, budget_mode=1, max_prompt_len=8193),
     ]
     for kw in bad:
         c = B.make_config(40, 40, 8, 8192, max_seqs=32)
@@ -68,6 +73,26 @@ def test_region_sizes():
     assert B.ra_workspace_bytes(c) >= 32 * 8 * 64 * 5 * 130 * 4
 
 
+def test_paged_sizes():
+    """Paged layout: a head's most rows round up to whole pages; the metadata
+    buffer holds a block table of ceil((max prompt + K + r + R) / page_rows)
+    entries per slot; a prompt longer than the bound is refused."""
+    c = B.make_config(40, 40, 8, 8192, max_seqs=32, layout=B.RA_LAYOUT_PAGED,
+                      page_rows=64, max_prompt_len=2048)
+    assert B.ra_config_check(c) == B.RA_OK
+    assert B.ra_region_rows(c, 1024) == 9344            # 1024 + 8192 + 128, 146 pages
+    assert B.ra_region_rows(c, 1000) == 9344            # 9320 rounded up to a page
+    assert B.ra_seq_rows(c, 1000) == 40 * 8 * 9344      # whole page groups
+    assert B.ra_region_rows(c, 2049) == B.RA_ERR_CAPACITY
+    pages = -(-(2048 + 8192 + 64 + 64) // 64)
+    records = -(-(64 * 32) // 256) * 256
+    assert B.ra_meta_bytes(c) == records + -(-(4 * 32 * pages) // 256) * 256
+    t = B.make_config(2, 4, 2, 300, budget_mode=B.RA_BUDGET_TOTAL, max_seqs=3,
+                      layout=B.RA_LAYOUT_PAGED, page_rows=32, max_prompt_len=300)
+    assert B.ra_region_rows(t, 100) == 448              # 300 + 64 + 64 = 428 -> 14 pages
+    assert B.ra_region_rows(t, 301) == B.RA_ERR_BUDGET
+
+
 def test_create_rejects_null_buffers_without_gpu():
     c = B.make_config(2, 4, 2, 64, max_seqs=2)
     out = ctypes.c_void_p()
@@ -83,6 +108,13 @@ def test_create_rejects_null_buffers_without_gpu():
     # pool rows must be a multiple of 32
     st = lib.ra_cache_create(ctypes.byref(c), ctypes.c_void_p(16), ctypes.c_void_p(16),
                              ctypes.c_void_p(16), 1000, ctypes.c_void_p(16), 4096,
+                             None, ctypes.byref(out))
+    assert st == B.RA_ERR_INVALID_ARG
+    # paged: of a whole number of page groups (L * Hkv * page_rows = 256 rows)
+    p = B.make_config(2, 4, 2, 64, max_seqs=2, layout=B.RA_LAYOUT_PAGED, page_rows=64,
+                      max_prompt_len=16)
+    st = lib.ra_cache_create(ctypes.byref(p), ctypes.c_void_p(16), ctypes.c_void_p(16),
+                             ctypes.c_void_p(16), 1024 + 32, ctypes.c_void_p(16), 4096,
                              None, ctypes.byref(out))
     assert st == B.RA_ERR_INVALID_ARG
 

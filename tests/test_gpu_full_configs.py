@@ -34,14 +34,14 @@ WINDOW = 72          # steps decoded on the GPU (events at 32704 and 32768)
 
 
 @pytest.mark.parametrize("name,layout", [(n, 0) for n in sorted(SHAPES)] +
-                         [("qwen3-14b", 1)])
+                         [("qwen3-14b", 1), ("qwen3-14b", 2)])
 def test_full_size(name, layout):
     L, Hq, Hkv, Bsz, lp, K, seed = SHAPES[name]
     log("full size %s layout %d: L=%d Hq=%d Hkv=%d B=%d lp=%d K=%d"
         % (name, layout, L, Hq, Hkv, Bsz, lp, K))
     run = Run(L=L, Hq=Hq, Hkv=Hkv, K=K, lps=[lp] * Bsz, r=64, every=64,
               seeds=[seed * 1000003 + b for b in range(Bsz)], rids=list(range(Bsz)),
-              wl_seed=seed, write_prompt=False, layout=layout)
+              wl_seed=seed, write_prompt=False, layout=layout, page_rows=64)
     t0 = T - WINDOW
     run.fast_forward(t0)
     for b in range(Bsz):
@@ -72,7 +72,8 @@ def test_full_size(name, layout):
         for o in oracles.values():
             o.rep.end_step()
     for b, l, g in sites:
-        got = run.sorted_positions(b, l, g) if layout else run.positions(b, l, g)
+        got = (run.sorted_positions(b, l, g) if layout == B.RA_LAYOUT_HOLE_FILL
+               else run.positions(b, l, g))
         want = oracles[b].rep.P[(l, g)]
         assert np.array_equal(got, want), (name, b, l, g)
     assert oracles[0].rep.event >= 2

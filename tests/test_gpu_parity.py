@@ -16,7 +16,7 @@ from paper_2609_03430_amd import binding as B
 
 pytestmark = pytest.mark.gpu
 
-@pytest.mark.parametrize("layout", [B.RA_LAYOUT_CHRONOLOGICAL, B.RA_LAYOUT_HOLE_FILL])
+@pytest.mark.parametrize("layout", [B.RA_LAYOUT_CHRONOLOGICAL, B.RA_LAYOUT_HOLE_FILL, B.RA_LAYOUT_PAGED])
 @pytest.mark.parametrize("dtype", [B.RA_BF16, B.RA_F32])
 def test_small_decode_parity(dtype, layout):
     """Three sequences (prompts 5, 0, 17), r=8, every=8, K=40, 150 steps:
@@ -55,6 +55,10 @@ def test_small_decode_parity(dtype, layout):
     (3, 50, 40, 8, B.RA_BUDGET_EVICTABLE, 1),        # r > every: recent rows move
     (0, 64, 0, 1, B.RA_BUDGET_EVICTABLE, 1),
     (129, 8192, 64, 64, B.RA_BUDGET_EVICTABLE, 1),
+    (37, 100, 16, 16, B.RA_BUDGET_EVICTABLE, 2),
+    (0, 64, 0, 1, B.RA_BUDGET_EVICTABLE, 2),
+    (300, 300, 64, 64, B.RA_BUDGET_TOTAL, 2),
+    (129, 8192, 64, 64, B.RA_BUDGET_EVICTABLE, 2),
 ])
 def test_fast_forward_and_evict_now(lp, K, r, every, mode, layout):
     """Positions-only fast forward and explicit events at arbitrary steps
@@ -90,7 +94,7 @@ POLICIES = [(B.RA_POLICY_SHARED, 1), (B.RA_POLICY_BLOCK, 4), (B.RA_POLICY_BLOCK,
             (B.RA_POLICY_RECENCY, 1)]
 
 
-@pytest.mark.parametrize("layout", [B.RA_LAYOUT_CHRONOLOGICAL, B.RA_LAYOUT_HOLE_FILL])
+@pytest.mark.parametrize("layout", [B.RA_LAYOUT_CHRONOLOGICAL, B.RA_LAYOUT_HOLE_FILL, B.RA_LAYOUT_PAGED])
 @pytest.mark.parametrize("policy,block", POLICIES)
 def test_policy_decode_parity(policy, block, layout):
     """The diagnostic policies (shared draw, block-wise, recency + prompt):
@@ -117,7 +121,7 @@ def test_policy_decode_parity(policy, block, layout):
     run.close()
 
 
-@pytest.mark.parametrize("layout", [B.RA_LAYOUT_CHRONOLOGICAL, B.RA_LAYOUT_HOLE_FILL])
+@pytest.mark.parametrize("layout", [B.RA_LAYOUT_CHRONOLOGICAL, B.RA_LAYOUT_HOLE_FILL, B.RA_LAYOUT_PAGED])
 @pytest.mark.parametrize("policy,block", POLICIES + [(B.RA_POLICY_BLOCK, 16)])
 def test_policy_large_select(policy, block, layout):
     """8256 candidates per head (the 1024-thread select): kept sets after a
@@ -150,6 +154,7 @@ def test_policy_large_select(policy, block, layout):
     (20000, B.RA_LAYOUT_HOLE_FILL),
     (32704, B.RA_LAYOUT_CHRONOLOGICAL),   # K + every = 32768 candidates, the largest
     (32640, B.RA_LAYOUT_HOLE_FILL),       # K + every + r = 32768
+    (32704, B.RA_LAYOUT_PAGED),
 ])
 def test_largest_select(K, layout):
     """More than 16,384 candidates per head (the 1024-thread select with 32
@@ -183,7 +188,8 @@ def test_largest_select(K, layout):
 @pytest.mark.parametrize("C,layout", [
     (c, B.RA_LAYOUT_CHRONOLOGICAL) for c in
     (1024, 1025, 2048, 2049, 3072, 3073, 5120, 5121, 9216, 9217, 16384, 16385)
-] + [(3073, B.RA_LAYOUT_HOLE_FILL), (16385, B.RA_LAYOUT_HOLE_FILL)])
+] + [(3073, B.RA_LAYOUT_HOLE_FILL), (16385, B.RA_LAYOUT_HOLE_FILL),
+      (5121, B.RA_LAYOUT_PAGED), (16385, B.RA_LAYOUT_PAGED)])
 def test_select_size_boundaries(C, layout):
     """An explicit event with exactly C candidates per head, on and just past
     each boundary of the selection's scores-per-thread builds (1,024 threads

@@ -125,6 +125,34 @@ def test_fast_forward_refuses_to_outgrow_a_region_before_any_launch():
     cache.close()
 
 
+def test_paged_rows_are_bounded_by_the_block_table():
+    """Paged layout, external policy: rows pile up to the block table's size
+    (ceil((max prompt + K + r + R) / page_rows) pages = 2 pages of 32 rows
+    here), however many free pages the pool has.  A fast forward or a decode
+    step that would go past it is refused before any launch."""
+    log("paged table bound")
+    cfg = B.make_config(1, 2, 1, 16, 8, 8, B.RA_BUDGET_EVICTABLE, B.RA_BF16, 1,
+                        policy=B.RA_POLICY_EXTERNAL, layout=B.RA_LAYOUT_PAGED,
+                        page_rows=32, max_prompt_len=4)
+    cache = B.Cache(cfg, 8 * 32)                   # 8 page groups
+    h = cache.handle
+    B.ra_seq_begin(h, 0, 4, 1, 0)
+    before = _infos_of(h, 1)
+    assert _status(B.ra_fast_forward, h, 61) == B.RA_ERR_CAPACITY
+    assert _infos_of(h, 1) == before
+    B.ra_fast_forward(h, 60)                       # 64 rows: both pages full
+    info = B.ra_get_seq_info(h, 0)
+    assert (info.len, info.cap) == (64, 64)
+    assert list(B.ra_read_positions(h, 0, 0, 0, 64)) == list(range(64))
+    q = torch.zeros(1, 2, 128, dtype=torch.bfloat16, device="cuda")
+    kv = torch.zeros(1, 1, 128, dtype=torch.bfloat16, device="cuda")
+    out = torch.zeros_like(q)
+    assert _status(B.ra_decode_attention, h, 0, q, kv, kv, out, cache.workspace) == \
+        B.RA_ERR_CAPACITY
+    assert _infos_of(h, 1) == [(1, 64, 60, 0)]
+    cache.close()
+
+
 def _infos_of(h, n):
     return [(i.active, i.len, i.step, i.event) for i in
             (B.ra_get_seq_info(h, s) for s in range(n))]

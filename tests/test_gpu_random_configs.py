@@ -46,15 +46,13 @@ def draw_config(case):
     return c
 
 
-@pytest.mark.parametrize("case", range(N_CASES))
-def test_random_config_parity(case):
-    c = draw_config(case)
-    log("random config %d: %s" % (case, c))
+def _run_config(case, c, page_rows=32):
     run = Run(L=c["L"], Hq=c["Hkv"] * c["G"], Hkv=c["Hkv"], K=c["K"], lps=c["lps"],
               r=c["r"], every=c["every"], dtype=c["dtype"], mode=c["mode"],
               layout=c["layout"], policy=c["policy"], block=c["block"],
               seeds=[case * 7919 + s for s in range(len(c["lps"]))],
-              rids=[case * 31 + s for s in range(len(c["lps"]))], wl_seed=500 + case)
+              rids=[case * 31 + s for s in range(len(c["lps"]))], wl_seed=500 + case,
+              page_rows=page_rows)
     oracles = [OracleSeq(run, s) for s in range(run.n)]
     worst, events = 0.0, 0
     for t in range(c["T"]):
@@ -63,7 +61,8 @@ def test_random_config_parity(case):
         for o in oracles:
             o.rep.append()
             for layer in range(run.L):
-                err = attn_err(outs[layer, o.slot], o.attend(layer, t), c["dtype"], (case, t, o.slot, layer,))
+                err = attn_err(outs[layer, o.slot], o.attend(layer, t), c["dtype"],
+                               (case, t, o.slot, layer))
                 worst = max(worst, err)
             o.rep.end_step()
         if ev:
@@ -73,3 +72,21 @@ def test_random_config_parity(case):
     log("  steps=%d events=%d worst=%.3g" % (c["T"], events, worst))
     assert events >= 1
     run.close()
+
+
+@pytest.mark.parametrize("case", range(N_CASES))
+def test_random_config_parity(case):
+    c = draw_config(case)
+    log("random config %d: %s" % (case, c))
+    _run_config(case, c)
+
+
+@pytest.mark.parametrize("case", range(6))
+def test_random_config_parity_paged(case):
+    """The same drawn configurations in the paged layout, with pages of 32,
+    64 or 128 rows."""
+    c = draw_config(case)
+    c["layout"] = B.RA_LAYOUT_PAGED
+    page_rows = (32, 64, 128)[case % 3]
+    log("random config %d paged (%d-row pages): %s" % (case, page_rows, c))
+    _run_config(case, c, page_rows)

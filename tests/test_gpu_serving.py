@@ -26,7 +26,7 @@ def _check_sets(run, o):
         assert np.array_equal(got, o.rep.P[(layer, g)]), (o.slot, o.rid, layer, g, o.rep.step)
 
 
-@pytest.mark.parametrize("layout", [B.RA_LAYOUT_CHRONOLOGICAL, B.RA_LAYOUT_HOLE_FILL])
+@pytest.mark.parametrize("layout", [B.RA_LAYOUT_CHRONOLOGICAL, B.RA_LAYOUT_HOLE_FILL, B.RA_LAYOUT_PAGED])
 def test_requests_finish_and_are_replaced(layout):
     log("serving churn layout=%d" % layout)
     rng = np.random.default_rng(31)
@@ -35,10 +35,12 @@ def test_requests_finish_and_are_replaced(layout):
     reqs = [dict(lp=int(rng.integers(0, 60)), gen=int(rng.integers(40, 220)),
                  seed=1000 + i, rid=500 + i) for i in range(n_req)]
     # room for every slot at the largest prompt, and no more
-    probe = B.make_config(2, 4, 2, K, r, every, B.RA_BUDGET_EVICTABLE, B.RA_BF16, slots)
+    probe = B.make_config(2, 4, 2, K, r, every, B.RA_BUDGET_EVICTABLE, B.RA_BF16, slots,
+                          layout=layout, page_rows=32, max_prompt_len=60)
     pool = slots * B.ra_seq_rows(probe, 60)
     run = Run(L=2, Hq=4, Hkv=2, K=K, lps=[0] * slots, r=r, every=every, begin=False,
-              max_seqs=slots, pool_rows=pool, layout=layout)
+              max_seqs=slots, pool_rows=pool, layout=layout, page_rows=32,
+              max_prompt_len=60)
     queue = list(range(n_req))
     live, oracles, done = {}, {}, []
 
@@ -78,13 +80,15 @@ def test_requests_finish_and_are_replaced(layout):
                 if queue:
                     admit(s)
     assert sorted(done) == list(range(n_req))
-    # every row was returned and merged: one sequence of the whole pool fits
-    big = pool // (run.L * run.Hkv) - (K + r + every)
-    big = big - big % 32 - 32
-    assert B.ra_seq_rows(run.cfg, big) <= pool
-    run.lps[0] = big
-    run.begin(0)
-    assert B.ra_get_seq_info(run.h, 0).base == 0
+    assert B.ra_pool_info(run.h) == (0, pool)      # every row was returned
+    if layout != B.RA_LAYOUT_PAGED:
+        # and the free list merged it: one sequence of the whole pool fits
+        big = pool // (run.L * run.Hkv) - (K + r + every)
+        big = big - big % 32 - 32
+        assert B.ra_seq_rows(run.cfg, big) <= pool
+        run.lps[0] = big
+        run.begin(0)
+        assert B.ra_get_seq_info(run.h, 0).base == 0
     log("  %d requests over %d steps, worst %.3g" % (n_req, steps, worst))
     run.close()
 
