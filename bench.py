@@ -99,7 +99,8 @@ def run_signature(args):
     return {"workload": args.workload, "steps": args.steps, "warmup": args.warmup,
             "layout": args.layout, "policy": args.policy,
             "block": args.block if args.policy == "block" else None,
-            "attn_split": args.attn_split}
+            "attn_split": args.attn_split,
+            "page_rows": args.page_rows if args.layout == "paged" else None}
 
 
 def read_traffic(signature):
@@ -527,6 +528,188 @@ def serving(B, torch, Workload, steps, log):
     return res
 
 
+def serving_cap(B, torch, Workload, steps, log, layout_name, page_rows=64,
+                watermark=0.02):
+    """Serving at a fixed memory cap: contiguous regions against pages.
+
+    Phi-4-reasoning attention shape (40 layers, 40 Q / 10 KV heads), K = 2048,
+    r = 64, every 64, prompts ~U[64, 2048], 8192-token generations, up to 256
+    slots, and one pool for both layouts: the rows 128 sequences with the
+    longest prompt take in contiguous regions.  Requests come from a queue.
+    Contiguous regions are sized by each request's own prompt and placed by
+    first fit; a request is admitted while a region fits.  Pages are taken as
+    rows are appended; a request is admitted while the free rows, less a
+    watermark (2% of the pool), cover its prompt; a step whose new rows find
+    no free page preempts the youngest request (its progress is lost and it
+    returns to the head of the queue).  The pool starts filled by requests of
+    staggered ages, reached through the real sampler.  Rows are not
+    materialised and admitted prompts are positions only: the timing does not
+    depend on the values, and the rows left in the pool are synthetic data
+    either way.  Timed: every step's launches, end-of-step evictions,
+    preemptions and admissions, wall clock.
+    """
+    import collections
+    import numpy as np
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    L, Hq, Hkv, K, GEN, SLOTS = 40, 40, 10, 2048, 8192, 256
+    layout = {"chronological": B.RA_LAYOUT_CHRONOLOGICAL, "paged": B.RA_LAYOUT_PAGED}[layout_name]
+    ref = B.make_config(L, Hq, Hkv, K, R, EVERY, B.RA_BUDGET_EVICTABLE, B.RA_BF16, 128)
+    pool = 128 * B.ra_seq_rows(ref, 2048)
+    cfg = B.make_config(L, Hq, Hkv, K, R, EVERY, B.RA_BUDGET_EVICTABLE, B.RA_BF16, SLOTS,
+                        layout=layout, page_rows=page_rows, max_prompt_len=2048)
+    if layout == B.RA_LAYOUT_PAGED:
+        pool -= pool % (L * Hkv * page_rows)
+    cache = B.Cache(cfg, pool, device=dev)
+    h = cache.handle
+    rng = np.random.default_rng(1006)
+    n_req = 1 << 14
+    lps = rng.integers(64, 2049, n_req).tolist()
+    queue = collections.deque(range(n_req))
+    res = {}                           # slot -> [rid, step]
+    group = L * Hkv * page_rows
+
+    def rows_held(lp, age):
+        # cached rows after `age` steps: growth until the first event (the
+        # first multiple of 64 with more than K evictable rows), then K + r
+        # plus the steps since the last event
+        first = EVERY * ((K + R) // EVERY + 1)
+        n = lp + age if age < first else lp + K + R + age % EVERY
+        if layout == B.RA_LAYOUT_PAGED:
+            return group * -(-n // page_rows)
+        return B.ra_seq_rows(cfg, lp)
+
+    def ages_for(n):
+        return [int(GEN * (n - i - 0.5) / n) for i in range(n)]   # oldest first
+
+    # the starting population: the most requests of uniformly spread ages
+    # that fit the cap (less the watermark for pages)
+    room = pool * (1 - watermark) if layout == B.RA_LAYOUT_PAGED else pool
+    n_start = 1
+    while n_start < SLOTS and sum(rows_held(lps[i], a) for i, a in
+                                  enumerate(ages_for(n_start + 1))) <= room:
+        n_start += 1
+    ages = ages_for(n_start)
+
+    def begin(slot, rid):
+        try:
+            B.ra_seq_begin(h, slot, lps[rid], 7 * rid + 1, rid, None, None, stream)
+        except B.RandAttnError as e:
+            if e.status != B.RA_ERR_CAPACITY:
+                raise
+            return False
+        res[slot] = [rid, 0]
+        return True
+
+    # begun oldest first, with a fast forward between begins
+    t0 = time.time()
+    for i in range(n_start):
+        if not begin(i, queue[0]):
+            break
+        queue.popleft()
+        run = ages[i] - (ages[i + 1] if i + 1 < n_start else 0)
+        try:
+            B.ra_fast_forward(h, run, stream)
+        except B.RandAttnError as e:
+            if e.status != B.RA_ERR_CAPACITY:
+                raise
+            B.ra_seq_end(h, i, stream)
+            queue.appendleft(res.pop(i)[0])
+            break
+        for s in res:
+            res[s][1] += run
+    start_resident = len(res)
+    # per-slot input rings (inputs of a slot's request template; the values do
+    # not change the timing)
+    wl = Workload(1006, L, Hq, Hkv, 128, torch.bfloat16, True, ring=RING, device=dev)
+    bidx = torch.arange(SLOTS, device=dev)
+    lp_t = torch.tensor(lps[:SLOTS], device=dev)
+    q_ring = torch.empty(RING, L, SLOTS, Hq, 128, dtype=torch.bfloat16, device=dev)
+    k_ring = torch.empty(RING, L, SLOTS, Hkv, 128, dtype=torch.bfloat16, device=dev)
+    v_ring = torch.empty_like(k_ring)
+    for j in range(RING):
+        st = torch.full((SLOTS,), j, device=dev)
+        for l in range(L):
+            q_ring[j, l] = wl.q_step(bidx, l, st)
+            k, v = wl.kv_step(bidx, l, lp_t + st, lp_t)
+            k_ring[j, l], v_ring[j, l] = k, v
+    out = torch.empty(SLOTS, Hq, 128, dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    log("serving at a fixed cap (%s): %d requests resident at the start (%.1fs)"
+        % (layout_name, start_resident, time.time() - t0))
+
+    tokens = events = admissions = done = preempted = lost = 0
+    resident_sum = 0
+    kv_bytes = 0
+    wall0 = time.perf_counter()
+    for it in range(steps):
+        j = it % RING
+        while True:                   # the first layer takes the step's pages
+            try:
+                B.ra_decode_attention(h, 0, q_ring[j, 0], k_ring[j, 0], v_ring[j, 0], out,
+                                      cache.workspace, stream)
+                break
+            except B.RandAttnError as e:
+                if e.status != B.RA_ERR_CAPACITY or not res:
+                    raise
+                victim = min(res, key=lambda s: res[s][1])
+                B.ra_seq_end(h, victim, stream)
+                rid, step = res.pop(victim)
+                queue.appendleft(rid)
+                preempted += 1
+                lost += step
+        for l in range(1, L):
+            B.ra_decode_attention(h, l, q_ring[j, l], k_ring[j, l], v_ring[j, l], out,
+                                  cache.workspace, stream)
+        events += B.ra_end_step(h, stream)
+        tokens += len(res)
+        resident_sum += len(res)
+        for s in list(res):
+            res[s][1] += 1
+            kv_bytes += L * Hkv * 2 * 128 * 2 * B.ra_get_seq_info(h, s).len
+            if res[s][1] == GEN:
+                B.ra_seq_end(h, s, stream)
+                del res[s]
+                done += 1
+        # admissions into free slots while the pool accepts them
+        for slot in range(SLOTS):
+            if slot in res or not queue:
+                continue
+            if layout == B.RA_LAYOUT_PAGED:
+                _, free = B.ra_pool_info(h)
+                if free - L * Hkv * (lps[queue[0]] + page_rows) < watermark * pool:
+                    break
+            if not begin(slot, queue[0]):
+                break
+            queue.popleft()
+            admissions += 1
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    used, free = B.ra_pool_info(h)
+    out_d = {
+        "metric": "serving decode tokens/s at a fixed memory cap",
+        "value": tokens / wall, "unit": "tokens/s", "steps": steps,
+        "layout": layout_name + ("" if layout != B.RA_LAYOUT_PAGED else
+                                 " (%d-row pages)" % page_rows),
+        "pool_gb": pool * (2 * 128 * 2 + 4) / 1e9,
+        "resident_start": start_resident,
+        "resident_mean": resident_sum / steps,
+        "preemptions": preempted, "steps_lost_to_preemption": lost,
+        "admissions": admissions, "completions": done,
+        "compressions_per_step": events / steps,
+        "ms_per_step": 1e3 * wall / steps,
+        "attention_kv_gbs": kv_bytes / wall / 1e9,
+        "pool_used_at_end": used / (used + free),
+        "config": {"workload": "Phi-4-reasoning-shaped attention stack, prompts ~U[64,2048], "
+                               "8192-token generations, K=2048, r=64, evict every 64 steps, "
+                               "up to 256 slots, pool = 128 contiguous regions at the "
+                               "longest prompt"},
+    }
+    cache.close()
+    torch.cuda.empty_cache()
+    return out_d
+
+
 def time_window_scorer(B, torch, h, wl, cfg, Bsz, L, Hq, Hkv, stream, comp, log):
     """One round of the observation-window scoring pass over every sequence
     (what a score-based evictor computes before it can evict, and Random
@@ -587,7 +770,7 @@ def build_parser():
                     help="decode steps of the oracle's timed sample (about 10 s)")
     ap.add_argument("--attn-split", type=int, default=0)
     ap.add_argument("--layout", default="chronological",
-                    choices=["chronological", "holefill"],
+                    choices=["chronological", "holefill", "paged"],
                     help="row order kept by eviction (chronological: the paper's)")
     ap.add_argument("--policy", default="random",
                     choices=["random", "shared", "block", "recency"],
@@ -603,6 +786,12 @@ def build_parser():
                     help="continuous batching of a request stream on the Phi-4 shape "
                          "(staggered compressions, requests finishing and replaced); "
                          "prints its own JSON line; --steps sets the window")
+    ap.add_argument("--serving-cap", action="store_true",
+                    help="serving at a fixed memory cap, the pool of 128 contiguous "
+                         "regions, with --layout chronological or paged (--page-rows); "
+                         "prints its own JSON line; --steps sets the window")
+    ap.add_argument("--page-rows", type=int, default=64,
+                    help="rows per page of --layout paged")
     ap.add_argument("--evict-cost-methods", default="random,snapkv",
                     help="comma-separated rounds timed by --evict-cost: random, "
                          "random-holefill (the hole-fill layout) and the score-based "
@@ -722,6 +911,13 @@ def main():
         print(json.dumps({"calibrate_copy_bytes": src.numel() * 4}))
         return
 
+    if args.serving_cap:
+        def clog(msg):
+            print("[bench] " + msg, file=sys.stderr, flush=True)
+        print(json.dumps(serving_cap(B, torch, Workload, args.steps, clog, args.layout,
+                                     args.page_rows)), flush=True)
+        return
+
     if args.serving:
         def slog(msg):
             print("[bench] " + msg, file=sys.stderr, flush=True)
@@ -755,7 +951,8 @@ def main():
     total = args.warmup + args.steps
     lps, starts = sequence_plan(args.workload, w, total)
     assert min(starts) >= 0
-    layout = B.RA_LAYOUT_HOLE_FILL if args.layout == "holefill" else B.RA_LAYOUT_CHRONOLOGICAL
+    layout = {"chronological": B.RA_LAYOUT_CHRONOLOGICAL, "holefill": B.RA_LAYOUT_HOLE_FILL,
+              "paged": B.RA_LAYOUT_PAGED}[args.layout]
     policy = {"random": B.RA_POLICY_RANDOM, "shared": B.RA_POLICY_SHARED,
               "block": B.RA_POLICY_BLOCK, "recency": B.RA_POLICY_RECENCY}[args.policy]
     if policy == B.RA_POLICY_BLOCK and (args.block < 1 or EVERY % args.block):
@@ -763,7 +960,8 @@ def main():
         sys.exit(2)
     cfg = B.make_config(L, Hq, Hkv, K, R, EVERY, B.RA_BUDGET_EVICTABLE, B.RA_BF16, Bsz,
                         attn_split=args.attn_split, layout=layout, policy=policy,
-                        policy_block=args.block)
+                        policy_block=args.block, page_rows=args.page_rows,
+                        max_prompt_len=max(lps))
     rows = sum(B.ra_seq_rows(cfg, lp) for lp in lps)
     log("workload %s: pools %.1f GB" % (args.workload, rows * (128 * 2 * 2 + 4) / 1e9))
     cache = B.Cache(cfg, rows, device=dev)
@@ -948,7 +1146,8 @@ def main():
         "data": "synthetic",
         "config": {
             "workload": w["desc"],
-            "layout": args.layout,
+            "layout": args.layout + (" (%d-row pages)" % args.page_rows
+                                     if layout == B.RA_LAYOUT_PAGED else ""),
             "policy": args.policy if policy != B.RA_POLICY_BLOCK
             else "block%d" % args.block,
             "timed_window": window,
@@ -976,7 +1175,10 @@ def main():
         "end_to_end_gbs": total_bytes / wall / 1e9,
         "end_to_end_frac": total_bytes / wall / 1e9 / PEAK_HBM_GBS,
     }
-    if args.workload == "phi4-ragged" or args.window_scorer:
+    if layout != B.RA_LAYOUT_CHRONOLOGICAL and (args.workload == "phi4-ragged" or
+                                               args.window_scorer):
+        result["window_scorer"] = "not run: the scorer reads the contiguous chronological layout"
+    elif args.workload == "phi4-ragged" or args.window_scorer:
         del q_ring, k_ring, v_ring
         torch.cuda.empty_cache()
         result["window_scorer"] = time_window_scorer(B, torch, h, wl, cfg, Bsz, L, Hq,

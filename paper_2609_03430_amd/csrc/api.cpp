@@ -338,7 +338,8 @@ ra_status ra_config_check(const ra_config* c) {
         c->max_prompt_len < 0 ||
         (c->budget_mode == RA_BUDGET_TOTAL && c->max_prompt_len > c->budget_k))
       return RA_ERR_INVALID_ARG;
-    if (pages_per_seq(*c) > (int64_t(1) << 20)) return RA_ERR_UNSUPPORTED;
+    // the eviction kernel holds a sequence's block table in LDS
+    if (pages_per_seq(*c) > ra::kMaxPagesLds) return RA_ERR_UNSUPPORTED;
   }
   if (c->head_dim != ra::kHeadDim) return RA_ERR_UNSUPPORTED;
   if (c->num_q_heads / c->num_kv_heads > ra::kMaxGroup) return RA_ERR_UNSUPPORTED;

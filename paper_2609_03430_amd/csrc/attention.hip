@@ -219,17 +219,18 @@ __device__ __forceinline__ LaneMap lane_map() {
   return m;
 }
 
-// Kb, Vb: the block's first key row and first value tile (32 consecutive
-// rows, within one page in the paged layout).
-__device__ __forceinline__ void load_block(BlockRegs& b, const uint16_t* Kb,
-                                           const uint16_t* Vb, const LaneMap& lm) {
+// Rows kb .. kb+31 from the key rows at Kr and the value tiles at Vr (the
+// head's region; in the paged layout the block's page, with kb = 0).
+__device__ __forceinline__ void load_block(BlockRegs& b, const uint16_t* Kr,
+                                           const uint16_t* Vr, int kb,
+                                           const LaneMap& lm) {
 #pragma unroll
   for (int t = 0; t < 2; ++t) {
-    const uint16_t* row = Kb + lm.krow[t] * kHeadDim + lm.kcol;
+    const uint16_t* row = Kr + static_cast<int64_t>(kb + lm.krow[t]) * kHeadDim + lm.kcol;
 #pragma unroll
     for (int s = 0; s < 4; ++s) b.k[t][s] = ld16(row + 32 * s);
   }
-  const uint16_t* vt = Vb + lm.vrow * kHeadDim + lm.vch * 8;
+  const uint16_t* vt = Vr + static_cast<int64_t>(kb + lm.vrow) * kHeadDim + lm.vch * 8;
 #pragma unroll
   for (int u = 0; u < 8; ++u) b.v[u] = ld16_stream(vt + 16 * 8 * u);
 }
@@ -313,8 +314,18 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
   const LaneMap lm = lane_map();
   const uint16_t* kpool = static_cast<const uint16_t*>(a.kpool);
   const uint16_t* vpool = static_cast<const uint16_t*>(a.vpool);
-  // the first row of key block kb (a multiple of 32) in the pools
-  auto block_row = [&](int kb) -> int64_t { return pool_row<PAGED>(w.rm, kb); };
+  const uint16_t* Kr = kpool + w.rm.region * kHeadDim;
+  const uint16_t* Vr = vpool + w.rm.region * kHeadDim;
+  // key block kb (a multiple of 32): its 32 rows lie in one page of the paged
+  // layout, found through the block table; contiguous layouts index the region
+  auto load = [&](BlockRegs& b, int kb) {
+    if constexpr (PAGED) {
+      const int64_t br = pool_row<true>(w.rm, kb);
+      load_block(b, kpool + br * kHeadDim, vpool + br * kHeadDim, 0, lm);
+    } else {
+      load_block(b, Kr, Vr, kb, lm);
+    }
+  };
   const uint16_t* kn = static_cast<const uint16_t*>(a.k_new) +
                        (static_cast<int64_t>(w.slot) * Hkv + w.g) * kHeadDim;
   const uint16_t* vn = static_cast<const uint16_t*>(a.v_new) +
@@ -343,7 +354,13 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
   // this wavefront's keys: [k0, k1) within the split (a multiple of 32 long
   // except where it ends at the new key)
   const int kpw = a.split_keys / W;
-  const int k0 = w.k0 + wave * kpw;
+  // the same in every lane of the wavefront; in the paged builds of up to 8
+  // wavefronts, made scalar, so that block-table entries are scalar loads
+  // and block bases scalar sums (the 12-wavefront build has no registers to
+  // spare for it and looks the table up per lane)
+  constexpr bool kScalarTable = PAGED && W <= 8;
+  const int k0 = kScalarTable ? __builtin_amdgcn_readfirstlane(w.k0 + wave * kpw)
+                              : w.k0 + wave * kpw;
   const int k1 = min(k0 + kpw, w.k1);
   const bool has = k0 < k1;
   const bool owns_last = has && k1 == w.n_keys;
@@ -357,17 +374,13 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
     const int last = nfull - 1;
     BlockRegs buf[kNBuf];
 #pragma unroll
-    for (int j = 0; j < kNBuf; ++j) {
-      const int64_t br = block_row(k0 + 32 * min(j, last));
-      load_block(buf[j], kpool + br * kHeadDim, vpool + br * kHeadDim, lm);
-    }
+    for (int j = 0; j < kNBuf; ++j) load(buf[j], k0 + 32 * min(j, last));
     int i = 0;
     for (; i + kNBuf - 1 < nfull; i += kNBuf) {
 #pragma unroll
       for (int j = 0; j < kNBuf; ++j) {
         compute_block(st, buf[j], qop, scale_log2, 32);
-        const int64_t br = block_row(k0 + 32 * min(i + kNBuf + j, last));
-        load_block(buf[j], kpool + br * kHeadDim, vpool + br * kHeadDim, lm);
+        load(buf[j], k0 + 32 * min(i + kNBuf + j, last));
       }
     }
 #pragma unroll
@@ -378,11 +391,16 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
     // tail block: cached rows below len, the new pair at len, masked above
     const int kb = k0 + 32 * nfull;
     const int limit = w.n_keys - kb;       // 1..32 valid keys
-    // rows below len of this block lie in its page (the page of row len may
-    // not be mapped yet when len is a multiple of 32: only rows < len are read)
-    const int64_t br = kb < w.len ? block_row(kb) : 0;
-    const uint16_t* Kb = kpool + br * kHeadDim;
-    const uint16_t* Vb = vpool + br * kHeadDim;
+    // rows of this block below len lie in one page of the paged layout (only
+    // rows below len are read from the pools: the page of row len may not be
+    // in the table yet when len is a multiple of 32)
+    const uint16_t* Kb = Kr + static_cast<int64_t>(kb) * kHeadDim;
+    const uint16_t* Vb = Vr + static_cast<int64_t>(kb) * kHeadDim;
+    if constexpr (PAGED) {
+      const int64_t br = kb < w.len ? pool_row<true>(w.rm, kb) : 0;
+      Kb = kpool + br * kHeadDim;
+      Vb = vpool + br * kHeadDim;
+    }
     BlockRegs b;
     const u32x4 z = {0u, 0u, 0u, 0u};
 #pragma unroll

@@ -137,6 +137,33 @@ __device__ __forceinline__ u32x4 funnel8(u32x4 a, u32x4 b, int off) {
   }
 }
 
+// Pool row of row j of the head being compacted: a contiguous region, or
+// pages found through the sequence's block table, copied to LDS.
+// Positions are indexed by pos_row(j) from the base the caller passes: the
+// region's first position for a contiguous region, the pool's otherwise.
+struct RegionRows {
+  static constexpr bool kPaged = false;
+  int64_t region;
+  __device__ __forceinline__ int64_t operator()(int j) const { return region + j; }
+  __device__ __forceinline__ int pos_row(int j) const { return j; }
+  // region + a + b, added in that order (the 64-bit sum first keeps the
+  // compaction within its 128 registers)
+  __device__ __forceinline__ int64_t plus(int a, int b) const { return region + a + b; }
+};
+
+struct PagedRows {
+  static constexpr bool kPaged = true;
+  const int* table;        // LDS copy of the sequence's block table
+  int64_t group_rows, head_off;
+  int shift;
+  __device__ __forceinline__ int64_t operator()(int j) const {
+    return static_cast<int64_t>(table[j >> shift]) * group_rows + head_off +
+           (j & ((1 << shift) - 1));
+  }
+  __device__ __forceinline__ int64_t pos_row(int j) const { return (*this)(j); }
+  __device__ __forceinline__ int64_t plus(int a, int b) const { return (*this)(a + b); }
+};
+
 // Order-preserving in-place compaction of one head's region: destination
 // row j < new_len (from the first drop d0 on) receives source row
 // j + #{k : f[k] <= j}, where f[k] = d_k - k for the ascending drop list d.
@@ -145,12 +172,12 @@ __device__ __forceinline__ u32x4 funnel8(u32x4 a, u32x4 b, int off) {
 // returned and synchronises, then writes.  Sources are never below destinations and a
 // chunk's writes land below the next chunk's sources, so the move is
 // race-free.  Called by every thread of the workgroup.
-template <int NT, typename E, bool POS_ONLY, bool PAGED>
+template <int NT, typename E, bool POS_ONLY, typename Rows>
 __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, int d0,
-                                             int new_len, int old_len, const RowMap& rm,
+                                             int new_len, int old_len, const Rows& row,
                                              E* __restrict__ kpool, E* __restrict__ vpool,
-                                             int32_t* __restrict__ pos) {
-  auto row = [&](int j) -> int64_t { return pool_row<PAGED>(rm, j); };
+                                             int32_t* __restrict__ P) {
+  constexpr bool PAGED = Rows::kPaged;
   constexpr int kEpu = 16 / sizeof(E);            // elements per 16-byte unit
   constexpr int kKUnitsRow = kHeadDim / kEpu;     // 16-byte units per key row
   constexpr int kVUnitsCh = 8 / kEpu;             // units per (tile, channel)
@@ -168,7 +195,7 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
 
     int pval = 0;
     const bool pos_mine = t < kChunk && j0 + t >= d0 && j0 + t < new_len;
-    if (pos_mine) pval = pos[row(src_of[t])];
+    if (pos_mine) pval = P[row.pos_row(src_of[t])];
     u32x4 kbuf[POS_ONLY ? 1 : kKPer];
     E vbuf[POS_ONLY ? 1 : kVPer][kEpu];
     if constexpr (!POS_ONLY) {
@@ -220,7 +247,7 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
 
-    if (pos_mine) pos[row(j0 + t)] = pval;
+    if (pos_mine) P[row.pos_row(j0 + t)] = pval;
     if constexpr (!POS_ONLY) {
 #pragma unroll
       for (int q = 0; q < kKPer; ++q) {
@@ -239,7 +266,7 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
         const int rem = u % (kHeadDim * kVUnitsCh);
         const int ch = rem / kVUnitsCh, part = rem % kVUnitsCh;
         if (u < kVUnits && j0 + tile * 8 < new_len) {
-          E* dst = vpool + vt_index(row(j0 + tile * 8), ch) + part * kEpu;
+          E* dst = vpool + vt_index(row.plus(j0, tile * 8), ch) + part * kEpu;
           u32x4 w;
           __builtin_memcpy(&w, vbuf[q], 16);
           store_stream(dst, w);
@@ -278,10 +305,20 @@ __global__ __launch_bounds__(NT) void evict_kernel(
   // are [lp, old_len - r); after hole-fill events the recent rows may sit
   // anywhere above the prompt, so every slot from lp is examined
   const int span = LAYOUT == 1 ? old_len - lp : C;
-  const RowMap rm = row_map(Mref, slot, lg, pg);
-  const int64_t region = rm.region;
-  int32_t* P = pos + region;     // hole-fill (contiguous) only
+  const int64_t region = Mref.base + static_cast<int64_t>(lg) * Mref.cap;
+  int32_t* P = pos + region;     // contiguous layouts
   const int t = threadIdx.x;
+  // paged: the sequence's block table, read once into LDS
+  __shared__ int tbl[PAGED ? kMaxPagesLds : 1];
+  PagedRows prow{};
+  if constexpr (PAGED) {
+    const int32_t* table = pg.tables + static_cast<int64_t>(slot) * pg.pages_per_seq;
+    const int n_pages = (old_len + (1 << pg.page_shift) - 1) >> pg.page_shift;
+    for (int i = t; i < n_pages; i += NT) tbl[i] = table[i];
+    __syncthreads();
+    prow = PagedRows{tbl, pg.group_rows, static_cast<int64_t>(lg) << pg.page_shift,
+                     pg.page_shift};
+  }
 
   // 1. scores of this thread's KPT consecutive slots; ties by position
   uint64_t score[KPT];
@@ -293,7 +330,9 @@ __global__ __launch_bounds__(NT) void evict_kernel(
     score[i] = 0;
     tie[i] = 0;
     if (c < span) {
-      const int p = pos[pool_row<PAGED>(rm, lp + c)];
+      int p;
+      if constexpr (PAGED) p = pos[prow(lp + c)];
+      else p = P[lp + c];
       if (p < thr) {
         score[i] = policy_key(policy, block, p, lp, event, layer, g, seed, rid);
         tie[i] = static_cast<uint32_t>(p);
@@ -346,8 +385,11 @@ __global__ __launch_bounds__(NT) void evict_kernel(
 
   // 4. order-preserving in-place compaction of positions, keys and values
   __shared__ int src_of[chunk_rows<NT, E>()];
-  compact_rows<NT, E, POS_ONLY, PAGED>(f, m, src_of, d0, new_len, old_len, rm, kpool, vpool,
-                                       pos);
+  if constexpr (PAGED)
+    compact_rows<NT, E, POS_ONLY>(f, m, src_of, d0, new_len, old_len, prow, kpool, vpool, pos);
+  else
+    compact_rows<NT, E, POS_ONLY>(f, m, src_of, d0, new_len, old_len, RegionRows{region},
+                                  kpool, vpool, P);
 }
 
 // Compaction of a score-based round: each due head's drop list comes from
@@ -371,9 +413,9 @@ __global__ __launch_bounds__(NT) void compact_drops_kernel(
   const int32_t* d = drops + static_cast<int64_t>(blockIdx.x) * stride;
   for (int k = threadIdx.x; k < m; k += NT) f[k] = d[k] - k;
   __syncthreads();
-  const RowMap rm = row_map(M, slot, lg, Paging{});
-  compact_rows<NT, E, false, false>(f, m, src_of, f[0], new_len, old_len, rm, kpool, vpool,
-                                    pos);
+  const int64_t region = M.base + static_cast<int64_t>(lg) * M.cap;
+  compact_rows<NT, E, false>(f, m, src_of, f[0], new_len, old_len, RegionRows{region}, kpool,
+                             vpool, pos + region);
 }
 
 template <int NT, int KPT, bool POS_ONLY, int LAYOUT>

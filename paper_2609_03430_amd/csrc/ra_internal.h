@@ -31,6 +31,7 @@ constexpr int kMaxSplits = 64;      // attention work items per head
 constexpr int kMaxEvery = 1024;     // evict_every limit: drops per event <= this
 constexpr int kMaxCandidates = 32768;
 constexpr int kRegionAlign = 32;    // region rows rounded to the key block
+constexpr int kMaxPagesLds = 4096;  // paged layout: block-table entries per sequence
 
 // Per-slot device state, 64 bytes.  The hot-path kernels read it; the
 // end-of-step and plan kernels update it; the host keeps an identical mirror.

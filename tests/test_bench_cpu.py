@@ -32,13 +32,14 @@ def test_ragged_plan_is_seeded_and_in_range():
 
 def test_traffic_is_reported_only_for_the_profiled_run(monkeypatch):
     """The stored counter traffic is the mean over the timed launches of one
-    run (the default bench line); a run with other settings, or kernels
-    changed since, reports none."""
+    run (the bench line the driver runs: --gpus 1 --steps 20 --warmup 5); a
+    run with other settings, or kernels changed since, reports none."""
     sys.path.insert(0, ROOT)
     import bench
     with open(os.path.join(ROOT, "profiles", "attention_traffic_qwen3-14b.json")) as f:
         stored = json.load(f)
-    default = bench.run_signature(bench.build_parser().parse_args([]))
+    default = bench.run_signature(bench.build_parser().parse_args(
+        ["--gpus", "1", "--steps", "20", "--warmup", "5"]))
     assert stored["run"] == default
     monkeypatch.setattr(bench, "kernel_source_hash", lambda read=None: stored["kernel_source_hash"])
     assert bench.read_traffic(default) == stored["hbm_bytes_per_launch"]
@@ -60,3 +61,49 @@ def test_tiny_cpu_baseline_replays_the_whole_run():
     r = bench.tiny_cpu_baseline(128, 256, 1024, 4, 2, 1000 * 1000003, 0)
     assert r["events"] == 11 and r["kind"] == "oracle" and r["unit"] == "us/step"
     assert r["value"] > 0 and r["cores"] >= 1
+
+
+def test_traffic_summary_parses_counter_csvs(tmp_path, monkeypatch):
+    """The summary takes the last steps x layers attention dispatches of a
+    FETCH_SIZE and a WRITE_SIZE run (the timed ones), scales them by the 1 GiB
+    copy's counts, and records the run's signature."""
+    sys.path.insert(0, ROOT)
+    import bench
+    cols = ["Correlation_Id", "Dispatch_Id", "Agent_Id", "Queue_Id", "Process_Id",
+            "Thread_Id", "Grid_Size", "Kernel_Id", "Kernel_Name", "Workgroup_Size",
+            "LDS_Block_Size", "Scratch_Size", "VGPR_Count", "SGPR_Count",
+            "Counter_Name", "Counter_Value", "Start_Timestamp", "End_Timestamp"]
+
+    def write(d, counter, rows):
+        d.mkdir()
+        with open(d / "run_counter_collection.csv", "w") as f:
+            f.write(",".join(cols) + "\n")
+            for i, (name, v) in enumerate(rows):
+                vals = {c: "0" for c in cols}
+                vals.update(Dispatch_Id=str(i + 1), Kernel_Name='"%s"' % name,
+                            Counter_Name=counter, Counter_Value=str(v))
+                f.write(",".join(vals[c] for c in cols) + "\n")
+
+    steps, L = 2, bench.WORKLOADS["qwen3-14b"]["L"]
+    attn = "void ra::attn_bf16_kernel<12, 1, false>(ra::AttnLaunch, ra::Paging, int)"
+    full = "void ra::evict_kernel<1024, 9, unsigned short, false, 0>(ra::SeqMeta const*)"
+    warm = [(attn, 999.0)] * L                       # warm-up launches: not sampled
+    write(tmp_path / "f", "FETCH_SIZE", warm + [(attn, 100.0)] * (steps * L) + [(full, 50.0)])
+    write(tmp_path / "w", "WRITE_SIZE", warm + [(attn, 2.0)] * (steps * L) + [(full, 40.0)])
+    write(tmp_path / "cf", "FETCH_SIZE", [("copy_kernel", 524288.0)] * 3)
+    write(tmp_path / "cw", "WRITE_SIZE", [("copy_kernel", 1048576.0)] * 3)
+    written = {}
+    monkeypatch.setattr(bench.json, "dump", lambda obj, f, **kw: written.update(obj))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda read=None: "0" * 16)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    (tmp_path / "profiles").mkdir()
+    args = bench.build_parser().parse_args(
+        ["--steps", str(steps), "--warmup", "1", "--traffic-summary",
+         str(tmp_path / "f"), str(tmp_path / "w"), str(tmp_path / "cf"), str(tmp_path / "cw")])
+    bench.traffic_summary(args)
+    assert written["launches_sampled"] == steps * L
+    assert written["copy_calibration"]["fetch_scale"] == 2.0
+    assert written["fetch_bytes_per_launch"] == 100.0 * 1024 * 2.0
+    assert written["write_bytes_per_launch"] == 2.0 * 1024
+    assert written["evict_full_event"] == {"fetch_bytes": 50.0 * 2048, "write_bytes": 40.0 * 1024}
+    assert written["run"]["steps"] == steps and written["run"]["warmup"] == 1
