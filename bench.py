@@ -58,15 +58,23 @@ WORKLOADS = {
 SEEDS = {"qwen3-4b": 1001, "qwen3-14b": 1002, "qwen3-32b": 1003, "phi4-ragged": 1004}
 
 
-def sequence_plan(name, w, total):
-    """Per-sequence (prompt length, step at the start of the warm-up)."""
+def sequence_plan(name, w, total, steps=None):
+    """Per-sequence (prompt length, step at the start of the warm-up).
+
+    The timed steps of a uniform workload end at the last step of the
+    generation; a window shorter than two trigger periods is instead centred
+    on the event one period before the end, so that it holds the event and
+    the step after it (whose attention moves a deferred event's rows)."""
     import numpy as np
     if name == "phi4-ragged":
         rng = np.random.default_rng(SEEDS[name])
         lps = rng.integers(64, 2049, w["B"]).tolist()
         gens = sorted(rng.integers(4096, 32769, w["B"]).tolist(), reverse=True)
         return lps, gens
-    return [w["lp"]] * w["B"], [w["T"] - total] * w["B"]
+    start = w["T"] - total
+    if steps is not None and steps < 2 * EVERY:
+        start = w["T"] - EVERY - (total - steps) - steps // 2
+    return [w["lp"]] * w["B"], [start] * w["B"]
 R = 64
 EVERY = 64
 RING = 64
@@ -837,8 +845,14 @@ def _counter_rows(d):
 
 
 def traffic_summary(args):
-    """Copy-calibrated HBM bytes per attention launch (and per full eviction
-    event) of the timed region of one bench run, from two counter runs."""
+    """Copy-calibrated HBM bytes per attention launch, and per eviction event,
+    of the timed region of one bench run, from two counter runs.
+
+    An event either moves its rows itself (a full evict_kernel dispatch) or
+    selects only (the last positions-only evict_kernel dispatch: the fast
+    forward's are earlier) and leaves the moves to the next step's attention
+    (attn_bf16_move_kernel, one dispatch per layer); the latter's bytes above
+    as many plain attention launches are the moves' share."""
     fetch_dir, write_dir, cfetch_dir, cwrite_dir = args.traffic_summary
     w = WORKLOADS[args.workload]
 
@@ -854,15 +868,29 @@ def traffic_summary(args):
     copy_bytes = 1 << 30
     cf, cw = copy_kib(cfetch_dir, "FETCH_SIZE"), copy_kib(cwrite_dir, "WRITE_SIZE")
     fscale, wscale = copy_bytes / (cf * 1024), copy_bytes / (cw * 1024)
-    timed = args.steps * w["L"]
     attn = lambda n: "attn_bf16_kernel" in n
+    move = lambda n: "attn_bf16_move_kernel" in n
     full_evict = lambda n: "evict_kernel" in n and "false" in n
+    select_evict = lambda n: "evict_kernel" in n and "true" in n
+    fm = per_dispatch(fetch_dir, "FETCH_SIZE", move)
+    wm = per_dispatch(write_dir, "WRITE_SIZE", move)
+    timed = args.steps * w["L"] - len(fm)
     fa = per_dispatch(fetch_dir, "FETCH_SIZE", attn)[-timed:]
     wa = per_dispatch(write_dir, "WRITE_SIZE", attn)[-timed:]
     fe = per_dispatch(fetch_dir, "FETCH_SIZE", full_evict)
     we = per_dispatch(write_dir, "WRITE_SIZE", full_evict)
     fb = sum(fa) / len(fa) * 1024 * fscale
     wb = sum(wa) / len(wa) * 1024 * wscale
+    deferred = None
+    if fm and wm:
+        fs = per_dispatch(fetch_dir, "FETCH_SIZE", select_evict)[-1] * 1024 * fscale
+        ws = per_dispatch(write_dir, "WRITE_SIZE", select_evict)[-1] * 1024 * wscale
+        mf, mw = sum(fm) * 1024 * fscale, sum(wm) * 1024 * wscale
+        deferred = {"select_fetch_bytes": fs, "select_write_bytes": ws,
+                    "move_attention_launches": len(fm),
+                    "move_attention_fetch_bytes": mf, "move_attention_write_bytes": mw,
+                    "moves_fetch_bytes": mf - len(fm) * fb,
+                    "moves_write_bytes": mw - len(wm) * wb}
     out = {
         "workload": args.workload,
         "kernel": "attn_bf16_kernel",
@@ -878,6 +906,7 @@ def traffic_summary(args):
         "evict_full_event": ({"fetch_bytes": sum(fe) / len(fe) * 1024 * fscale,
                               "write_bytes": sum(we) / len(we) * 1024 * wscale}
                              if fe and we else None),
+        "evict_deferred_event": deferred,
         "run": run_signature(args),
     }
     path = os.path.join(ROOT, "profiles", "attention_traffic_%s.json" % args.workload)
@@ -949,7 +978,7 @@ def main():
         print("[bench] " + msg, file=sys.stderr, flush=True)
 
     total = args.warmup + args.steps
-    lps, starts = sequence_plan(args.workload, w, total)
+    lps, starts = sequence_plan(args.workload, w, total, None if args.full_run else args.steps)
     assert min(starts) >= 0
     layout = {"chronological": B.RA_LAYOUT_CHRONOLOGICAL, "holefill": B.RA_LAYOUT_HOLE_FILL,
               "paged": B.RA_LAYOUT_PAGED}[args.layout]
@@ -1041,12 +1070,17 @@ def main():
                 x1 = torch.cuda.Event(enable_timing=True)
                 x0.record(stream)
             nev = B.ra_end_step(h, stream)
+            deferred = nev > 0 and any(B.ra_get_seq_info(h, b).move_pending for b in range(Bsz))
             if timed:
                 x1.record(stream)
-                rec.append((lens, evs, (x0, x1), nev))
+                rec.append((lens, evs, (x0, x1), nev, deferred))
+            last_event[0] = nev > 0
         return rec
 
+    last_event = [False]     # whether the step before the next one ended in an event
+
     run_steps(0, args.warmup, False)
+    post0 = last_event[0]    # the first timed step follows an event
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     rec = run_steps(args.warmup, args.steps, True)
@@ -1081,7 +1115,13 @@ def main():
         first = 0.0 if policy == B.RA_POLICY_RECENCY else unit * (n_u - j_u) / (j_u + 1)
         moved = K + R - first
         per_head = moved * (2 * 128 * s_el + 4) * 2 + C * 4
-    for lens, evs, (x0, x1), nev in rec:
+    post = []                # per timed step: it follows an event step
+    prev = post0
+    any_deferred = False
+    for lens, evs, (x0, x1), nev, deferred in rec:
+        post.append(prev)
+        prev = nev > 0
+        any_deferred = any_deferred or deferred
         per_launch = sum(Hkv * ((n + 1) * 2 * 128 * s_el + (2 * 128 * s_el + 4)) +
                          2 * Hq * 128 * s_el for n in lens)
         for e0, e1 in evs:            # one span = L launches
@@ -1092,20 +1132,35 @@ def main():
             seq_events += nev
             ev_ms.append(x0.elapsed_time(x1))
             ev_bytes.append(per_head * nev * L * Hkv)
+    # a deferred event's rows move in the next step's attention: its cost is
+    # the end-of-step time plus that step's extra attention time
+    plain = [ms for ms, p in zip(attn_ms, post) if not p]
+    after = [ms for ms, p in zip(attn_ms, post) if p]
+    post_extra = (sum(after) / len(after) - sum(plain) / len(plain)
+                  if any_deferred and after and plain else 0.0)
     attn_avg_ms = sum(attn_ms) / (len(attn_ms) * L)
     attn_gbs = sum(attn_bytes) / (sum(attn_ms) * 1e-3) / 1e9
     comp = None
     if ev_ms:
+        end_ms = sum(ev_ms) / len(ev_ms)
+        event_ms = end_ms + post_extra
+        gbs = sum(ev_bytes) / len(ev_bytes) / (event_ms * 1e-3) / 1e9
         comp = {
             "end_steps_with_events": n_events,
             "sequence_events": seq_events,
-            "avg_ms_per_end_step_with_events": sum(ev_ms) / len(ev_ms),
-            "achieved_gbs": sum(ev_bytes) / (sum(ev_ms) * 1e-3) / 1e9,
+            "avg_ms_per_end_step_with_events": end_ms,
+            "rows_moved_by_next_attention": any_deferred,
+            "next_attention_extra_ms": post_extra if any_deferred else None,
+            "event_ms": event_ms,
+            "achieved_gbs": gbs,
             "peak_gbs": PEAK_HBM_GBS,
-            "frac": sum(ev_bytes) / (sum(ev_ms) * 1e-3) / 1e9 / PEAK_HBM_GBS,
+            "frac": gbs / PEAK_HBM_GBS,
             "bytes_note": "per (sequence, layer, KV head) event: expected rows moved by "
                           "the order-preserving shift (from the first drop to the end) x "
-                          "(key + value + position) x 2, plus candidate positions read",
+                          "(key + value + position) x 2, plus candidate positions read; "
+                          "over event_ms = the end-of-step time plus, when the next step's "
+                          "attention moves the rows, that step's attention time above "
+                          "the other steps' mean",
         }
     total_bytes = sum(attn_bytes) + sum(ev_bytes)
     # Steady-state rate: a window of `steps` steps holds round(steps / 64)
@@ -1114,19 +1169,20 @@ def main():
     # every step the mean attention span, the mean end-of-step time of steps
     # without events, and 1/64 of the mean event.
     amortised = None
-    if ev_ms and len(set(starts)) == 1:
-        quiet = [x0.elapsed_time(x1) for _, _, (x0, x1), nev in rec if not nev]
-        step_ms = (sum(attn_ms) / len(attn_ms) + (sum(quiet) / len(quiet) if quiet else 0.0) +
-                   sum(ev_ms) / len(ev_ms) / EVERY)
+    if ev_ms and len(set(starts)) == 1 and plain and (after or not any_deferred):
+        quiet = [x0.elapsed_time(x1) for _, _, (x0, x1), nev, _ in rec if not nev]
+        step_ms = (sum(plain) / len(plain) + (sum(quiet) / len(quiet) if quiet else 0.0) +
+                   comp["event_ms"] / EVERY)
         amortised = {"value": Bsz / (step_ms * 1e-3), "unit": "tokens/s",
                      "ms_per_step": step_ms,
-                     "note": "mean attention span per step + mean end-of-step time "
-                             "without an event + mean event / 64 (GPU time from HIP "
-                             "events; the raw value is wall time over the window)"}
+                     "note": "mean attention span of the steps that follow no event + "
+                             "mean end-of-step time without an event + (the event's "
+                             "end-of-step time + the next attention's extra time) / 64 "
+                             "(GPU time from HIP events; the raw value is wall time over "
+                             "the window)"}
     if len(set(starts)) == 1:
         window = ("decode steps %d..%d of %d (%d end-of-step eviction events)"
-                  % (starts[0] + args.warmup + 1, starts[0] + total, starts[0] + total,
-                     n_events))
+                  % (starts[0] + args.warmup + 1, starts[0] + total, w["T"], n_events))
     else:
         window = ("%d timed decode steps per sequence, sequence i from step "
                   "start_i + %d (start_i %d..%d), %d sequence eviction events"

@@ -186,6 +186,9 @@ typedef struct {
   int32_t k_keep;       /* evictable rows kept per head */
   int32_t cap;          /* row capacity of each (layer, KV head) region */
   int64_t base;         /* first pool row of the sequence's regions */
+  int32_t move_pending; /* 1: the last event compacted the positions and the
+                           next step's attention moves the key/value rows
+                           (see ra_end_step) */
 } ra_seq_info;
 
 /* ---- sizing (pure host functions; no device access) --------------------- */
@@ -282,7 +285,11 @@ ra_status ra_get_seq_info(const ra_cache* cache, int32_t seq, ra_seq_info* out);
  * RA_ERR_CAPACITY is returned before a region would overflow.  In the paged
  * layout the first layer of a step takes a page group for every sequence
  * whose new row starts a page; RA_ERR_CAPACITY, before any launch, if the
- * pool has too few free groups (ending a sequence frees its groups). */
+ * pool has too few free groups (ending a sequence frees its groups).  After
+ * an event whose row moves were deferred (ra_end_step), the layer's
+ * attention also moves that layer's surviving rows to their compacted slots
+ * (if the step's plan splits a head into several work items, a separate
+ * launch moves them first). */
 ra_status ra_decode_attention(ra_cache* cache, int32_t layer, const void* q,
                               const void* k_new, const void* v_new, void* out,
                               void* workspace, size_t workspace_bytes,
@@ -310,7 +317,13 @@ ra_status ra_decode_attention_noalloc(ra_cache* cache, int32_t layer, const void
 /* End the decode step of every active sequence: step += 1, then run the
  * periodic eviction (Eq. 1 with Random Attention's scores, Appendix F
  * trigger) on every (layer, KV head) of each sequence that is due (never
- * under RA_POLICY_EXTERNAL).
+ * under RA_POLICY_EXTERNAL).  bf16, contiguous chronological layout: when
+ * every active sequence is due at this step and the next step's attention
+ * gives each head one work item, the event selects and compacts the
+ * positions only, and that attention moves each layer's key/value rows while
+ * it reads them (the kept sets are final at once; the rows are final after
+ * the next step, or as soon as a call that reads or writes rows, or plans
+ * another event, moves them first).
  * Requires every layer to have been appended this step.  If n_evicted is
  * non-NULL it receives the number of sequences evicted (host mirror). */
 ra_status ra_end_step(ra_cache* cache, void* stream, int32_t* n_evicted);

@@ -82,7 +82,8 @@ class ra_seq_info(ctypes.Structure):
     _fields_ = [("active", ctypes.c_int32), ("prompt_len", ctypes.c_int32),
                 ("len", ctypes.c_int32), ("step", ctypes.c_int32),
                 ("event", ctypes.c_int32), ("k_keep", ctypes.c_int32),
-                ("cap", ctypes.c_int32), ("base", ctypes.c_int64)]
+                ("cap", ctypes.c_int32), ("base", ctypes.c_int64),
+                ("move_pending", ctypes.c_int32)]
 
 
 _P = ctypes.c_void_p

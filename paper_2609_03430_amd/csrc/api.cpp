@@ -81,6 +81,26 @@ size_t meta_records_bytes(const ra_config& c) {
   return static_cast<size_t>(round_up(static_cast<int64_t>(sizeof(SeqMeta)) * c.max_seqs, 256));
 }
 
+size_t tables_bytes(const ra_config& c) {
+  if (!paged(c)) return 0;
+  return static_cast<size_t>(round_up(
+      static_cast<int64_t>(sizeof(int32_t)) * c.max_seqs * pages_per_seq(c), 256));
+}
+
+// Events whose row moves the next step's attention can carry (bf16, the
+// contiguous chronological layout): their drop lists, evict_every per head.
+bool defers_moves(const ra_config& c) {
+  return c.dtype == RA_BF16 && c.layout == RA_LAYOUT_CHRONOLOGICAL &&
+         c.policy != RA_POLICY_EXTERNAL;
+}
+
+size_t drops_bytes(const ra_config& c) {
+  if (!defers_moves(c)) return 0;
+  return static_cast<size_t>(round_up(static_cast<int64_t>(sizeof(int32_t)) * c.max_seqs *
+                                          c.num_layers * c.num_kv_heads * c.evict_every,
+                                      256));
+}
+
 }  // namespace
 
 struct ra_cache {
@@ -103,6 +123,8 @@ struct ra_cache {
   int64_t n_groups = 0;                  // page groups in the pool
   std::vector<int32_t> free_groups;      // stack: the next group is back()
   std::vector<std::vector<int32_t>> groups;   // per slot: its table, in order
+  // deferred row moves (see ra_end_step)
+  int32_t* drops = nullptr;              // drop lists of the last events
   void* scratch = nullptr;               // device address of the no-alloc partials
 
   ra::Shape shape() const {
@@ -111,6 +133,11 @@ struct ra_cache {
                      cfg.policy, std::max(1, cfg.policy_block), pg};
   }
   bool is_paged() const { return cfg.layout == RA_LAYOUT_PAGED; }
+  bool any_pending() const {
+    for (int s = slot_lo; s < slot_hi; ++s)
+      if (mirror[s].active && mirror[s].due == ra::kDueMovePending) return true;
+    return false;
+  }
   int64_t pages_for(int64_t rows) const { return (rows + page_rows - 1) / page_rows; }
   // paged: page groups slot `s` must add to hold `rows` rows
   // paged: whether `rows` rows fit the block table of one sequence (rows
@@ -254,6 +281,18 @@ ra_status check_decode(const ra_cache* c, int32_t layer, const void* q, const vo
   return RA_OK;
 }
 
+// Moves the key/value rows of every sequence whose last event deferred them
+// (their positions are already compacted); a call that reads or writes rows,
+// or plans another event, runs this first.
+ra_status flush_pending(ra_cache* c, hipStream_t s) {
+  if (!c->any_pending()) return RA_OK;
+  RA_LAUNCH(ra::launch_flush_pending(c->shape(), c->meta, c->kpool, c->vpool, c->drops,
+                                     c->cfg.evict_every, c->slot_lo, c->slot_hi, s));
+  for (int i = c->slot_lo; i < c->slot_hi; ++i)
+    if (c->mirror[i].due == ra::kDueMovePending) c->mirror[i].due = 0;
+  return RA_OK;
+}
+
 // Marks the layer appended and launches its append + attention with the
 // given partials buffers (split_stride partial slots per head).
 ra_status launch_decode(ra_cache* c, int32_t layer, const void* q, const void* k_new,
@@ -268,6 +307,17 @@ ra_status launch_decode(ra_cache* c, int32_t layer, const void* q, const void* k
       const hipError_t e = ra::launch_table_set(c->shape(), te.data(),
                                                 static_cast<int>(te.size()), stream);
       if (e != hipSuccess) return hip_fail(e);
+    }
+  }
+  // rows of deferred events move in this step's attention when every head is
+  // one work item; otherwise they move first, on their own
+  bool move = false;
+  if (c->any_pending()) {
+    if (plan.max_splits == 1) {
+      move = true;
+    } else {
+      const ra_status st = flush_pending(c, stream);
+      if (st != RA_OK) return st;
     }
   }
   c->appended[layer] = 1;
@@ -291,6 +341,12 @@ ra_status launch_decode(ra_cache* c, int32_t layer, const void* q, const void* k
   a.max_splits = plan.max_splits;
   a.waves = plan.waves;
   a.wide_regs = plan.wide_regs;
+  if (move) {
+    a.move = 1;
+    a.waves = 8;
+    a.drops = c->drops;
+    a.drop_stride = c->cfg.evict_every;
+  }
   const hipError_t e = ra::launch_attention(c->shape(), a, stream);
   if (e != hipSuccess) {
     c->appended[layer] = 0;
@@ -387,11 +443,7 @@ int64_t ra_required_slots(const ra_config* c, const int32_t* prompt_lens, int32_
 
 size_t ra_meta_bytes(const ra_config* c) {
   if (ra_config_check(c) != RA_OK) return 0;
-  size_t bytes = meta_records_bytes(*c);
-  if (paged(*c))
-    bytes += static_cast<size_t>(round_up(
-        static_cast<int64_t>(sizeof(int32_t)) * c->max_seqs * pages_per_seq(*c), 256));
-  return bytes;
+  return meta_records_bytes(*c) + tables_bytes(*c) + drops_bytes(*c);
 }
 
 size_t ra_workspace_bytes(const ra_config* c) {
@@ -447,6 +499,9 @@ ra_status ra_cache_create(const ra_config* cfg, void* k_pool, void* v_pool,
       c->free_groups[i] = static_cast<int32_t>(c->n_groups - 1 - i);   // 0 first
     c->groups.assign(cfg->max_seqs, {});
   }
+  if (defers_moves(*cfg))
+    c->drops = reinterpret_cast<int32_t*>(static_cast<char*>(meta) + meta_records_bytes(*cfg) +
+                                          tables_bytes(*cfg));
   const hipError_t e = ra::launch_zero_words(static_cast<uint32_t*>(meta),
                                              static_cast<int64_t>(ra_meta_bytes(cfg) / 4),
                                              static_cast<hipStream_t>(stream));
@@ -482,6 +537,7 @@ ra_status ra_get_seq_info(const ra_cache* c, int32_t seq, ra_seq_info* out) {
   out->k_keep = M.k_keep;
   out->cap = M.cap;
   out->base = M.base;
+  out->move_pending = M.due == ra::kDueMovePending;
   return RA_OK;
 }
 
@@ -654,15 +710,31 @@ ra_status ra_end_step(ra_cache* c, void* stream, int32_t* n_evicted) {
     if (!M.active) continue;
     M.step += 1;
     M.len += 1;
-    mirror_plan(M, c->cfg.recent_r, at_trigger(c->cfg, M.step));
+    mirror_plan(M, c->cfg.recent_r, at_trigger(c->cfg, M.step));   // clears a pending move
     due += M.due;
     // the pages past the new length are free once the event (launched below,
     // ahead of any later use of them on this stream) has moved their rows
     if (M.due && c->is_paged()) c->shrink(i, M.len);
   }
   if (due) {
+    // When every active sequence evicts at this step and the next step's
+    // attention gives every head one work item, the event only selects
+    // (positions compacted, each head's drop list kept) and that attention,
+    // which reads every row anyway, moves the key/value rows
+    // (attn_bf16_move_kernel): the rows are read once instead of twice.
+    // Sequences evicting on staggered phases keep the event's own moves, so
+    // that steps of heads with nothing to move run the streaming kernel.
+    int n_active = 0;
+    for (int i = c->slot_lo; i < c->slot_hi; ++i) n_active += c->mirror[i].active;
+    const bool defer = c->drops && due == n_active && attention_plan(c).max_splits == 1;
     RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos,
-                               c->slot_lo, c->slot_hi, c->max_candidates_due(), false, s));
+                               c->slot_lo, c->slot_hi, c->max_candidates_due(), defer, s,
+                               defer ? c->drops : nullptr, c->cfg.evict_every));
+    if (defer) {
+      RA_LAUNCH(ra::launch_mark_pending(c->meta, c->slot_lo, c->slot_hi, s));
+      for (int i = c->slot_lo; i < c->slot_hi; ++i)
+        if (c->mirror[i].active && c->mirror[i].due) c->mirror[i].due = ra::kDueMovePending;
+    }
   }
   if (n_evicted) *n_evicted = due;
   return RA_OK;
@@ -682,6 +754,8 @@ ra_status ra_evict_now(ra_cache* c, int32_t seq, void* stream) {
       ra::kMaxCandidates)
     return RA_ERR_UNSUPPORTED;
   const hipStream_t s = static_cast<hipStream_t>(stream);
+  const ra_status fl = flush_pending(c, s);
+  if (fl != RA_OK) return fl;
   RA_LAUNCH(ra::launch_plan_now(c->meta, seq, c->cfg.recent_r, s));
   for (int i = c->slot_lo; i < c->slot_hi; ++i) c->mirror[i].due = 0;
   mirror_plan(M, c->cfg.recent_r, true);
@@ -698,6 +772,8 @@ ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
   if (c->step_open()) return RA_ERR_STATE;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const int every = c->cfg.evict_every;
+  const ra_status fl = flush_pending(c, s);
+  if (fl != RA_OK) return fl;
   // Runs of steps up to the next trigger of any sequence.  The first pass
   // replays them on a copy of the mirror only, so that a capacity error (rows
   // piling up under the external policy) is reported before any launch; the
@@ -790,6 +866,8 @@ ra_status ra_write_rows(ra_cache* c, int32_t seq, const void* dev_k, const void*
   if (c->step_open()) return RA_ERR_STATE;
   const SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
+  const ra_status fl = flush_pending(c, static_cast<hipStream_t>(stream));
+  if (fl != RA_OK) return fl;
   // positions are left as they are: pass the region's own positions through
   RA_LAUNCH(ra::launch_write_rows(c->shape(), M, seq, M.len, dev_k, dev_v, nullptr,
                                   c->kpool, c->vpool, nullptr, static_cast<hipStream_t>(stream)));
@@ -804,6 +882,8 @@ ra_status ra_read_rows(ra_cache* c, int32_t seq, int32_t layer, int32_t kv_head,
   if (c->step_open()) return RA_ERR_STATE;
   const SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
+  const ra_status fl = flush_pending(c, static_cast<hipStream_t>(stream));
+  if (fl != RA_OK) return fl;
   RA_LAUNCH(ra::launch_read_rows(c->shape(), M, seq, layer * c->cfg.num_kv_heads + kv_head,
                                  M.len, c->kpool, c->vpool, dev_k_out, dev_v_out,
                                  static_cast<hipStream_t>(stream)));
@@ -830,6 +910,8 @@ ra_status ra_window_select(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
   if (max_len == 0) return RA_OK;
   if (dev_scores && scores_stride < max_len) return RA_ERR_INVALID_ARG;
   if (max_len - c->cfg.recent_r > 512 * 32) return RA_ERR_UNSUPPORTED;
+  const ra_status fl = flush_pending(c, static_cast<hipStream_t>(stream));
+  if (fl != RA_OK) return fl;
   RA_LAUNCH(ra::launch_window_score(c->shape(), c->meta, c->kpool, c->pos, dev_q_window,
                                     dev_scores, dev_drops, scores_stride, seq_lo, seq_hi,
                                     max_len, static_cast<hipStream_t>(stream)));
@@ -883,6 +965,8 @@ ra_status ra_scored_evict(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
   int32_t* drops = static_cast<int32_t*>(dev_scratch);
   float* scores = reinterpret_cast<float*>(drops + heads * every);
   const hipStream_t s = static_cast<hipStream_t>(stream);
+  const ra_status fl = flush_pending(c, s);
+  if (fl != RA_OK) return fl;
   // 1. score and select on the current rows; 2. the plan rule (new length,
   // event count) on device and mirror; 3. compaction from the drop lists
   if (prm->scorer == RA_SCORER_SNAPKV) {

@@ -242,10 +242,13 @@ struct Softmax {
 };
 
 // One 32-key block.  `limit`: keys with index >= limit (block-relative) are
-// masked out (32 for a full block).
+// masked out (32 for a full block); with MASKED, so are the keys whose bit is
+// set in `dropped`.
+template <bool MASKED = false>
 __device__ __forceinline__ void compute_block(Softmax& st, const BlockRegs& b,
                                               const bf16x8 (&qop)[4],
-                                              float scale_log2, int limit) {
+                                              float scale_log2, int limit,
+                                              uint32_t dropped = 0) {
   f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
@@ -263,6 +266,13 @@ __device__ __forceinline__ void compute_block(Softmax& st, const BlockRegs& b,
 #pragma unroll
     for (int e = 0; e < 8; ++e)
       if (8 * grp + e >= limit) x[e] = kNegInf;
+  }
+  if constexpr (MASKED) {
+    if (dropped) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if ((dropped >> (8 * grp + e)) & 1u) x[e] = kNegInf;
+    }
   }
   float bm = x[0];
 #pragma unroll
@@ -502,6 +512,280 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// bf16, MFMA, moving the rows of a deferred eviction on the way
+// ---------------------------------------------------------------------------
+
+// The last block of a head's source rows, kb .. kb+31, reaching past the
+// cached rows: it is loaded as a full block (rows past the region's end read
+// its row 0, so every lane issues the same sixteen loads as for any block and
+// the loads in flight stay countable) and, once the data has arrived, row
+// n_rows becomes the step's new pair (staged in LDS: nk, nv) and the rows
+// above it zero.
+__device__ __forceinline__ void load_block_clamped(BlockRegs& b, const uint16_t* Kr,
+                                                   const uint16_t* Vr, int kb, int n_rows,
+                                                   const LaneMap& lm) {
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int key = kb + lm.krow[t];
+    const uint16_t* row = Kr + static_cast<int64_t>(key < n_rows ? key : 0) * kHeadDim + lm.kcol;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) b.k[t][s] = ld16(row + 32 * s);
+  }
+  const int key0 = kb + lm.vrow;                      // a tile's first row (8-aligned)
+  const uint16_t* vt = Vr + static_cast<int64_t>(key0 < n_rows ? key0 : 0) * kHeadDim + lm.vch * 8;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) b.v[u] = ld16_stream(vt + 16 * 8 * u);
+}
+
+__device__ __forceinline__ void patch_block_tail(BlockRegs& b, const uint16_t* nk,
+                                                 const uint16_t* nv, int kb, int n_rows,
+                                                 const LaneMap& lm) {
+  const u32x4 z = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int t = 0; t < 2; ++t) {
+    const int key = kb + lm.krow[t];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      if (key == n_rows) b.k[t][s] = *reinterpret_cast<const u32x4*>(nk + lm.kcol + 32 * s);
+      else if (key > n_rows) b.k[t][s] = z;
+    }
+  }
+  const int key0 = kb + lm.vrow;
+  if (key0 + 8 > n_rows) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      uint16_t e8[8];
+      __builtin_memcpy(e8, &b.v[u], 16);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if (key0 + e == n_rows) e8[e] = nv[16 * u + lm.vch];
+        else if (key0 + e > n_rows) e8[e] = 0;
+      }
+      __builtin_memcpy(&b.v[u], e8, 16);
+    }
+  }
+}
+
+// Decode attention for the step after a deferred eviction (contiguous
+// chronological layout, bf16, one workgroup of W wavefronts per (sequence,
+// KV head), the whole head).  A sequence whose event deferred its row moves
+// (due == kDueMovePending) holds its key/value rows in the order before the
+// event, rows [0, plan_len), and the event's drop slots; its positions are
+// already compacted and len = plan_len - m.  Attention runs over the
+// surviving rows and the step's new pair (the dropped rows are masked), and
+// every surviving row j after the first drop moves down to its compacted
+// slot j - #{drops below j}, so the rows end as a full event would leave
+// them, without reading them a second time.  The blocks are dealt in rounds,
+// block r * W + v to wavefront v; every wavefront's loads of a round have
+// returned (the round's softmax consumed them) before the barrier that
+// precedes the round's moves.  A row moves only down, into a block of its
+// own round or of an earlier one, which was read before that barrier, and
+// no round reads a row that an earlier round wrote; the next round's loads,
+// issued before the barrier, read only rows above every destination of the
+// round.  The new pair is stored at len after the last round.  Sequences
+// with nothing to move take the same path without moves.
+template <int W>
+__global__ __launch_bounds__(64 * W, 1) void attn_bf16_move_kernel(
+    AttnLaunch a, int L, int G, int Hq, int Hkv, float scale_log2) {
+  __shared__ float s_m[W][kMaxGroup];
+  __shared__ float s_l[W][kMaxGroup];
+  __shared__ float s_o[W][kMaxGroup][kHeadDim];
+  __shared__ int s_drop[kMaxEvery];
+  // a round's surviving value rows in destination order, per channel, offset
+  // by the round's first destination row mod 8 so that destination tiles
+  // start on 16-byte boundaries
+  constexpr int kStage = W * 32 + 16;
+  __shared__ __align__(16) uint16_t s_v[kHeadDim][kStage];
+  __shared__ __align__(16) uint16_t s_new[2][kHeadDim];  // the step's key, value
+  const int g = blockIdx.y, slot = blockIdx.z;
+  const SeqMeta& M = a.meta[slot];
+  if (!M.active) return;
+  const bool moving = M.due == kDueMovePending;
+  const int len = M.len;                              // rows once compacted
+  const int n_rows = moving ? M.plan_len : len;       // rows in the region now
+  const int m = min(n_rows - len, kMaxEvery);        // <= evict_every (host)
+  const int lg = a.layer * Hkv + g;
+  const int64_t region = M.base + static_cast<int64_t>(lg) * M.cap;
+  // wavefront-uniform (the block indices and the drop scans below are scalar)
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, qi = lane & 15, grp = lane >> 4;
+  if (moving) {
+    const int32_t* d = a.drops + (static_cast<int64_t>(slot) * L * Hkv + lg) * a.drop_stride;
+    for (int k = threadIdx.x; k < min(m, kMaxEvery); k += 64 * W) s_drop[k] = d[k];
+  }
+  {
+    const uint16_t* src = threadIdx.x < kHeadDim ? static_cast<const uint16_t*>(a.k_new)
+                                                 : static_cast<const uint16_t*>(a.v_new);
+    if (threadIdx.x < 2 * kHeadDim)
+      (&s_new[0][0])[threadIdx.x] =
+          src[(static_cast<int64_t>(slot) * Hkv + g) * kHeadDim + (threadIdx.x & (kHeadDim - 1))];
+  }
+  __syncthreads();
+  const LaneMap lm = lane_map();
+  uint16_t* kpool = static_cast<uint16_t*>(a.kpool);
+  uint16_t* vpool = static_cast<uint16_t*>(a.vpool);
+  const uint16_t* Kr = kpool + region * kHeadDim;
+  const uint16_t* Vr = vpool + region * kHeadDim;
+
+  bf16x8 qop[4];
+  {
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) +
+        (static_cast<int64_t>(slot) * Hq + g * G + qi) * kHeadDim + 8 * grp;
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const u32x4 z = {0u, 0u, 0u, 0u};
+      qop[s] = as_bf16x8(qi < G ? ld16(qrow + 32 * s) : z);
+    }
+  }
+  Softmax st;
+  st.m = kNegInf;
+  st.l = 0.f;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) st.acc[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int n_keys = n_rows + 1;                      // the region's rows + the new pair
+  const int nblk = (n_keys + 31) / 32;
+  const int rounds = (nblk + W - 1) / W;
+  auto load = [&](BlockRegs& b, int blk) {
+    const int kb = blk * 32;
+    if (kb + 32 <= n_rows) load_block(b, Kr, Vr, kb, lm);
+    else load_block_clamped(b, Kr, Vr, kb, n_rows, lm);
+  };
+  // two register buffers, each named (an array indexed by the round's parity
+  // would live in scratch memory): the loop below runs two rounds per pass
+  // every round issues its sixteen prefetch loads, also for blocks past the
+  // last key (they read the region's row 0 and are never used): with a fixed
+  // count of loads after each block's, the wait for a block leaves the next
+  // block's loads in flight
+  BlockRegs buf0, buf1;
+  load(buf0, wave);
+  int di = 0;                 // drops below the current block (wavefront-uniform)
+  auto round = [&](int r, BlockRegs& cur, BlockRegs& nxt) {
+    const int blk = r * W + wave;
+    const int kb = blk * 32;
+    const bool have = blk < nblk;
+    load(nxt, blk + W);
+    uint32_t dropped = 0;
+    if (have) {
+      if (kb + 32 > n_rows) patch_block_tail(cur, s_new[0], s_new[1], kb, n_rows, lm);
+      while (di < m && s_drop[di] < kb) ++di;
+      for (int k = di; k < m && s_drop[k] < kb + 32; ++k) dropped |= 1u << (s_drop[k] - kb);
+      compute_block<true>(st, cur, qop, scale_log2, min(32, n_keys - kb), dropped);
+    }
+    __syncthreads();          // every load of the round has been consumed
+    if (moving && have) {
+      const BlockRegs& b = cur;
+      // key rows: this lane's two rows, four 16-byte chunks each
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const int rr = lm.krow[t], j = kb + rr;
+        if (j < n_rows && !((dropped >> rr) & 1u)) {
+          const int dst = j - di - __popc(__builtin_amdgcn_ubfe(dropped, 0, rr));
+          if (dst != j) {
+            uint16_t* row = kpool + (region + dst) * kHeadDim + lm.kcol;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) *reinterpret_cast<u32x4*>(row + 32 * s) = b.k[t][s];
+          }
+        }
+      }
+    }
+    if (moving) {
+      // values: the round's survivors go to LDS in destination order, then the
+      // workgroup writes whole destination tiles (16 bytes per channel); only
+      // the round's first and last tiles, shared with the neighbouring rounds,
+      // are written element by element
+      const int r0 = r * W * 32;                                 // round's first source row
+      int fr = 0;                                                // drops below r0
+      while (fr < m && s_drop[fr] < r0) ++fr;
+      const int r1 = min(r0 + W * 32, n_rows);                   // round's source rows [r0, r1)
+      int fe = fr;
+      while (fe < m && s_drop[fe] < r1) ++fe;
+      const int d_lo = r0 - fr, d_hi = r1 - fe;                  // destinations [d_lo, d_hi)
+      const int off = d_lo & 7;
+      if (have && kb < n_rows) {
+        const BlockRegs& b = cur;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int rr = lm.vrow + e, j = kb + rr;
+          if (j < n_rows && !((dropped >> rr) & 1u)) {
+            const int dst = j - di - __popc(__builtin_amdgcn_ubfe(dropped, 0, rr));
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+              uint16_t e8[8];
+              __builtin_memcpy(e8, &b.v[u], 16);
+              s_v[16 * u + lm.vch][off + dst - d_lo] = e8[e];
+            }
+          }
+        }
+      }
+      __syncthreads();
+      if (d_hi > d_lo && r1 > s_drop[0]) {
+        const int t_lo = d_lo >> 3, t_hi = (d_hi - 1) >> 3;       // destination tiles
+        const int items = (t_hi - t_lo + 1) * kHeadDim;
+        for (int it = threadIdx.x; it < items; it += 64 * W) {
+          const int tile = t_lo + it / kHeadDim, ch = it % kHeadDim;
+          const int lo = max(tile * 8, d_lo), hi = min(tile * 8 + 8, d_hi);
+          const int64_t row0 = region + tile * 8;                // 8-aligned (region is)
+          uint16_t* dstp = vpool + row0 * kHeadDim + ch * 8;
+          const uint16_t* src = &s_v[ch][off + tile * 8 - d_lo];
+          if (lo == tile * 8 && hi == tile * 8 + 8) {
+            *reinterpret_cast<u32x4*>(dstp) = *reinterpret_cast<const u32x4*>(src);
+          } else {
+            for (int x = lo; x < hi; ++x) dstp[x - tile * 8] = src[x - tile * 8];
+          }
+        }
+      }
+    }
+  };
+  for (int r = 0; r < rounds; r += 2) {
+    round(r, buf0, buf1);
+    if (r + 1 < rounds) round(r + 1, buf1, buf0);
+  }
+  st.l += __shfl_xor(st.l, 16, 64);
+  st.l += __shfl_xor(st.l, 32, 64);
+  // lane indices taken afresh (kept from before the rounds, they would be
+  // spilled: the rounds hold every register)
+  const int lane_e = __lane_id(), qe = lane_e & 15, ge = lane_e >> 4;
+  const int tid = wave * 64 + lane_e;
+  __syncthreads();            // every move is done: the new pair goes to row len
+  if (wave == 0) {
+    const int64_t row = region + len;
+    for (int c = lane_e; c < kHeadDim; c += 64) {
+      kpool[row * kHeadDim + c] = s_new[0][c];
+      vpool[(row & ~int64_t(7)) * kHeadDim + c * 8 + (row & 7)] = s_new[1][c];
+    }
+    if (lane_e == 0) a.pos[row] = M.prompt_len + M.step;
+  }
+
+  // merge the W wavefronts in LDS and write the normalised output
+  if (qe < G) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      *reinterpret_cast<f32x4*>(&s_o[wave][qe][16 * u + 4 * ge]) = st.acc[u];
+    if (ge == 0) {
+      s_m[wave][qe] = st.m;
+      s_l[wave][qe] = st.l;
+    }
+  }
+  __syncthreads();
+  uint16_t* out = static_cast<uint16_t*>(a.out);
+  for (int idx = tid; idx < G * kHeadDim; idx += 64 * W) {
+    const int q = idx / kHeadDim, c = idx % kHeadDim;
+    float mx = kNegInf;
+#pragma unroll
+    for (int v = 0; v < W; ++v) mx = fmaxf(mx, s_m[v][q]);
+    float lsum = 0.f, o = 0.f;
+#pragma unroll
+    for (int v = 0; v < W; ++v) {
+      const float sc = s_m[v][q] == kNegInf ? 0.f : exp2f(s_m[v][q] - mx);
+      lsum += s_l[v][q] * sc;
+      o += s_o[v][q][c] * sc;
+    }
+    out[(static_cast<int64_t>(slot) * Hq + g * G + q) * kHeadDim + c] = f32_to_bf16(o / lsum);
+  }
+}
+
+// ---------------------------------------------------------------------------
 // fp32, VALU
 // ---------------------------------------------------------------------------
 
@@ -652,7 +936,14 @@ hipError_t launch_attention_t(const Shape& sh, const AttnLaunch& a, hipStream_t 
   // scores in log2 units: q.k / sqrt(d) * log2(e)
   const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(kHeadDim));
   const dim3 cgrid(sh.Hkv, a.max_seqs);
-  if (sh.dtype == 1) {
+  if (sh.dtype == 1 && a.move) {
+    // one workgroup per head (max_splits == 1), rows of deferred events moved;
+    // eight wavefronts (256 registers each: two per SIMD; a four-wavefront
+    // build needs more than 256 and would run one per SIMD)
+    const dim3 mgrid(1, sh.Hkv, a.max_seqs);
+    hipLaunchKernelGGL((attn_bf16_move_kernel<8>), mgrid, dim3(512), 0, s, a, sh.L, sh.G,
+                       sh.Hq, sh.Hkv, scale_log2);
+  } else if (sh.dtype == 1) {
     if (a.waves == 12)
       hipLaunchKernelGGL((attn_bf16_kernel<12, 1, PAGED>), grid, dim3(768), 0, s, a, sh.pg,
                          sh.G, sh.Hq, sh.Hkv, scale_log2);

@@ -172,7 +172,7 @@ struct PagedRows {
 // returned and synchronises, then writes.  Sources are never below destinations and a
 // chunk's writes land below the next chunk's sources, so the move is
 // race-free.  Called by every thread of the workgroup.
-template <int NT, typename E, bool POS_ONLY, typename Rows>
+template <int NT, typename E, bool POS_ONLY, typename Rows, bool MOVE_POS = true>
 __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, int d0,
                                              int new_len, int old_len, const Rows& row,
                                              E* __restrict__ kpool, E* __restrict__ vpool,
@@ -194,7 +194,7 @@ __device__ __forceinline__ void compact_rows(const int* f, int m, int* src_of, i
     __syncthreads();
 
     int pval = 0;
-    const bool pos_mine = t < kChunk && j0 + t >= d0 && j0 + t < new_len;
+    const bool pos_mine = MOVE_POS && t < kChunk && j0 + t >= d0 && j0 + t < new_len;
     if (pos_mine) pval = P[row.pos_row(src_of[t])];
     u32x4 kbuf[POS_ONLY ? 1 : kKPer];
     E vbuf[POS_ONLY ? 1 : kVPer][kEpu];
@@ -281,7 +281,8 @@ template <int NT, int KPT, typename E, bool POS_ONLY, int LAYOUT>
 __global__ __launch_bounds__(NT) void evict_kernel(
     const SeqMeta* __restrict__ meta, E* __restrict__ kpool,
     E* __restrict__ vpool, int32_t* __restrict__ pos, int L, int Hkv, int r,
-    int slot_lo, int policy, int block, Paging pg) {
+    int slot_lo, int policy, int block, Paging pg, int32_t* __restrict__ drops_out,
+    int drop_stride) {
   constexpr bool PAGED = LAYOUT == 2;
   static_assert(KPT <= 32, "drop flags live in one 32-bit mask");
   __shared__ SelectShared sel_sh;
@@ -345,6 +346,12 @@ __global__ __launch_bounds__(NT) void evict_kernel(
   const uint32_t drop = select_smallest<NT, KPT, 64>(score, tie, valid, m, sel_sh);
   drop_list<NT, KPT>(drop, lp, f, sel_sh);
   const int d0 = f[0];
+  // deferred row moves: this head's drop slots, ascending, for the next
+  // step's attention (rows are left in place by a positions-only event)
+  if (drops_out) {
+    int32_t* dst = drops_out + (static_cast<int64_t>(slot) * per_seq + lg) * drop_stride;
+    for (int k = t; k < m; k += NT) dst[k] = f[k] + k;
+  }
 
   if constexpr (LAYOUT == 1) {
     // hole-fill: the h holes below new_len take the h surviving rows of the
@@ -418,21 +425,45 @@ __global__ __launch_bounds__(NT) void compact_drops_kernel(
                              vpool, pos + region);
 }
 
+// Key/value rows of a deferred event (contiguous chronological layout): the
+// event compacted the positions and recorded each head's drop slots; the
+// rows move here, for sequences whose next attention did not move them.
+template <int NT, typename E>
+__global__ __launch_bounds__(NT) void move_pending_kernel(
+    const SeqMeta* __restrict__ meta, E* __restrict__ kpool, E* __restrict__ vpool,
+    const int32_t* __restrict__ drops, int stride, int L, int Hkv, int slot_lo) {
+  __shared__ int f[kMaxEvery];
+  __shared__ int src_of[chunk_rows<NT, E>()];
+  const int per_seq = L * Hkv;
+  const int slot = slot_lo + static_cast<int>(blockIdx.x) / per_seq;
+  const int lg = static_cast<int>(blockIdx.x) % per_seq;
+  const SeqMeta& M = meta[slot];
+  if (!M.active || M.due != kDueMovePending) return;
+  const int old_len = M.plan_len, new_len = M.len, m = old_len - new_len;
+  if (m <= 0 || m > stride) return;
+  const int32_t* d = drops + (static_cast<int64_t>(slot) * per_seq + lg) * stride;
+  for (int k = threadIdx.x; k < m; k += NT) f[k] = d[k] - k;
+  __syncthreads();
+  const int64_t region = M.base + static_cast<int64_t>(lg) * M.cap;
+  compact_rows<NT, E, false, RegionRows, false>(f, m, src_of, f[0], new_len, old_len,
+                                                RegionRows{region}, kpool, vpool, nullptr);
+}
+
 template <int NT, int KPT, bool POS_ONLY, int LAYOUT>
 hipError_t launch_layout(const Shape& sh, const SeqMeta* meta, void* kpool,
                          void* vpool, int32_t* pos, int slot_lo, int slot_hi,
-                         hipStream_t s) {
+                         hipStream_t s, int32_t* drops_out, int drop_stride) {
   const dim3 grid((slot_hi - slot_lo) * sh.L * sh.Hkv);
   if (sh.dtype == 1) {
     hipLaunchKernelGGL((evict_kernel<NT, KPT, uint16_t, POS_ONLY, LAYOUT>), grid,
                        dim3(NT), 0, s, meta, static_cast<uint16_t*>(kpool),
                        static_cast<uint16_t*>(vpool), pos, sh.L, sh.Hkv, sh.r,
-                       slot_lo, sh.policy, sh.block, sh.pg);
+                       slot_lo, sh.policy, sh.block, sh.pg, drops_out, drop_stride);
   } else {
     hipLaunchKernelGGL((evict_kernel<NT, KPT, float, POS_ONLY, LAYOUT>), grid,
                        dim3(NT), 0, s, meta, static_cast<float*>(kpool),
                        static_cast<float*>(vpool), pos, sh.L, sh.Hkv, sh.r,
-                       slot_lo, sh.policy, sh.block, sh.pg);
+                       slot_lo, sh.policy, sh.block, sh.pg, drops_out, drop_stride);
   }
   return hipGetLastError();
 }
@@ -440,40 +471,41 @@ hipError_t launch_layout(const Shape& sh, const SeqMeta* meta, void* kpool,
 template <int NT, int KPT, bool POS_ONLY>
 hipError_t launch_kpt(const Shape& sh, const SeqMeta* meta, void* kpool,
                       void* vpool, int32_t* pos, int slot_lo, int slot_hi,
-                      hipStream_t s) {
+                      hipStream_t s, int32_t* drops_out, int drop_stride) {
   if (sh.layout == 1)
     return launch_layout<NT, KPT, POS_ONLY, 1>(sh, meta, kpool, vpool, pos, slot_lo,
-                                               slot_hi, s);
+                                               slot_hi, s, drops_out, drop_stride);
   if (sh.layout == 2)
     return launch_layout<NT, KPT, POS_ONLY, 2>(sh, meta, kpool, vpool, pos, slot_lo,
-                                               slot_hi, s);
+                                               slot_hi, s, drops_out, drop_stride);
   return launch_layout<NT, KPT, POS_ONLY, 0>(sh, meta, kpool, vpool, pos, slot_lo,
-                                             slot_hi, s);
+                                             slot_hi, s, drops_out, drop_stride);
 }
 
 template <bool POS_ONLY>
 hipError_t launch_mode(const Shape& sh, const SeqMeta* meta, void* kpool,
                        void* vpool, int32_t* pos, int slot_lo, int slot_hi,
-                       int max_candidates, hipStream_t s) {
+                       int max_candidates, hipStream_t s, int32_t* drops_out,
+                       int drop_stride) {
   // 1,024 threads, KPT scores each: the smallest KPT that holds the
   // candidates (C = K + 64 at the usual budgets: K = 1,024 -> 2, 2,048 -> 3,
   // 4,096 -> 5, 8,192 -> 9).  More than 16 scores per thread is kept for the
   // largest budgets only: 32 unrolled Philox evaluations exceed the
   // compiler's unroll budget and the score array then lives in scratch memory.
   if (max_candidates <= 1024 * 1)
-    return launch_kpt<1024, 1, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+    return launch_kpt<1024, 1, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s, drops_out, drop_stride);
   if (max_candidates <= 1024 * 2)
-    return launch_kpt<1024, 2, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+    return launch_kpt<1024, 2, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s, drops_out, drop_stride);
   if (max_candidates <= 1024 * 3)
-    return launch_kpt<1024, 3, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+    return launch_kpt<1024, 3, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s, drops_out, drop_stride);
   if (max_candidates <= 1024 * 5)
-    return launch_kpt<1024, 5, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+    return launch_kpt<1024, 5, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s, drops_out, drop_stride);
   if (max_candidates <= 1024 * 9)
-    return launch_kpt<1024, 9, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+    return launch_kpt<1024, 9, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s, drops_out, drop_stride);
   if (max_candidates <= 1024 * 16)
-    return launch_kpt<1024, 16, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+    return launch_kpt<1024, 16, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s, drops_out, drop_stride);
   if (max_candidates <= kMaxCandidates)
-    return launch_kpt<1024, 32, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s);
+    return launch_kpt<1024, 32, POS_ONLY>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi, s, drops_out, drop_stride);
   return hipErrorInvalidValue;
 }
 
@@ -498,13 +530,31 @@ hipError_t launch_compact_drops(const Shape& sh, const SeqMeta* meta, void* kpoo
 hipError_t launch_evict(const Shape& sh, const SeqMeta* meta, void* kpool,
                         void* vpool, int32_t* pos, int slot_lo, int slot_hi,
                         int max_candidates, bool positions_only,
-                        hipStream_t s) {
+                        hipStream_t s, int32_t* drops_out, int drop_stride) {
   if (slot_hi <= slot_lo) return hipSuccess;
   if (positions_only)
     return launch_mode<true>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi,
-                             max_candidates, s);
+                             max_candidates, s, drops_out, drop_stride);
   return launch_mode<false>(sh, meta, kpool, vpool, pos, slot_lo, slot_hi,
-                            max_candidates, s);
+                            max_candidates, s, drops_out, drop_stride);
+}
+
+hipError_t launch_flush_pending(const Shape& sh, SeqMeta* meta, void* kpool, void* vpool,
+                                const int32_t* drops, int drop_stride, int slot_lo,
+                                int slot_hi, hipStream_t s) {
+  if (slot_hi <= slot_lo) return hipSuccess;
+  const dim3 grid((slot_hi - slot_lo) * sh.L * sh.Hkv);
+  if (sh.dtype == 1)
+    hipLaunchKernelGGL((move_pending_kernel<1024, uint16_t>), grid, dim3(1024), 0, s, meta,
+                       static_cast<uint16_t*>(kpool), static_cast<uint16_t*>(vpool), drops,
+                       drop_stride, sh.L, sh.Hkv, slot_lo);
+  else
+    hipLaunchKernelGGL((move_pending_kernel<1024, float>), grid, dim3(1024), 0, s, meta,
+                       static_cast<float*>(kpool), static_cast<float*>(vpool), drops,
+                       drop_stride, sh.L, sh.Hkv, slot_lo);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_clear_pending(meta, slot_lo, slot_hi, s);
 }
 
 }  // namespace ra

@@ -46,11 +46,14 @@ struct SeqMeta {
   uint64_t seed;       // Philox key word 0
   uint64_t rid;        // Philox key word 1 (request id)
   int32_t active;
-  int32_t due;         // 1: an eviction is planned for this sequence
+  int32_t due;         // 1: an eviction is planned for this sequence;
+                       // kDueMovePending: its positions are compacted and the
+                       // next step's attention moves its key/value rows
   int32_t plan_len;    // rows per region before the planned eviction
   int32_t plan_event;  // event index of the planned eviction
 };
 static_assert(sizeof(SeqMeta) == 64, "SeqMeta must stay 64 bytes");
+constexpr int kDueMovePending = 2;
 
 // Block tables of the paged layout (null tables: a contiguous layout).
 struct Paging {
@@ -108,7 +111,18 @@ hipError_t launch_append_positions(const Shape& sh, const SeqMeta* meta, int32_t
                                    int slot_lo, int slot_hi, int run, hipStream_t s);
 hipError_t launch_evict(const Shape& sh, const SeqMeta* meta, void* kpool,
                         void* vpool, int32_t* pos, int slot_lo, int slot_hi,
-                        int max_candidates, bool positions_only, hipStream_t s);
+                        int max_candidates, bool positions_only, hipStream_t s,
+                        int32_t* drops_out = nullptr, int drop_stride = 0);
+// Deferred row moves: the drop lists of the last event, [max_seqs][L][Hkv]
+// [drop_stride] int32 (ascending slots), written by a positions-only event.
+// launch_mark_pending turns due == 1 into kDueMovePending for the active
+// slots of [lo, hi); launch_flush_pending moves the key/value rows of every
+// pending sequence (positions are already in place) and clears the flag.
+hipError_t launch_mark_pending(SeqMeta* meta, int slot_lo, int slot_hi, hipStream_t s);
+hipError_t launch_clear_pending(SeqMeta* meta, int slot_lo, int slot_hi, hipStream_t s);
+hipError_t launch_flush_pending(const Shape& sh, SeqMeta* meta, void* kpool, void* vpool,
+                                const int32_t* drops, int drop_stride, int slot_lo,
+                                int slot_hi, hipStream_t s);
 // Rows [0, len) of every head of slot `slot` (host mirror M) from row-major
 // sources [L * Hkv][len][128] (positions: pos_src, or 0..len-1 if null).
 hipError_t launch_write_rows(const Shape& sh, const SeqMeta& M, int slot, int len,
@@ -149,6 +163,11 @@ struct AttnLaunch {
   int max_splits;
   int waves;           // wavefronts per work item (bf16 path: 1, 4, 8 or 12)
   int wide_regs;       // bf16, 4 wavefronts: the build for one wavefront per SIMD
+  // some sequence has a deferred row move (bf16, one split per head): the
+  // launch runs the kernel that moves rows while it attends
+  int move;
+  const int32_t* drops;  // the deferred drop lists (see launch_evict)
+  int drop_stride;
 };
 hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s);
 

@@ -66,6 +66,18 @@ __global__ void plan_now_kernel(SeqMeta* meta, int slot, int r) {
   meta[slot] = M;
 }
 
+__global__ void mark_pending_kernel(SeqMeta* meta, int lo, int hi) {
+  const int s = lo + blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= hi) return;
+  if (meta[s].active && meta[s].due == 1) meta[s].due = kDueMovePending;
+}
+
+__global__ void clear_pending_kernel(SeqMeta* meta, int lo, int hi) {
+  const int s = lo + blockIdx.x * blockDim.x + threadIdx.x;
+  if (s >= hi) return;
+  if (meta[s].due == kDueMovePending) meta[s].due = 0;
+}
+
 // Positions lp+step .. lp+step+run-1 into rows len .. len+run-1 of every
 // head of every active slot (rows themselves are not touched).
 // Grid: (slots, L * Hkv).
@@ -286,6 +298,22 @@ hipError_t launch_export_positions(const Shape& sh, const SeqMeta& M, int slot, 
   else
     hipLaunchKernelGGL(export_positions_kernel<false>, grid, dim3(256), 0, s, M, slot, len,
                        sh.pg, pos, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_mark_pending(SeqMeta* meta, int slot_lo, int slot_hi, hipStream_t s) {
+  if (slot_hi <= slot_lo) return hipSuccess;
+  const int n = slot_hi - slot_lo;
+  hipLaunchKernelGGL(mark_pending_kernel, dim3((n + 255) / 256), dim3(256), 0, s, meta,
+                     slot_lo, slot_hi);
+  return hipGetLastError();
+}
+
+hipError_t launch_clear_pending(SeqMeta* meta, int slot_lo, int slot_hi, hipStream_t s) {
+  if (slot_hi <= slot_lo) return hipSuccess;
+  const int n = slot_hi - slot_lo;
+  hipLaunchKernelGGL(clear_pending_kernel, dim3((n + 255) / 256), dim3(256), 0, s, meta,
+                     slot_lo, slot_hi);
   return hipGetLastError();
 }
 

@@ -106,4 +106,52 @@ def test_traffic_summary_parses_counter_csvs(tmp_path, monkeypatch):
     assert written["fetch_bytes_per_launch"] == 100.0 * 1024 * 2.0
     assert written["write_bytes_per_launch"] == 2.0 * 1024
     assert written["evict_full_event"] == {"fetch_bytes": 50.0 * 2048, "write_bytes": 40.0 * 1024}
+    assert written["evict_deferred_event"] is None
     assert written["run"]["steps"] == steps and written["run"]["warmup"] == 1
+
+
+def test_traffic_summary_deferred_event(tmp_path, monkeypatch):
+    """An event whose moves ride on the next step's attention: the summary
+    samples the plain launches of the timed steps (not the move launches),
+    takes the last positions-only eviction (the fast forward's come first)
+    as the selection, and reports the move launches' bytes above as many
+    plain launches."""
+    sys.path.insert(0, ROOT)
+    import bench
+    cols = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"]
+
+    def write(d, counter, rows):
+        d.mkdir()
+        with open(d / "run_counter_collection.csv", "w") as f:
+            f.write(",".join(cols) + "\n")
+            for i, (name, v) in enumerate(rows):
+                f.write('%d,"%s",%s,%s\n' % (i + 1, name, counter, v))
+
+    steps, L = 2, bench.WORKLOADS["qwen3-14b"]["L"]
+    attn = "void ra::attn_bf16_kernel<12, 1, false>(ra::AttnLaunch, ra::Paging, int)"
+    mv = "void ra::(anonymous namespace)::attn_bf16_move_kernel<8>(ra::AttnLaunch, int)"
+    sel = "void ra::evict_kernel<1024, 9, unsigned short, true, 0>(ra::SeqMeta const*)"
+    ff = [(sel, 7.0)] * 3                             # fast forward: not the event
+    write(tmp_path / "f", "FETCH_SIZE", ff + [(attn, 999.0)] * L + [(attn, 100.0)] * L +
+          [(sel, 5.0)] + [(mv, 150.0)] * L)
+    write(tmp_path / "w", "WRITE_SIZE", ff + [(attn, 9.0)] * L + [(attn, 2.0)] * L +
+          [(sel, 4.0)] + [(mv, 80.0)] * L)
+    write(tmp_path / "cf", "FETCH_SIZE", [("copy_kernel", 524288.0)] * 3)
+    write(tmp_path / "cw", "WRITE_SIZE", [("copy_kernel", 1048576.0)] * 3)
+    written = {}
+    monkeypatch.setattr(bench.json, "dump", lambda obj, f, **kw: written.update(obj))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda read=None: "0" * 16)
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    (tmp_path / "profiles").mkdir()
+    args = bench.build_parser().parse_args(
+        ["--steps", str(steps), "--warmup", "1", "--traffic-summary",
+         str(tmp_path / "f"), str(tmp_path / "w"), str(tmp_path / "cf"), str(tmp_path / "cw")])
+    bench.traffic_summary(args)
+    assert written["launches_sampled"] == L
+    assert written["fetch_bytes_per_launch"] == 100.0 * 2048
+    assert written["evict_full_event"] is None
+    d = written["evict_deferred_event"]
+    assert d["select_fetch_bytes"] == 5.0 * 2048 and d["select_write_bytes"] == 4.0 * 1024
+    assert d["move_attention_launches"] == L
+    assert d["moves_fetch_bytes"] == L * 50.0 * 2048
+    assert d["moves_write_bytes"] == L * 78.0 * 1024
