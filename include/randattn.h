@@ -324,8 +324,10 @@ ra_status ra_decode_attention_noalloc(ra_cache* cache, int32_t layer, const void
  * it reads them (the kept sets are final at once; the rows are final after
  * the next step, or as soon as a call that reads or writes rows, or plans
  * another event, moves them first).
- * Requires every layer to have been appended this step.  If n_evicted is
- * non-NULL it receives the number of sequences evicted (host mirror). */
+ * Requires every layer to have been appended this step (RA_ERR_STATE
+ * otherwise; with no active sequence, a step with no layer appended ends as
+ * a no-op).  If n_evicted is non-NULL it receives the number of sequences
+ * evicted (host mirror). */
 ra_status ra_end_step(ra_cache* cache, void* stream, int32_t* n_evicted);
 
 /* Run one eviction event on slot `seq` now, whatever the step count, if
@@ -348,11 +350,14 @@ ra_status ra_evict_now(ra_cache* cache, int32_t seq, void* stream);
  * to reach a long-generation state quickly; follow with ra_write_rows.
  * RA_ERR_STATE inside an open step; RA_ERR_CAPACITY, before any launch, if
  * some sequence would outgrow its region on the way (only possible under
- * RA_POLICY_EXTERNAL, whose rows are evicted by explicit rounds only). */
+ * RA_POLICY_EXTERNAL, whose rows are evicted by explicit rounds only) or, in
+ * the paged layout, if the pool has too few free page groups for the rows
+ * the sequences hold on the way. */
 ra_status ra_fast_forward(ra_cache* cache, int32_t n_steps, void* stream);
 
 /* Copy slot `seq`'s cached positions, [L][Hkv][len] int32 row-major, to
- * device memory (dev_out holds at least L*Hkv*len int32). */
+ * device memory (dev_out holds at least L*Hkv*len int32; RA_ERR_CAPACITY,
+ * nothing copied, if out_elems is smaller). */
 ra_status ra_export_positions(ra_cache* cache, int32_t seq, int32_t* dev_out,
                               int64_t out_elems, void* stream);
 

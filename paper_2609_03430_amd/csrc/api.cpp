@@ -697,6 +697,9 @@ ra_status ra_end_step(ra_cache* c, void* stream, int32_t* n_evicted) {
   if (!c) return RA_ERR_INVALID_ARG;
   if (n_evicted) *n_evicted = 0;
   bool any_active = c->slot_hi > c->slot_lo;
+  // a step is open once a layer is appended and must append every layer;
+  // with no active sequence, ending a step nothing was appended to is a no-op
+  if (c->n_appended != 0 && c->n_appended != c->cfg.num_layers) return RA_ERR_STATE;
   if (any_active && c->n_appended != c->cfg.num_layers) return RA_ERR_STATE;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   std::fill(c->appended.begin(), c->appended.end(), 0);
