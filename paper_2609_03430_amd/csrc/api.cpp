@@ -94,6 +94,12 @@ bool defers_moves(const ra_config& c) {
          c.policy != RA_POLICY_EXTERNAL;
 }
 
+// Split arrival counters of the bf16 attention, one per (slot, KV head).
+size_t arrivals_bytes(const ra_config& c) {
+  return static_cast<size_t>(
+      round_up(static_cast<int64_t>(sizeof(int32_t)) * c.max_seqs * c.num_kv_heads, 256));
+}
+
 size_t drops_bytes(const ra_config& c) {
   if (!defers_moves(c)) return 0;
   return static_cast<size_t>(round_up(static_cast<int64_t>(sizeof(int32_t)) * c.max_seqs *
@@ -125,6 +131,7 @@ struct ra_cache {
   std::vector<std::vector<int32_t>> groups;   // per slot: its table, in order
   // deferred row moves (see ra_end_step)
   int32_t* drops = nullptr;              // drop lists of the last events
+  int32_t* arrivals = nullptr;           // split arrival counters (bf16 attention)
   void* scratch = nullptr;               // device address of the no-alloc partials
 
   ra::Shape shape() const {
@@ -339,6 +346,7 @@ ra_status launch_decode(ra_cache* c, int32_t layer, const void* q, const void* k
   a.max_seqs = c->slot_hi;
   a.split_keys = plan.split_keys;
   a.max_splits = plan.max_splits;
+  a.arrivals = c->arrivals;
   a.waves = plan.waves;
   a.wide_regs = plan.wide_regs;
   if (move) {
@@ -443,7 +451,7 @@ int64_t ra_required_slots(const ra_config* c, const int32_t* prompt_lens, int32_
 
 size_t ra_meta_bytes(const ra_config* c) {
   if (ra_config_check(c) != RA_OK) return 0;
-  return meta_records_bytes(*c) + tables_bytes(*c) + drops_bytes(*c);
+  return meta_records_bytes(*c) + tables_bytes(*c) + drops_bytes(*c) + arrivals_bytes(*c);
 }
 
 size_t ra_workspace_bytes(const ra_config* c) {
@@ -502,6 +510,8 @@ ra_status ra_cache_create(const ra_config* cfg, void* k_pool, void* v_pool,
   if (defers_moves(*cfg))
     c->drops = reinterpret_cast<int32_t*>(static_cast<char*>(meta) + meta_records_bytes(*cfg) +
                                           tables_bytes(*cfg));
+  c->arrivals = reinterpret_cast<int32_t*>(static_cast<char*>(meta) + meta_records_bytes(*cfg) +
+                                           tables_bytes(*cfg) + drops_bytes(*cfg));
   const hipError_t e = ra::launch_zero_words(static_cast<uint32_t*>(meta),
                                              static_cast<int64_t>(ra_meta_bytes(cfg) / 4),
                                              static_cast<hipStream_t>(stream));

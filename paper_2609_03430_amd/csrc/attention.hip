@@ -127,17 +127,18 @@ __device__ __forceinline__ void append_row(const Work& w, const SeqMeta* meta,
   if (lane == 0) pos[row] = meta[w.slot].prompt_len + meta[w.slot].step;
 }
 
-// Merge the split partials of one (sequence, KV head) into the output.  One
-// workgroup per head, launched after the attention kernel (the kernel
-// boundary makes every partial visible; no device-scope fences are needed in
-// the streaming kernel).  Partial layout:
+// Merge the split partials of one (sequence, KV head) into the output: the
+// fp32 path (its kernel writes partials for every head) and the 12-wavefront
+// contiguous bf16 build (heads of one split write their output themselves).
+// One workgroup per head, launched after the attention kernel (the kernel
+// boundary makes every partial visible).  Partial layout:
 //   ws_o[((head * split_stride + split) * G + q) * 128 + c]  numerator / 2^m
 //   ws_ml[((head * split_stride + split) * G + q) * 2 + {0,1}] = (m, l)
 // with m the running max of the scores in log2 units and l the sum of
 // 2^(s - m) over the split's keys.
 template <typename E>
-__global__ __launch_bounds__(256) void combine_kernel(AttnLaunch a, int G, int Hq,
-                                                      int Hkv, bool skip_single) {
+__global__ __launch_bounds__(256) void combine_kernel(AttnLaunch a, int G, int Hq, int Hkv,
+                                                      bool skip_single) {
   __shared__ float sm[kMaxSplits * kMaxGroup];   // split maxima, then weights
   __shared__ float sl[kMaxSplits * kMaxGroup];   // split sums
   __shared__ float inv_l[kMaxGroup];
@@ -147,7 +148,6 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnLaunch a, int G, int H
   const int t = threadIdx.x;
   const int n_keys = M.len + 1;
   const int nsplit = (n_keys + a.split_keys - 1) / a.split_keys;
-  // a head with one split was written directly by the attention kernel
   if (skip_single && nsplit == 1) return;
   const int head = slot * Hkv + g;
   const float* ml = a.ws_ml + static_cast<int64_t>(head) * a.split_stride * G * 2;
@@ -188,6 +188,107 @@ __global__ __launch_bounds__(256) void combine_kernel(AttnLaunch a, int G, int H
       if constexpr (sizeof(E) == 2) out[orow + j] = f32_to_bf16(acc[j]);
       else out[orow + j] = acc[j];
     }
+  }
+}
+
+// Partials of a head merged inside the attention kernel travel through
+// device-coherent accesses (agent-scope relaxed atomics: stores written
+// through to the level the chip's dies share, loads served from it), so the
+// merge needs no whole-cache write-back or invalidation, which would stall
+// every workgroup still streaming on the same die.
+__device__ __forceinline__ void store_shared_level(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_shared_level(const float* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// The split partials of one head merged by the last of its splits to finish
+// (bf16 attention).  Every split stores its partials with store_shared_level
+// and waits until they are written; then one thread counts the split on the
+// head's arrival counter.  The split that brings the count to nsplit reads
+// every split's partials with load_shared_level, merges them as
+// combine_kernel does and resets the counter for the next launch.  Nothing
+// waits on another workgroup: the other splits simply end.  Called by every
+// thread of the workgroup after its partials are stored; the head and its
+// split count are taken afresh from the grid position and the slot record
+// (kept from before the key loop, they would take registers the loop needs).
+__device__ void merge_if_last(const AttnLaunch& a, int G, int Hq, int Hkv) {
+  __shared__ float sm[kMaxSplits * kMaxGroup];   // split maxima, then weights
+  __shared__ float sl[kMaxSplits * kMaxGroup];   // split sums
+  __shared__ float inv_l[kMaxGroup];
+  __shared__ int last;
+  const int slot = blockIdx.z, g = blockIdx.y, head = slot * Hkv + g;
+  const int nsplit = (a.meta[slot].len + 1 + a.split_keys - 1) / a.split_keys;
+  __builtin_amdgcn_s_waitcnt(0);     // this thread's partial stores are written
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const int prev = __hip_atomic_fetch_add(a.arrivals + head, 1, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT);
+    last = prev == nsplit - 1;
+    if (last)
+      __hip_atomic_store(a.arrivals + head, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!last) return;
+  const int t = threadIdx.x, nt = blockDim.x;
+  const float* ml = a.ws_ml + static_cast<int64_t>(head) * a.split_stride * G * 2;
+  const float* po = a.ws_o + static_cast<int64_t>(head) * a.split_stride * G * kHeadDim;
+  // up to four splits and two outputs per thread: the numerators are loaded
+  // together with the maxima and sums (one round trip to the shared level
+  // instead of two)
+  constexpr int kFastSplits = 4, kFastItems = 2;
+  const bool fast = nsplit <= kFastSplits && G * kHeadDim <= kFastItems * nt;
+  float pv[kFastItems][kFastSplits];
+  if (fast) {
+#pragma unroll
+    for (int j = 0; j < kFastItems; ++j) {
+      const int idx = t + j * nt;
+#pragma unroll
+      for (int s = 0; s < kFastSplits; ++s)
+        pv[j][s] = s < nsplit && idx < G * kHeadDim
+                       ? load_shared_level(po + (s * G) * kHeadDim + idx) : 0.f;
+    }
+  }
+  for (int i = t; i < nsplit * G; i += nt) {
+    sm[i] = load_shared_level(ml + 2 * i);
+    sl[i] = load_shared_level(ml + 2 * i + 1);
+  }
+  __syncthreads();
+  if (t < G) {
+    float mx = kNegInf;
+    for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, sm[s * G + t]);
+    float lsum = 0.f;
+    for (int s = 0; s < nsplit; ++s) {
+      const float wt = exp2f(sm[s * G + t] - mx);
+      sm[s * G + t] = wt;
+      lsum += wt * sl[s * G + t];
+    }
+    inv_l[t] = 1.f / lsum;
+  }
+  __syncthreads();
+  uint16_t* out = static_cast<uint16_t*>(a.out) +
+                  (static_cast<int64_t>(slot) * Hq + g * G) * kHeadDim;
+  if (fast) {
+#pragma unroll
+    for (int j = 0; j < kFastItems; ++j) {
+      const int idx = t + j * nt;
+      if (idx >= G * kHeadDim) break;
+      const int q = idx / kHeadDim;
+      float o = 0.f;
+#pragma unroll
+      for (int s = 0; s < kFastSplits; ++s)
+        if (s < nsplit) o += pv[j][s] * sm[s * G + q];
+      out[idx] = f32_to_bf16(o * inv_l[q]);
+    }
+    return;
+  }
+  for (int idx = t; idx < G * kHeadDim; idx += nt) {
+    const int q = idx / kHeadDim;
+    float o = 0.f;
+    for (int s = 0; s < nsplit; ++s)
+      o += load_shared_level(po + (s * G) * kHeadDim + idx) * sm[s * G + q];
+    out[idx] = f32_to_bf16(o * inv_l[q]);
   }
 }
 
@@ -314,6 +415,10 @@ template <int W, int MINW, bool PAGED>
 __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
     AttnLaunch a, Paging pg, int G, int Hq, int Hkv, float scale_log2) {
   constexpr int kNBuf = 2;   // register buffers (3 or 4 measured no faster)
+  // heads of several splits merged by their last split (merge_if_last); the
+  // contiguous 12-wavefront build has no registers to spare for it, and its
+  // multi-split heads are merged by combine_kernel
+  constexpr bool kFusedMerge = W != 12 || PAGED;
   __shared__ float s_m[W][kMaxGroup];
   __shared__ float s_l[W][kMaxGroup];
   __shared__ float s_o[W > 1 ? W : 1][kMaxGroup][kHeadDim];
@@ -466,10 +571,11 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
         float* po = a.ws_o + (item * G + qi) * kHeadDim;
 #pragma unroll
         for (int u = 0; u < 8; ++u)
-          *reinterpret_cast<f32x4*>(po + 16 * u + 4 * grp) = st.acc[u];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) store_shared_level(po + 16 * u + 4 * grp + i, st.acc[u][i]);
         if (grp == 0) {
-          a.ws_ml[(item * G + qi) * 2] = st.m;
-          a.ws_ml[(item * G + qi) * 2 + 1] = st.l;
+          store_shared_level(a.ws_ml + (item * G + qi) * 2, st.m);
+          store_shared_level(a.ws_ml + (item * G + qi) * 2 + 1, st.l);
         }
       }
     }
@@ -500,6 +606,12 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
       if (w.nsplit == 1) {
         out[(static_cast<int64_t>(w.slot) * Hq + w.g * G + q) * kHeadDim + c] =
             f32_to_bf16(o / lsum);
+      } else if constexpr (kFusedMerge) {
+        store_shared_level(a.ws_o + (item * G + q) * kHeadDim + c, o);
+        if (c == 0) {
+          store_shared_level(a.ws_ml + (item * G + q) * 2, mx);
+          store_shared_level(a.ws_ml + (item * G + q) * 2 + 1, lsum);
+        }
       } else {
         a.ws_o[(item * G + q) * kHeadDim + c] = o;
         if (c == 0) {
@@ -508,6 +620,9 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
         }
       }
     }
+  }
+  if constexpr (kFusedMerge) {
+    if (w.nsplit > 1) merge_if_last(a, G, Hq, Hkv);
   }
 }
 
@@ -961,9 +1076,11 @@ hipError_t launch_attention_t(const Shape& sh, const AttnLaunch& a, hipStream_t 
                          sh.G, sh.Hq, sh.Hkv, scale_log2);
     else
       return hipErrorInvalidConfiguration;
-    if (a.max_splits > 1)
-      hipLaunchKernelGGL(combine_kernel<uint16_t>, cgrid, dim3(256), 0, s, a, sh.G,
-                         sh.Hq, sh.Hkv, true);
+    // a head with several splits is merged by its last split (merge_if_last),
+    // except in the contiguous 12-wavefront build
+    if (a.max_splits > 1 && a.waves == 12 && !PAGED)
+      hipLaunchKernelGGL(combine_kernel<uint16_t>, cgrid, dim3(256), 0, s, a, sh.G, sh.Hq,
+                         sh.Hkv, true);
   } else {
     switch (sh.G) {
       case 1: launch_f32<1, PAGED>(grid, s, a, sh, scale_log2); break;
@@ -972,8 +1089,8 @@ hipError_t launch_attention_t(const Shape& sh, const AttnLaunch& a, hipStream_t 
       case 8: launch_f32<8, PAGED>(grid, s, a, sh, scale_log2); break;
       default: launch_f32<0, PAGED>(grid, s, a, sh, scale_log2); break;
     }
-    hipLaunchKernelGGL(combine_kernel<float>, cgrid, dim3(256), 0, s, a, sh.G,
-                       sh.Hq, sh.Hkv, false);
+    hipLaunchKernelGGL(combine_kernel<float>, cgrid, dim3(256), 0, s, a, sh.G, sh.Hq, sh.Hkv,
+                       false);
   }
   return hipGetLastError();
 }

@@ -168,6 +168,9 @@ struct AttnLaunch {
   int move;
   const int32_t* drops;  // the deferred drop lists (see launch_evict)
   int drop_stride;
+  // bf16: per (slot, KV head) count of the splits done this launch, zero
+  // between launches (the last split resets it after merging)
+  int* arrivals;
 };
 hipError_t launch_attention(const Shape& sh, const AttnLaunch& a, hipStream_t s);
 

@@ -76,7 +76,8 @@ def test_region_sizes():
 def test_paged_sizes():
     """Paged layout: a head's most rows round up to whole pages; the metadata
     buffer holds a block table of ceil((max prompt + K + r + R) / page_rows)
-    entries per slot; a prompt longer than the bound is refused."""
+    entries per slot (and the attention's split counters, one per slot and
+    KV head); a prompt longer than the bound is refused."""
     c = B.make_config(40, 40, 8, 8192, max_seqs=32, layout=B.RA_LAYOUT_PAGED,
                       page_rows=64, max_prompt_len=2048)
     assert B.ra_config_check(c) == B.RA_OK
@@ -86,7 +87,8 @@ def test_paged_sizes():
     assert B.ra_region_rows(c, 2049) == B.RA_ERR_CAPACITY
     pages = -(-(2048 + 8192 + 64 + 64) // 64)
     records = -(-(64 * 32) // 256) * 256
-    assert B.ra_meta_bytes(c) == records + -(-(4 * 32 * pages) // 256) * 256
+    arrivals = -(-(4 * 32 * 8) // 256) * 256           # split counters per (slot, KV head)
+    assert B.ra_meta_bytes(c) == records + -(-(4 * 32 * pages) // 256) * 256 + arrivals
     t = B.make_config(2, 4, 2, 300, budget_mode=B.RA_BUDGET_TOTAL, max_seqs=3,
                       layout=B.RA_LAYOUT_PAGED, page_rows=32, max_prompt_len=300)
     assert B.ra_region_rows(t, 100) == 448              # 300 + 64 + 64 = 428 -> 14 pages

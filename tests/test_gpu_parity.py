@@ -237,28 +237,43 @@ def test_evict_now_rejects_oversize_selection():
     cache.close()
 
 
-# (tag, KV heads, group, batch, K, wavefronts per item the plan must pick)
+# (tag, KV heads, group, batch, K, wavefronts per item the plan must pick,
+#  layout)
 PLAN_CASES = [
-    ("12 wavefronts, 1 split", 8, 2, 25, 7600, 12),
-    ("8 wavefronts, 2 splits", 8, 2, 16, 4000, 8),
-    ("4 wavefronts, 4 splits", 4, 2, 16, 2000, 4),
-    ("320 heads", 8, 2, 40, 600, 4),
-    ("800 heads", 8, 1, 100, 300, 4),
+    ("12 wavefronts, 1 split", 8, 2, 25, 7600, 12, B.RA_LAYOUT_CHRONOLOGICAL),
+    ("12 wavefronts, 2 splits", 8, 2, 16, 15400, 12, B.RA_LAYOUT_CHRONOLOGICAL),
+    ("12 wavefronts, 2 splits, paged", 8, 2, 16, 15400, 12, B.RA_LAYOUT_PAGED),
+    ("8 wavefronts, 2 splits", 8, 2, 16, 4000, 8, B.RA_LAYOUT_CHRONOLOGICAL),
+    ("8 wavefronts, 2 splits, paged", 8, 2, 16, 4000, 8, B.RA_LAYOUT_PAGED),
+    ("4 wavefronts, 4 splits", 4, 2, 16, 2000, 4, B.RA_LAYOUT_CHRONOLOGICAL),
+    ("320 heads", 8, 2, 40, 600, 4, B.RA_LAYOUT_CHRONOLOGICAL),
+    ("800 heads", 8, 1, 100, 300, 4, B.RA_LAYOUT_CHRONOLOGICAL),
 ]
 
 
-@pytest.mark.parametrize("tag,Hkv,G,Bsz,K,waves", PLAN_CASES)
-def test_attention_plans(tag, Hkv, G, Bsz, K, waves):
+def _arrivals_zero(run):
+    """The split arrival counters (the tail of the metadata buffer, one int32
+    per slot and KV head, rounded up to 256 bytes) are zero between launches:
+    the last split of every head reset its counter."""
+    torch.cuda.synchronize()
+    n = -(-4 * run.max_seqs * run.Hkv // 256) * 256
+    return int(run.cache.meta[-n:].count_nonzero()) == 0
+
+
+@pytest.mark.parametrize("tag,Hkv,G,Bsz,K,waves,layout", PLAN_CASES)
+def test_attention_plans(tag, Hkv, G, Bsz, K, waves, layout):
     """Each branch of the attention launch plan, on a ragged batch (prompts
     and generated lengths differ per sequence): every query head of every
     sequence against the oracle for two steps, the second after the
-    sequences that were due have evicted."""
+    sequences that were due have evicted.  Heads of several splits are merged
+    by their last split (or, in the contiguous 12-wavefront build, by the
+    merge kernel); the split counters are zero afterwards."""
     log("attention plan: %s" % tag)
     rng = np.random.default_rng(Bsz * 31 + K)
     lps = rng.integers(0, 300, Bsz).tolist()
     gens = sorted(rng.integers(K + 70, K + 700, Bsz).tolist(), reverse=True)
     run = Run(L=1, Hq=Hkv * G, Hkv=Hkv, K=K, lps=lps, r=64, every=64, begin=False,
-              write_prompt=False, wl_seed=77)
+              write_prompt=False, wl_seed=77, layout=layout, page_rows=64)
     for b in range(Bsz):
         run.begin(b)
         nxt = gens[b + 1] if b + 1 < Bsz else 0
@@ -283,6 +298,7 @@ def test_attention_plans(tag, Hkv, G, Bsz, K, waves):
                 err = attn_err(outs[0, b], o.attend(0, gens[b] + i), B.RA_BF16, (tag, i, b,))
                 worst = max(worst, err)
             o.rep.end_step()
+    assert _arrivals_zero(run)
     log("  worst %.3g" % worst)
     run.close()
 
@@ -328,6 +344,7 @@ def test_attention_shapes(dtype, Hq, Hkv, split):
                 checked += 1
             o.rep.end_step()
     assert checked == 7 * len(lps)
+    assert _arrivals_zero(run)
     run.close()
 
 
