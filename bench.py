@@ -817,6 +817,10 @@ def build_parser():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device-to-device copy three times (the "
                          "known-size reference for the HBM byte counters)")
+    ap.add_argument("--timeline-summary", metavar="TRACE_DIR",
+                    help="read a rocprofv3 --kernel-trace CSV of a run with the same "
+                         "--workload/--steps, and print per-layer attention, merge and "
+                         "gap durations over the timed launches")
     ap.add_argument("--traffic-summary", nargs=4,
                     metavar=("FETCH_DIR", "WRITE_DIR", "COPY_FETCH_DIR", "COPY_WRITE_DIR"),
                     help="CPU only: read the rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE "
@@ -842,6 +846,67 @@ def _counter_rows(d):
                 key = (int(row["Dispatch_Id"]), row["Kernel_Name"], row["Counter_Name"])
                 acc[key] = acc.get(key, 0.0) + float(row["Counter_Value"])
     return sorted((k[0], k[1], k[2], v) for k, v in acc.items())
+
+
+def _trace_rows(d):
+    """(start ns, end ns, kernel name) of the library's dispatches in a
+    rocprofv3 kernel-trace CSV under directory d, by start time."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*kernel_trace.csv"), recursive=True)
+    if not files:
+        raise SystemExit("no kernel_trace.csv under %s" % d)
+    rows = []
+    for path in files:
+        with open(path, newline="") as f:
+            for r in csv.DictReader(f):
+                if "ra::" in r["Kernel_Name"]:
+                    rows.append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]),
+                                 r["Kernel_Name"]))
+    return sorted(rows)
+
+
+def timeline_summary(args):
+    """Per-layer timeline of the timed launches of one bench run from its
+    kernel trace: the attention kernel, the gap to the split merge kernel (if
+    any), the merge, and the gap to the next layer's attention (launches
+    within one step; the step's end-of-step kernels come after its last
+    layer).  Steps whose attention moved a deferred event's rows
+    (attn_bf16_move_kernel) are reported apart."""
+    w = WORKLOADS[args.workload]
+    L = w["L"]
+    rows = _trace_rows(args.timeline_summary)
+    attn = [i for i, r in enumerate(rows)
+            if "attn_bf16_kernel" in r[2] or "attn_bf16_move_kernel" in r[2]]
+    timed = attn[-args.steps * L:]
+    acc = {"attention_us": [], "move_attention_us": [], "merge_us": [], "gap_to_merge_us": [],
+           "gap_to_next_layer_us": [], "layer_span_us": []}
+    for k, i in enumerate(timed):
+        s0, e, name = rows[i]
+        acc["move_attention_us" if "move" in name else "attention_us"].append((e - s0) / 1e3)
+        j = i + 1
+        if j < len(rows) and "combine" in rows[j][2]:
+            acc["gap_to_merge_us"].append((rows[j][0] - e) / 1e3)
+            acc["merge_us"].append((rows[j][1] - rows[j][0]) / 1e3)
+            e = rows[j][1]
+        if (k + 1) % L and k + 1 < len(timed):
+            nxt = rows[timed[k + 1]][0]
+            acc["gap_to_next_layer_us"].append((nxt - e) / 1e3)
+            if "move" not in name:
+                acc["layer_span_us"].append((nxt - s0) / 1e3)
+
+    def stat(v):
+        if not v:
+            return None
+        v = sorted(v)
+        return {"n": len(v), "mean": sum(v) / len(v), "p10": v[len(v) // 10],
+                "p50": v[len(v) // 2], "p90": v[(9 * len(v)) // 10]}
+
+    out = {k: stat(v) for k, v in acc.items()}
+    out["kernel"] = rows[timed[0]][2].split("(")[0]
+    out["workload"] = args.workload
+    out["launches"] = len(timed)
+    print(json.dumps(out))
 
 
 def traffic_summary(args):
@@ -925,6 +990,9 @@ def main():
 
     if args.traffic_summary:
         traffic_summary(args)
+        return
+    if args.timeline_summary:
+        timeline_summary(args)
         return
 
     import torch
@@ -1084,6 +1152,12 @@ def main():
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
     rec = run_steps(args.warmup, args.steps, True)
+    # an event at the last timed step left its row moves to the next step's
+    # attention: they are part of the timed work, done here (a fast forward
+    # of no steps moves them and does nothing else)
+    pending = any(B.ra_get_seq_info(h, b).move_pending for b in range(Bsz))
+    if pending:
+        B.ra_fast_forward(h, 0, stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     tokens = Bsz * args.steps
@@ -1158,6 +1232,9 @@ def main():
             "sequence_events": seq_events,
             "avg_ms_per_end_step_with_events": end_ms,
             "rows_moved_by_next_attention": any_deferred,
+            # the last timed step's event: its moves ran at the window's end
+            # (counted in the wall time, not in event_ms)
+            "last_event_moved_at_window_end": pending,
             "next_attention_extra_ms": post_extra if any_deferred else None,
             "event_ms": event_ms,
             "achieved_gbs": gbs,

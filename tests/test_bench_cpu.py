@@ -155,3 +155,40 @@ def test_traffic_summary_deferred_event(tmp_path, monkeypatch):
     assert d["move_attention_launches"] == L
     assert d["moves_fetch_bytes"] == L * 50.0 * 2048
     assert d["moves_write_bytes"] == L * 78.0 * 1024
+
+
+def test_timeline_summary_reads_kernel_trace(tmp_path, capsys):
+    """The timeline takes the last steps x layers attention dispatches of a
+    kernel trace and measures each one, the merge that follows it (if any)
+    and the gap to the next layer's attention within a step."""
+    sys.path.insert(0, ROOT)
+    import bench
+    L = bench.WORKLOADS["qwen3-4b"]["L"]
+    attn = "void ra::(anonymous namespace)::attn_bf16_kernel<8, 1, false>(ra::AttnLaunch)"
+    comb = "void ra::(anonymous namespace)::combine_kernel<unsigned short>(ra::AttnLaunch)"
+    adv = "ra::(anonymous namespace)::advance_kernel(ra::SeqMeta*, int)"
+    rows, t = [], 1000
+    for step in range(3):                       # one warm-up step, two timed
+        for l in range(L):
+            rows.append((attn, t, t + 90000))          # 90 us
+            rows.append((comb, t + 90010, t + 94810))  # 10 ns gap, 4.8 us
+            t += 94820                                  # 10 ns to the next layer
+        rows.append((adv, t, t + 3000))
+        t += 5000
+    d = tmp_path / "trace"
+    d.mkdir()
+    with open(d / "run_kernel_trace.csv", "w") as f:
+        f.write("Kernel_Name,Start_Timestamp,End_Timestamp\n")
+        for n, s, e in rows:
+            f.write('"%s",%d,%d\n' % (n, s, e))
+    args = bench.build_parser().parse_args(
+        ["--workload", "qwen3-4b", "--steps", "2", "--timeline-summary", str(d)])
+    bench.timeline_summary(args)
+    out = json.loads(capsys.readouterr().out)
+    assert out["launches"] == 2 * L
+    assert out["attention_us"]["n"] == 2 * L and abs(out["attention_us"]["mean"] - 90.0) < 1e-9
+    assert abs(out["merge_us"]["mean"] - 4.8) < 1e-9
+    assert abs(out["gap_to_merge_us"]["mean"] - 0.01) < 1e-9
+    assert out["gap_to_next_layer_us"]["n"] == 2 * (L - 1)
+    assert abs(out["layer_span_us"]["mean"] - 94.82) < 1e-9
+    assert out["move_attention_us"] is None
