@@ -903,7 +903,7 @@ def timeline_summary(args):
                 "p50": v[len(v) // 2], "p90": v[(9 * len(v)) // 10]}
 
     out = {k: stat(v) for k, v in acc.items()}
-    out["kernel"] = rows[timed[0]][2].split("(")[0]
+    out["kernel"] = rows[timed[0]][2].replace("(anonymous namespace)::", "").split("(")[0]
     out["workload"] = args.workload
     out["launches"] = len(timed)
     print(json.dumps(out))
