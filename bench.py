@@ -341,7 +341,7 @@ def tiny_cpu_baseline(lp, K, T, Hq, Hkv, seed, rid):
                       "numpy fp64" % T, "seconds": seconds}
 
 
-def tiny_latency(B, torch, Workload, with_cpu=True):
+def tiny_latency(B, torch, Workload, with_cpu=True, graph=False):
     """Per-step latency of the tiny case: 1 layer, 4 query / 2 KV heads,
     head_dim 128, fp32 N(0,1) rows, prompt 128, r=64, K=256, eviction every
     64 steps, 1024 decode steps from the pinned prompt (11 events).  A
@@ -367,18 +367,39 @@ def tiny_latency(B, torch, Workload, with_cpu=True):
         h = cache.handle
         B.ra_seq_begin(h, 0, lp, 1000 * 1000003, 0, kp, vp)
         torch.cuda.synchronize()
+
+        def issue(s):
+            n = 0
+            for t in range(T):
+                B.ra_decode_attention(h, 0, qs[t].unsqueeze(0), ks[t].unsqueeze(0),
+                                      vs[t].unsqueeze(0), out, cache.workspace, s)
+                n += B.ra_end_step(h, s)
+            return n
+
         e0 = torch.cuda.Event(enable_timing=True)
         e1 = torch.cuda.Event(enable_timing=True)
-        events = 0
+        if graph:
+            # the whole run as one graph: in graph mode every step's launches
+            # are independent of the host's state, so they can be recorded
+            # before any of them runs
+            B.ra_graph_mode(h, 1, stream)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                issue(None)
+            torch.cuda.synchronize()
         t0 = time.perf_counter()
         e0.record(stream)
-        for t in range(T):
-            B.ra_decode_attention(h, 0, qs[t].unsqueeze(0), ks[t].unsqueeze(0),
-                                  vs[t].unsqueeze(0), out, cache.workspace, stream)
-            events += B.ra_end_step(h, stream)
+        if graph:
+            g.replay()
+        else:
+            events = issue(stream)
         e1.record(stream)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
+        if graph:
+            B.ra_graph_mode(h, 0, stream)
+            events = B.ra_get_seq_info(h, 0).event
+            del g
         cache.close()
         result = {
             "metric": "tiny-case decode step latency (append + attention + end of step)",
@@ -386,6 +407,7 @@ def tiny_latency(B, torch, Workload, with_cpu=True):
                                    "K=256, r=64, evict every 64, 1024 steps from the prompt"},
             "steps": T,
             "events": events,
+            "graph": graph,
             "us_per_step_gpu": e0.elapsed_time(e1) * 1e3 / T,
             "us_per_step_wall": wall * 1e6 / T,
             "higher_is_better": False,
@@ -817,6 +839,11 @@ def build_parser():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a 1 GiB device-to-device copy three times (the "
                          "known-size reference for the HBM byte counters)")
+    ap.add_argument("--graph", action="store_true",
+                    help="capture the decode steps into HIP graphs (ra_graph_mode) and "
+                         "replay them: one graph of the layers' attention and one of the "
+                         "end of the step per input-ring slot, or with --tiny the whole "
+                         "run as one graph; events then move their rows themselves")
     ap.add_argument("--timeline-summary", metavar="TRACE_DIR",
                     help="read a rocprofv3 --kernel-trace CSV of a run with the same "
                          "--workload/--steps, and print per-layer attention, merge and "
@@ -1027,7 +1054,8 @@ def main():
         return
 
     if args.tiny:
-        print(json.dumps(tiny_latency(B, torch, Workload, not args.no_cpu_baseline)), flush=True)
+        print(json.dumps(tiny_latency(B, torch, Workload, not args.no_cpu_baseline, args.graph)),
+              flush=True)
         return
 
     w = WORKLOADS[args.workload]
@@ -1112,24 +1140,35 @@ def main():
     log("inputs ready; attention split %d keys x %d, %d wavefronts per item"
         % (split_keys, max_splits, waves))
 
-    def run_steps(first, n, timed):
+    def run_steps(first, n, timed, graphs=None, track=None):
         # HIP events bracket each step's L attention launches (one pair per
         # step: an event between every launch would add its own gap to the
-        # timed region) and each end-of-step call
+        # timed region) and each end-of-step call.  With graphs, the step
+        # replays the two graphs of its input-ring slot, and `track` follows
+        # the lengths and events the device produces (the library's mirror
+        # stays that of the entry into graph mode).
         rec = []
         for i in range(first, first + n):
             if timed and (i - first) % (2048 if n > 4096 else 64) == 0:
                 log("step %d of %d enqueued" % (i - first, n))
             j = i % RING
-            lens = [B.ra_get_seq_info(h, b).len for b in range(Bsz)] if timed else None
+            if not timed:
+                lens = None
+            elif track is not None:
+                lens = [t["len"] for t in track]
+            else:
+                lens = [B.ra_get_seq_info(h, b).len for b in range(Bsz)]
             evs = []
             if timed:
                 e0 = torch.cuda.Event(enable_timing=True)
                 e1 = torch.cuda.Event(enable_timing=True)
                 e0.record(stream)
-            for l in range(L):
-                B.ra_decode_attention(h, l, q_ring[j, l], k_ring[j, l], v_ring[j, l], out,
-                                      cache.workspace, stream)
+            if graphs is not None:
+                graphs[j][0].replay()
+            else:
+                for l in range(L):
+                    B.ra_decode_attention(h, l, q_ring[j, l], k_ring[j, l], v_ring[j, l], out,
+                                          cache.workspace, stream)
             if timed:
                 e1.record(stream)
                 evs.append((e0, e1))
@@ -1137,8 +1176,21 @@ def main():
                 x0 = torch.cuda.Event(enable_timing=True)
                 x1 = torch.cuda.Event(enable_timing=True)
                 x0.record(stream)
-            nev = B.ra_end_step(h, stream)
-            deferred = nev > 0 and any(B.ra_get_seq_info(h, b).move_pending for b in range(Bsz))
+            if graphs is not None:
+                graphs[j][1].replay()
+                nev = 0
+                for t in track:          # the end-of-step rule (trigger, then plan)
+                    t["step"] += 1
+                    t["len"] += 1
+                    if t["step"] % EVERY == 0 and t["len"] - t["lp"] - R > t["k_keep"]:
+                        t["len"] = t["lp"] + t["k_keep"] + R
+                        t["event"] += 1
+                        nev += 1
+                deferred = False
+            else:
+                nev = B.ra_end_step(h, stream)
+                deferred = nev > 0 and any(B.ra_get_seq_info(h, b).move_pending
+                                           for b in range(Bsz))
             if timed:
                 x1.record(stream)
                 rec.append((lens, evs, (x0, x1), nev, deferred))
@@ -1149,9 +1201,32 @@ def main():
 
     run_steps(0, args.warmup, False)
     post0 = last_event[0]    # the first timed step follows an event
+    graphs = track = None
+    if args.graph:
+        B.ra_graph_mode(h, 1, stream)
+        split_keys, max_splits, waves = B.ra_attention_plan(h)
+        torch.cuda.synchronize()
+        graphs = []
+        for j in range(RING):
+            ga, ge = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+            with torch.cuda.graph(ga):
+                for l in range(L):
+                    B.ra_decode_attention(h, l, q_ring[j, l], k_ring[j, l], v_ring[j, l], out,
+                                          cache.workspace)
+            with torch.cuda.graph(ge):
+                B.ra_end_step(h)
+            graphs.append((ga, ge))
+        track = []
+        for b in range(Bsz):
+            info = B.ra_get_seq_info(h, b)
+            track.append({"lp": lps[b], "k_keep": info.k_keep, "len": info.len,
+                          "step": info.step, "event": info.event})
+        torch.cuda.synchronize()
+        log("captured %d + %d graphs; attention split %d keys x %d, %d wavefronts per item"
+            % (RING, RING, split_keys, max_splits, waves))
     torch.cuda.synchronize()
     wall0 = time.perf_counter()
-    rec = run_steps(args.warmup, args.steps, True)
+    rec = run_steps(args.warmup, args.steps, True, graphs, track)
     # an event at the last timed step left its row moves to the next step's
     # attention: they are part of the timed work, done here (a fast forward
     # of no steps moves them and does nothing else)
@@ -1161,6 +1236,13 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     tokens = Bsz * args.steps
+    if args.graph:
+        B.ra_graph_mode(h, 0, stream)
+        for b in range(Bsz):
+            info = B.ra_get_seq_info(h, b)
+            assert (info.len, info.step, info.event) == (
+                track[b]["len"], track[b]["step"], track[b]["event"]), (b, info.len, track[b])
+        del graphs
     for b in range(Bsz):
         assert B.ra_get_seq_info(h, b).step == starts[b] + total
 
@@ -1299,6 +1381,7 @@ def main():
             "attn_split_keys": split_keys,
             "attn_splits": max_splits,
             "attn_waves_per_item": waves,
+            "graph": bool(args.graph),
         },
         "roofline": {
             "bound": "hbm",

@@ -334,6 +334,27 @@ ra_status ra_decode_attention_noalloc(ra_cache* cache, int32_t layer, const void
  * evicted (host mirror). */
 ra_status ra_end_step(ra_cache* cache, void* stream, int32_t* n_evicted);
 
+/* For callers that capture decode steps into HIP graphs (a step's
+ * ra_decode_attention calls for every layer and its ra_end_step, captured
+ * once and replayed at every step).  on = 1 enters graph mode: the attention
+ * plan is fixed for every state the active sequences can reach (their caches
+ * never outgrow their regions), and ra_end_step launches the step's advance
+ * and the eviction of every active head unconditionally; each eviction
+ * workgroup reads on the device whether its sequence is due, so the launches
+ * of a step depend on no host state and a captured step replays correctly at
+ * any later step.  The host mirror is not advanced in graph mode:
+ * ra_get_seq_info reports the state at entry, ra_end_step's n_evicted
+ * receives 0, and calls that need the mirror (ra_seq_begin, ra_seq_end,
+ * ra_evict_now, ra_fast_forward, row and position reads and writes, the
+ * measurement-only calls) return RA_ERR_STATE.  Events do not defer their
+ * row moves in graph mode (rows pending from an earlier event are moved at
+ * entry).  on = 0 leaves graph mode: the stream is synchronised and the
+ * device's per-slot records become the mirror again.  RA_ERR_STATE inside
+ * an open step; RA_ERR_UNSUPPORTED for the paged layout (page groups are
+ * handed out by the host) and RA_POLICY_EXTERNAL.  Entering or leaving a
+ * second time is a no-op. */
+ra_status ra_graph_mode(ra_cache* cache, int32_t on, void* stream);
+
 /* Run one eviction event on slot `seq` now, whatever the step count, if
  * its evictable rows exceed k_keep (otherwise a no-op).  The event is the
  * one of Eq. 1 with Section 3's scores (i.i.d. uniform per candidate, the

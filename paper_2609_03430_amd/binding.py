@@ -42,7 +42,7 @@ EXPORTS = (
     "ra_workspace_bytes", "ra_cache_create", "ra_cache_destroy",
     "ra_pool_info", "ra_seq_begin", "ra_seq_end", "ra_get_seq_info", "ra_decode_attention",
     "ra_decode_attention_noalloc",
-    "ra_end_step", "ra_evict_now", "ra_fast_forward", "ra_export_positions",
+    "ra_end_step", "ra_graph_mode", "ra_evict_now", "ra_fast_forward", "ra_export_positions",
     "ra_write_rows", "ra_read_rows", "ra_read_positions", "ra_status_string",
     "ra_last_hip_error", "ra_attention_plan", "ra_window_select",
     "ra_scored_scratch_bytes", "ra_scored_evict",
@@ -109,6 +109,7 @@ _SIGS = {
     "ra_decode_attention": (_I32, [_P, _I32, _P, _P, _P, _P, _P, _SZ, _P]),
     "ra_decode_attention_noalloc": (_I32, [_P, _I32, _P, _P, _P, _P, _P]),
     "ra_end_step": (_I32, [_P, _P, ctypes.POINTER(_I32)]),
+    "ra_graph_mode": (_I32, [_P, _I32, _P]),
     "ra_evict_now": (_I32, [_P, _I32, _P]),
     "ra_fast_forward": (_I32, [_P, _I32, _P]),
     "ra_export_positions": (_I32, [_P, _I32, _P, _I64, _P]),
@@ -342,6 +343,10 @@ def ra_end_step(handle, stream=None):
     _check(_lib().ra_end_step(handle, _stream(stream), ctypes.byref(n)),
            "ra_end_step")
     return n.value
+
+
+def ra_graph_mode(handle, on, stream=None):
+    _check(_lib().ra_graph_mode(handle, 1 if on else 0, _stream(stream)), "ra_graph_mode")
 
 
 def ra_evict_now(handle, seq, stream=None):

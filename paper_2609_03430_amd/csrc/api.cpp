@@ -132,6 +132,10 @@ struct ra_cache {
   // deferred row moves (see ra_end_step)
   int32_t* drops = nullptr;              // drop lists of the last events
   int32_t* arrivals = nullptr;           // split arrival counters (bf16 attention)
+  // graph mode (see ra_graph_mode): launches that depend on no host state
+  bool graph = false;
+  int graph_split_keys = 0, graph_max_splits = 0, graph_waves = 0, graph_wide_regs = 0;
+  int graph_candidates = 0;              // bound on any event's candidate slots
   void* scratch = nullptr;               // device address of the no-alloc partials
 
   ra::Shape shape() const {
@@ -228,16 +232,9 @@ struct Plan {
   int split_keys, max_splits, waves, wide_regs;
 };
 
-Plan attention_plan(const ra_cache* c) {
-  // sized by the longest cache of this step (cached rows + the new one), so
-  // that while sequences are younger than their budget no wavefront or split
-  // is planned over rows that do not exist yet
-  int keys_max = 32, n_active = 0;
-  for (int s = c->slot_lo; s < c->slot_hi; ++s) {
-    if (!c->mirror[s].active) continue;
-    keys_max = std::max(keys_max, c->mirror[s].len + 1);
-    ++n_active;
-  }
+// The plan for `n_active` sequences whose longest cache, the new row
+// included, has keys_max keys.
+Plan plan_for(const ra_cache* c, int keys_max, int n_active) {
   const int heads = std::max(1, n_active * c->cfg.num_kv_heads);
   Plan p{0, 0, 1, 0};
   int splits = 1;
@@ -264,6 +261,21 @@ Plan attention_plan(const ra_cache* c) {
   p.split_keys = sk;
   p.max_splits = (keys_max + sk - 1) / sk;
   return p;
+}
+
+Plan attention_plan(const ra_cache* c) {
+  if (c->graph)
+    return Plan{c->graph_split_keys, c->graph_max_splits, c->graph_waves, c->graph_wide_regs};
+  // sized by the longest cache of this step (cached rows + the new one), so
+  // that while sequences are younger than their budget no wavefront or split
+  // is planned over rows that do not exist yet
+  int keys_max = 32, n_active = 0;
+  for (int s = c->slot_lo; s < c->slot_hi; ++s) {
+    if (!c->mirror[s].active) continue;
+    keys_max = std::max(keys_max, c->mirror[s].len + 1);
+    ++n_active;
+  }
+  return plan_for(c, keys_max, n_active);
 }
 
 // Host checks shared by both attention entry points; nothing is launched.
@@ -580,6 +592,7 @@ ra_status ra_seq_begin(ra_cache* c, int32_t seq, int32_t prompt_len, uint64_t se
   if (!c || seq < 0 || seq >= c->cfg.max_seqs || prompt_len < 0 ||
       (dev_k_prompt == nullptr) != (dev_v_prompt == nullptr))
     return RA_ERR_INVALID_ARG;
+  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (c->step_open()) return RA_ERR_STATE;
   if (c->mirror[seq].active) return RA_ERR_STATE;
   const int64_t cap = ra_region_rows(&c->cfg, prompt_len);
@@ -638,6 +651,7 @@ ra_status ra_seq_begin(ra_cache* c, int32_t seq, int32_t prompt_len, uint64_t se
 
 ra_status ra_seq_end(ra_cache* c, int32_t seq, void* stream) {
   if (!c || seq < 0 || seq >= c->cfg.max_seqs) return RA_ERR_INVALID_ARG;
+  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (c->step_open()) return RA_ERR_STATE;
   SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
@@ -717,6 +731,13 @@ ra_status ra_end_step(ra_cache* c, void* stream, int32_t* n_evicted) {
   if (!any_active) return RA_OK;
   RA_LAUNCH(ra::launch_advance(c->meta, c->slot_lo, c->slot_hi, 1, c->cfg.recent_r,
                                trigger_every(c->cfg), s));
+  if (c->graph) {
+    // every head's workgroup reads on the device whether its sequence is
+    // due; the mirror stays that of the entry into graph mode
+    RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos, c->slot_lo,
+                               c->slot_hi, c->graph_candidates, false, s));
+    return RA_OK;
+  }
   int due = 0;
   for (int i = c->slot_lo; i < c->slot_hi; ++i) {
     SeqMeta& M = c->mirror[i];
@@ -753,8 +774,54 @@ ra_status ra_end_step(ra_cache* c, void* stream, int32_t* n_evicted) {
   return RA_OK;
 }
 
+ra_status ra_graph_mode(ra_cache* c, int32_t on, void* stream) {
+  if (!c || (on != 0 && on != 1)) return RA_ERR_INVALID_ARG;
+  if (c->step_open()) return RA_ERR_STATE;
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (on) {
+    if (c->graph) return RA_OK;
+    // page groups are handed out by the host as rows grow, and rows piling
+    // up under the external policy need the host's capacity checks
+    if (c->is_paged() || c->cfg.policy == RA_POLICY_EXTERNAL) return RA_ERR_UNSUPPORTED;
+    int cap_max = 32, n_active = 0, candidates = 0;
+    for (int i = c->slot_lo; i < c->slot_hi; ++i) {
+      const SeqMeta& M = c->mirror[i];
+      if (!M.active) continue;
+      cap_max = std::max(cap_max, M.cap);      // no cache outgrows its region
+      candidates = std::max(candidates, M.cap - M.prompt_len);
+      ++n_active;
+    }
+    if (candidates > ra::kMaxCandidates) return RA_ERR_UNSUPPORTED;
+    const ra_status fl = flush_pending(c, s);
+    if (fl != RA_OK) return fl;
+    const Plan p = plan_for(c, cap_max, n_active);
+    c->graph_split_keys = p.split_keys;
+    c->graph_max_splits = p.max_splits;
+    c->graph_waves = p.waves;
+    c->graph_wide_regs = p.wide_regs;
+    c->graph_candidates = candidates;
+    c->graph = true;
+    return RA_OK;
+  }
+  if (!c->graph) return RA_OK;
+  // the records the device advanced become the mirror again
+  std::vector<SeqMeta> dev(c->cfg.max_seqs);
+  RA_LAUNCH(hipMemcpyAsync(dev.data(), c->meta, sizeof(SeqMeta) * dev.size(),
+                           hipMemcpyDeviceToHost, s));
+  RA_LAUNCH(hipStreamSynchronize(s));
+  for (int i = c->slot_lo; i < c->slot_hi; ++i) {
+    if (!c->mirror[i].active) continue;
+    if (!dev[i].active || dev[i].base != c->mirror[i].base || dev[i].cap != c->mirror[i].cap)
+      return RA_ERR_STATE;
+    c->mirror[i] = dev[i];
+  }
+  c->graph = false;
+  return RA_OK;
+}
+
 ra_status ra_evict_now(ra_cache* c, int32_t seq, void* stream) {
   if (!c || seq < 0 || seq >= c->cfg.max_seqs) return RA_ERR_INVALID_ARG;
+  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (c->step_open()) return RA_ERR_STATE;
   SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
@@ -782,6 +849,7 @@ ra_status ra_evict_now(ra_cache* c, int32_t seq, void* stream) {
 
 ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
   if (!c || n_steps < 0) return RA_ERR_INVALID_ARG;
+  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (c->step_open()) return RA_ERR_STATE;
   const hipStream_t s = static_cast<hipStream_t>(stream);
   const int every = c->cfg.evict_every;
@@ -863,6 +931,7 @@ ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
 ra_status ra_export_positions(ra_cache* c, int32_t seq, int32_t* dev_out,
                               int64_t out_elems, void* stream) {
   if (!c || seq < 0 || seq >= c->cfg.max_seqs || !dev_out) return RA_ERR_INVALID_ARG;
+  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (c->step_open()) return RA_ERR_STATE;
   const SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
@@ -876,6 +945,7 @@ ra_status ra_export_positions(ra_cache* c, int32_t seq, int32_t* dev_out,
 ra_status ra_write_rows(ra_cache* c, int32_t seq, const void* dev_k, const void* dev_v,
                         void* stream) {
   if (!c || seq < 0 || seq >= c->cfg.max_seqs || !dev_k || !dev_v) return RA_ERR_INVALID_ARG;
+  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (c->step_open()) return RA_ERR_STATE;
   const SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
@@ -892,6 +962,7 @@ ra_status ra_read_rows(ra_cache* c, int32_t seq, int32_t layer, int32_t kv_head,
   if (!c || seq < 0 || seq >= c->cfg.max_seqs || layer < 0 ||
       layer >= c->cfg.num_layers || kv_head < 0 || kv_head >= c->cfg.num_kv_heads)
     return RA_ERR_INVALID_ARG;
+  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (c->step_open()) return RA_ERR_STATE;
   const SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
@@ -908,6 +979,7 @@ ra_status ra_window_select(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
                            int32_t scores_stride, int32_t* dev_drops, void* stream) {
   if (!c || seq_lo < 0 || seq_hi > c->cfg.max_seqs || seq_lo >= seq_hi || !dev_q_window)
     return RA_ERR_INVALID_ARG;
+  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (c->cfg.dtype != RA_BF16 || c->cfg.layout != RA_LAYOUT_CHRONOLOGICAL)
     return RA_ERR_UNSUPPORTED;
   if (c->step_open()) return RA_ERR_STATE;
@@ -946,6 +1018,7 @@ ra_status ra_scored_evict(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
   if (!c || !prm || seq_lo < 0 || seq_hi > c->cfg.max_seqs || seq_lo >= seq_hi ||
       !dev_q_window || !dev_scratch)
     return RA_ERR_INVALID_ARG;
+  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (prm->scorer < RA_SCORER_SNAPKV || prm->scorer > RA_SCORER_VASE)
     return RA_ERR_INVALID_ARG;
   if (c->cfg.dtype != RA_BF16 || c->cfg.layout != RA_LAYOUT_CHRONOLOGICAL)
@@ -1011,6 +1084,7 @@ ra_status ra_read_positions(ra_cache* c, int32_t seq, int32_t layer, int32_t kv_
       layer >= c->cfg.num_layers || kv_head < 0 || kv_head >= c->cfg.num_kv_heads ||
       !host_out || !n_out)
     return RA_ERR_INVALID_ARG;
+  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (c->step_open()) return RA_ERR_STATE;
   const SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
