@@ -697,8 +697,12 @@ __device__ __forceinline__ void patch_block_tail(BlockRegs& b, const uint16_t* n
 // own round or of an earlier one, which was read before that barrier, and
 // no round reads a row that an earlier round wrote; the next round's loads,
 // issued before the barrier, read only rows above every destination of the
-// round.  The new pair is stored at len after the last round.  Sequences
-// with nothing to move take the same path without moves.
+// round, except that loads of blocks past the last key, and of tail rows
+// past the cached ones, read the region's row 0 (which a round may be
+// writing when the prompt is empty): those values are never used, being
+// replaced by the new pair or zero, or belonging to no block.  The new pair
+// is stored at len after the last round.  Sequences with nothing to move
+// take the same path without moves.
 template <int W>
 __global__ __launch_bounds__(64 * W, 1) void attn_bf16_move_kernel(
     AttnLaunch a, int L, int G, int Hq, int Hkv, float scale_log2) {

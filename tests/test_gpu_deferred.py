@@ -155,3 +155,33 @@ def test_calls_between_event_and_next_step_move_rows_first():
         _step(run, list(oracles.values()), t)
     check_heads(run, list(oracles.values()))
     run.close()
+
+
+@pytest.mark.parametrize("K,lps", [(1500, [3, 50, 211]), (3000, [0, 1, 33])])
+def test_moves_across_many_rounds(K, lps):
+    """Caches of 1.6k-3.2k rows, so the moving attention works through 7-13
+    rounds of 256 rows and destination value tiles shared by neighbouring
+    rounds: after each of two events the rows are the oracle's once the next
+    step has run, and every output is within tolerance."""
+    log("deferred moves over many rounds K=%d" % K)
+    run = Run(L=2, Hq=8, Hkv=2, K=K, lps=lps, r=64, every=64, attn_split=ONE_SPLIT)
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    t0 = 64 * ((K + 128) // 64 + 1) - 3          # three steps before an event
+    run.fast_forward(t0)
+    for o in oracles:
+        o.advance(t0)
+    for s in range(run.n):
+        run.materialise(s)
+    assert B.ra_attention_plan(run.h)[1] == 1
+    events = 0
+    for t in range(3 + 64 + 2):
+        ev = _step(run, oracles, t)
+        if ev:
+            events += 1
+            assert all(_pending(run))
+        elif t > 0 and t in (3, 3 + 64):
+            assert not any(_pending(run))
+            check_heads(run, oracles)                 # moved by the attention
+    assert events == 2
+    check_heads(run, oracles)
+    run.close()
