@@ -1250,6 +1250,7 @@ def main():
     s_el = 2
     attn_ms, attn_bytes = [], []
     ev_ms, ev_bytes = [], []
+    ev_work = []             # per event: the bytes a separate compaction moves
     n_events = 0
     seq_events = 0
     C = K + EVERY                      # candidates at every event of these workloads
@@ -1292,6 +1293,7 @@ def main():
             seq_events += nev
             ev_ms.append(x0.elapsed_time(x1))
             ev_bytes.append((per_head_deferred if deferred else per_head) * nev * L * Hkv)
+            ev_work.append(per_head * nev * L * Hkv)
     # a deferred event's rows move in the next step's attention: its cost is
     # the end-of-step time plus that step's extra attention time
     plain = [ms for ms, p in zip(attn_ms, post) if not p]
@@ -1323,6 +1325,13 @@ def main():
             "peak_gbs": PEAK_HBM_GBS,
             "frac": gbs / PEAK_HBM_GBS,
             "bytes_per_event": sum(ev_bytes) / len(ev_bytes),
+            # the event's work priced as a separate compaction (its rows read
+            # and written): the rate at which that work completes, comparable
+            # across events that move their rows themselves and events whose
+            # moves ride on the next attention
+            "separate_compaction_bytes_per_event": sum(ev_work) / len(ev_work),
+            "separate_compaction_equivalent_gbs":
+                sum(ev_work) / len(ev_work) / (event_ms * 1e-3) / 1e9,
             "bytes_note": "per (sequence, layer, KV head) event: expected rows moved by "
                           "the order-preserving shift (from the first drop to the end) x "
                           "(key + value + position), read and written (written only, when "
