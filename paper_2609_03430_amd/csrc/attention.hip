@@ -73,10 +73,6 @@ __device__ __forceinline__ u32x4 ld16_stream(const void* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
 
-__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
-  return __uint_as_float(static_cast<uint32_t>(h) << 16);
-}
-
 __device__ __forceinline__ uint16_t f32_to_bf16(float x) {
   __bf16 b = static_cast<__bf16>(x);   // round to nearest even
   uint16_t h;
