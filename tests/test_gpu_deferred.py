@@ -185,3 +185,25 @@ def test_moves_across_many_rounds(K, lps):
     assert events == 2
     check_heads(run, oracles)
     run.close()
+
+
+@pytest.mark.parametrize("r,every", [(0, 8), (0, 1), (8, 1)])
+def test_moves_with_no_buffer_or_every_step(r, every):
+    """No buffer of recent pairs (the newest rows are candidates too), and an
+    event at every step (each step's attention moves the previous event's
+    rows while the step's own event defers the next moves): rows and sets
+    the oracle's, outputs within tolerance, throughout."""
+    log("deferred moves r=%d every=%d" % (r, every))
+    run = Run(L=2, Hq=8, Hkv=2, K=30, lps=[4, 0, 13], r=r, every=every, attn_split=ONE_SPLIT)
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    events = 0
+    for t in range(90):
+        ev = _step(run, oracles, t)
+        events += bool(ev)
+        if ev:
+            assert all(_pending(run))
+        if t % 17 == 16:
+            check_heads(run, oracles)                 # reading rows moves them first
+    assert events >= (6 if every > 1 else 50)     # from step ~31 on
+    check_heads(run, oracles)
+    run.close()
