@@ -3,8 +3,8 @@
 // Drives one cache through a random sequence of calls of the C ABI: sequences
 // begin and end, decode steps (every layer, then the end of the step, with
 // the allocation-free entry point now and then), explicit events, fast
-// forwards, row and position reads and writes, and calls that break the
-// protocol or pass bad arguments.  The device side is the stand-ins of
+// forwards, row and position reads and writes, entering and leaving graph
+// mode, and calls that break the protocol or pass bad arguments.  The device side is the stand-ins of
 // stub_launchers.cpp, so this runs on the CPU, under AddressSanitizer and
 // UndefinedBehaviorSanitizer.  After every call it prints one JSON line: the
 // call, its status and every slot's host mirror (active, len, step, event,
@@ -186,6 +186,7 @@ int main(int argc, char** argv) {
     }
   }
 
+  int in_graph = 0;
   for (int op = 0; op < n_ops; ++op) {
     int kind = rnd(100);
     if (lockstep && kind < 21 && rnd(8)) kind = 21 + rnd(45);   // mostly steps instead
@@ -273,6 +274,11 @@ int main(int argc, char** argv) {
       const int st2 = ra_export_positions(g_c, s, ex.data(), elems, nullptr);
       std::snprintf(args, sizeof args, "%d,%lld", s, static_cast<long long>(elems));
       print_state("write", args, st, st2);
+    } else if (kind < 91) {                            // enter or leave graph mode
+      const int st = ra_graph_mode(g_c, !in_graph, nullptr);
+      std::snprintf(args, sizeof args, "%d", !in_graph);
+      if (st == RA_OK) in_graph = !in_graph;
+      print_state("graph", args, st, 0);
     } else {                                           // bad arguments
       ra_seq_info i;
       const int e1 = ra_get_seq_info(g_c, c.max_seqs, &i);

@@ -14,7 +14,11 @@
 //     (block tables), and touches the caller's row buffers at the lengths the
 //     library passes;
 //   * hipMemcpyAsync copies (host to host), so position reads are checked
-//     against the position pool and the caller's output.
+//     against the position pool and the caller's output;
+//   * the end-of-step and plan launches advance the slot records as the
+//     device does (the trigger and plan rule restated below), so that the
+//     records read back when graph mode ends are the ones the GPU would
+//     hold.
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
@@ -46,6 +50,19 @@ std::vector<char>& scratch_array() {
 }
 
 size_t elem_bytes(const ra::Shape& sh) { return sh.dtype == 1 ? 2 : 4; }
+
+// The plan rule of an end-of-step trigger: a due sequence drops to
+// prompt + k_keep + r rows and counts an event.
+void plan(ra::SeqMeta& M, int r, bool at_trigger) {
+  M.due = 0;
+  if (at_trigger && M.len - M.prompt_len - r > M.k_keep) {
+    M.due = 1;
+    M.plan_len = M.len;
+    M.plan_event = M.event;
+    M.len = M.prompt_len + M.k_keep + r;
+    M.event += 1;
+  }
+}
 
 // Rows [0, len) of every head of slot `slot` lie in the pool.
 void check_rows(const ra::Shape& sh, const ra::SeqMeta& M, int slot, int len) {
@@ -130,15 +147,22 @@ hipError_t launch_seq_set(SeqMeta* meta, int slot, const SeqMeta& v, hipStream_t
   return hipSuccess;
 }
 
-hipError_t launch_advance(SeqMeta* meta, int slot_lo, int slot_hi, int, int, int, hipStream_t) {
+hipError_t launch_advance(SeqMeta* meta, int slot_lo, int slot_hi, int n_steps, int r, int every,
+                          hipStream_t) {
   if (slot_lo < 0 || slot_hi > g_max_seqs || slot_lo > slot_hi) fail("advance range", slot_lo, slot_hi);
-  touch_read(meta + slot_lo, sizeof(SeqMeta) * (slot_hi - slot_lo));
+  for (int s = slot_lo; s < slot_hi; ++s) {
+    SeqMeta& M = meta[s];
+    if (!M.active) continue;
+    M.step += n_steps;
+    M.len += n_steps;
+    plan(M, r, every > 0 && M.step % every == 0);
+  }
   return hipSuccess;
 }
 
-hipError_t launch_plan_now(SeqMeta* meta, int slot, int, hipStream_t) {
+hipError_t launch_plan_now(SeqMeta* meta, int slot, int r, hipStream_t) {
   if (slot < 0 || slot >= g_max_seqs) fail("plan_now slot", slot, g_max_seqs);
-  touch_read(meta + slot, sizeof(SeqMeta));
+  if (meta[slot].active) plan(meta[slot], r, true);
   return hipSuccess;
 }
 
@@ -161,13 +185,15 @@ hipError_t launch_evict(const Shape&, const SeqMeta* meta, void*, void*, int32_t
 
 hipError_t launch_mark_pending(SeqMeta* meta, int slot_lo, int slot_hi, hipStream_t) {
   if (slot_lo < 0 || slot_hi > g_max_seqs) fail("mark range", slot_lo, slot_hi);
-  touch_read(meta + slot_lo, sizeof(SeqMeta) * (slot_hi - slot_lo));
+  for (int s = slot_lo; s < slot_hi; ++s)
+    if (meta[s].active && meta[s].due == 1) meta[s].due = kDueMovePending;
   return hipSuccess;
 }
 
 hipError_t launch_clear_pending(SeqMeta* meta, int slot_lo, int slot_hi, hipStream_t) {
   if (slot_lo < 0 || slot_hi > g_max_seqs) fail("clear range", slot_lo, slot_hi);
-  touch_read(meta + slot_lo, sizeof(SeqMeta) * (slot_hi - slot_lo));
+  for (int s = slot_lo; s < slot_hi; ++s)
+    if (meta[s].due == kDueMovePending) meta[s].due = 0;
   return hipSuccess;
 }
 
@@ -175,8 +201,7 @@ hipError_t launch_flush_pending(const Shape&, SeqMeta* meta, void*, void*, const
                                 int drop_stride, int slot_lo, int slot_hi, hipStream_t) {
   if (slot_lo < 0 || slot_hi > g_max_seqs || !drops || drop_stride < 1)
     fail("flush", slot_lo, drop_stride);
-  touch_read(meta + slot_lo, sizeof(SeqMeta) * (slot_hi - slot_lo));
-  return hipSuccess;
+  return launch_clear_pending(meta, slot_lo, slot_hi, nullptr);   // as the device's does
 }
 
 hipError_t launch_write_rows(const Shape& sh, const SeqMeta& M, int slot, int len,

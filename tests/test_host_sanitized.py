@@ -6,17 +6,21 @@ allocators, the deferred-move bookkeeping) is built for the host alone with
 both sanitizers and linked with stand-ins for the device launches
 (tests/host_fuzz/stub_launchers.cpp: they keep the slot records and block
 tables in the caller's metadata buffer, check that every row a launch would
-touch lies in the pool, and copy positions for real).  The fuzzer
-(tests/host_fuzz/fuzz_protocol.cpp) makes random calls -- begins, ends,
-decode steps, explicit events, fast forwards, row and position reads and
-writes, calls inside an open step, bad arguments -- and prints every slot's
+touch lies in the pool, copy positions for real, and advance the slot
+records as the device does).  The fuzzer (tests/host_fuzz/fuzz_protocol.cpp)
+makes random calls -- begins, ends, decode steps, explicit events, fast
+forwards, row and position reads and writes, entering and leaving graph
+mode, calls inside an open step, bad arguments -- and prints every slot's
 mirror after each.  Here the same calls are replayed on the oracle's
 SequenceReplay (the length, step and event count of every sequence after
 every call, Eq. 1 with the periodic trigger), the statuses are checked
 against what the header promises, and the pool's accounting against the
 slots: regions disjoint inside the pool (contiguous layouts), ceil(len /
 page_rows) page groups per sequence between steps, no group in two tables
-(paged).  Any sanitizer report fails the run.
+(paged).  In graph mode the calls that need the host mirror must be refused
+and the mirror must stay that of the entry while the oracle advances; the
+records read back on leaving must be the oracle's again.  Any sanitizer
+report fails the run.
 """
 
 import json
@@ -85,6 +89,8 @@ class Replay:
          self.max_seqs, self.attn_split, self.layout, self.policy, self.block,
          self.page_rows, self.max_prompt_len, self.max_lp) = cfg
         self.reps = {}
+        self.graph = False
+        self.entry = None
 
     def begin(self, s, lp, seed, rid):
         pol = POLICY_RANDOM if self.policy == EXTERNAL else self.policy
@@ -153,7 +159,23 @@ def test_protocol_fuzz_matches_oracle(fuzzer, seed):
             break
         was_active = [x[0] for x in prev["s"]]
         between = True
-        if op == "begin":
+        refused_in_graph = rp.graph and op in ("begin", "end", "evict_now", "fast_forward",
+                                               "read", "write")
+        if refused_in_graph:
+            assert st == STATE, line
+            if op in ("read", "write"):
+                assert line["x"] == STATE, line
+        elif op == "graph":
+            if a[0] == 1:
+                if rp.layout == 2 or rp.policy == EXTERNAL:
+                    assert st == UNSUPPORTED, line
+                else:
+                    assert st == OK, line
+                    rp.graph, rp.entry = True, [list(x) for x in line["s"]]
+            else:
+                assert st == OK, line
+                rp.graph = False
+        elif op == "begin":
             s, lp = a[0], a[1]
             if was_active[s]:
                 assert st == STATE
@@ -172,9 +194,9 @@ def test_protocol_fuzz_matches_oracle(fuzzer, seed):
         elif op == "step":
             assert st == OK
             ev = rp.steps(1)
-            assert line["x"] == ev, (line, ev)
+            assert line["x"] == (0 if rp.graph else ev), (line, ev)
         elif op == "step_refused":
-            assert st == CAPACITY and a[0] == 0
+            assert st == CAPACITY and a[0] == 0 and not rp.graph
             assert [x[:6] for x in line["s"]] == [x[:6] for x in prev["s"]]
         elif op == "evict_now":
             s = a[0]
@@ -214,7 +236,11 @@ def test_protocol_fuzz_matches_oracle(fuzzer, seed):
             assert e4 in (INVALID, STATE)
             # a short workspace; a step the pool cannot hold is refused first
             assert e6 in (INVALID, CAPACITY)
-        _check_slots(rp, line)
+        if rp.graph:
+            # the mirror is the entry's until graph mode ends
+            assert [x[:6] + x[7:] for x in line["s"]] == [x[:6] + x[7:] for x in rp.entry], line
+        else:
+            _check_slots(rp, line)
         _check_pool(rp, line, pool_rows, between)
         # deferred row moves: set by an end-of-step event of every active
         # sequence at once; moved by any call that reads or writes rows or
