@@ -349,7 +349,9 @@ ra_status ra_end_step(ra_cache* cache, void* stream, int32_t* n_evicted);
  * measurement-only calls) return RA_ERR_STATE.  Events do not defer their
  * row moves in graph mode (rows pending from an earlier event are moved at
  * entry).  on = 0 leaves graph mode: the stream is synchronised and the
- * device's per-slot records become the mirror again.  RA_ERR_STATE inside
+ * device's per-slot records become the mirror again; graphs captured in
+ * graph mode are to be replayed only while it lasts (replayed later, they
+ * would advance the device past the mirror).  RA_ERR_STATE inside
  * an open step; RA_ERR_UNSUPPORTED for the paged layout (page groups are
  * handed out by the host) and RA_POLICY_EXTERNAL.  Entering or leaving a
  * second time is a no-op. */
