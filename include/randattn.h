@@ -220,7 +220,8 @@ int64_t ra_required_slots(const ra_config* cfg, const int32_t* host_prompt_lens,
  * paged layout the block tables, max_seqs * ceil((max_prompt_len + k_keep +
  * recent_r + evict_every) / page_rows) int32; in the bf16 chronological
  * layout the drop lists of deferred row moves, max_seqs * L * Hkv *
- * evict_every int32; the attention's split arrival counters, max_seqs * Hkv
+ * evict_every int32 (none, and no deferred moves, when that would exceed
+ * 256 MiB); the attention's split arrival counters, max_seqs * Hkv
  * int32 (zero between calls: one cache is driven from one stream).  0 on a
  * bad config. */
 size_t ra_meta_bytes(const ra_config* cfg);

@@ -88,10 +88,17 @@ size_t tables_bytes(const ra_config& c) {
 }
 
 // Events whose row moves the next step's attention can carry (bf16, the
-// contiguous chronological layout): their drop lists, evict_every per head.
+// contiguous chronological layout): their drop lists, evict_every per head,
+// kept in the metadata buffer.  Past 256 MiB of lists (far more slots,
+// layers or drops per event than any measured shape: the Qwen3-14B batch
+// needs 2.6 MB) the cache does not defer, rather than ask for that much.
+constexpr int64_t kMaxDropsBytes = int64_t(256) << 20;
+
 bool defers_moves(const ra_config& c) {
+  const int64_t lists = static_cast<int64_t>(sizeof(int32_t)) * c.max_seqs * c.num_layers *
+                        c.num_kv_heads * c.evict_every;
   return c.dtype == RA_BF16 && c.layout == RA_LAYOUT_CHRONOLOGICAL &&
-         c.policy != RA_POLICY_EXTERNAL;
+         c.policy != RA_POLICY_EXTERNAL && lists <= kMaxDropsBytes;
 }
 
 // Split arrival counters of the bf16 attention, one per (slot, KV head).

@@ -130,3 +130,21 @@ def test_null_handle_calls_fail_cleanly():
         == B.RA_ERR_INVALID_ARG
     for code in range(-6, 1):
         assert B.ra_status_string(code) != "unknown status"
+
+
+def test_meta_bytes_hold_drop_lists_up_to_a_cap():
+    """bf16 chronological caches keep a drop list of evict_every slots per
+    (slot, layer, KV head) for deferred row moves, unless the lists would
+    pass 256 MiB (then moves are not deferred and no lists are kept)."""
+    def records(n):
+        return -(-(64 * n) // 256) * 256
+
+    def arrivals(n, hkv):
+        return -(-(4 * n * hkv) // 256) * 256
+    c = B.make_config(40, 40, 8, 8192, max_seqs=32)
+    drops = 4 * 32 * 40 * 8 * 64
+    assert B.ra_meta_bytes(c) == records(32) + drops + arrivals(32, 8)
+    f = B.make_config(40, 40, 8, 8192, max_seqs=32, dtype=B.RA_F32)
+    assert B.ra_meta_bytes(f) == records(32) + arrivals(32, 8)
+    big = B.make_config(64, 64, 16, 8192, 64, 1024, max_seqs=65536)
+    assert B.ra_meta_bytes(big) == records(65536) + arrivals(65536, 16)
