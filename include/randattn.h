@@ -383,6 +383,21 @@ ra_status ra_evict_now(ra_cache* cache, int32_t seq, void* stream);
  * the sequences hold on the way. */
 ra_status ra_fast_forward(ra_cache* cache, int32_t n_steps, void* stream);
 
+/* ra_fast_forward for the one active slot `seq`: the other slots' records,
+ * positions and rows are left as they are (their deferred row moves stay
+ * pending unless `seq` has one too).  Use: resuming a preempted request
+ * inside a live batch (Appendix G: eviction under paging must stay correct
+ * across preemption).  Its kept positions depend only on its seed, request
+ * id and step, so ra_seq_begin with the same prompt length, seed and
+ * request id (prompt rows optional), ra_seq_fast_forward by the steps it
+ * had decoded, then ra_write_rows with its saved rows (ra_read_rows of
+ * every head before ra_seq_end) restore the state it had, in any free slot.
+ * Only periodic events are replayed: a request that had explicit events
+ * (ra_evict_now, ra_scored_evict) resumes in another state.  Errors as
+ * ra_fast_forward, and RA_ERR_STATE if the slot is not active. */
+ra_status ra_seq_fast_forward(ra_cache* cache, int32_t seq, int32_t n_steps,
+                              void* stream);
+
 /* Copy slot `seq`'s cached positions, [L][Hkv][len] int32 row-major, to
  * device memory (dev_out holds at least L*Hkv*len int32; RA_ERR_CAPACITY,
  * nothing copied, if out_elems is smaller). */

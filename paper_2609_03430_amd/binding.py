@@ -42,7 +42,8 @@ EXPORTS = (
     "ra_workspace_bytes", "ra_cache_create", "ra_cache_destroy",
     "ra_pool_info", "ra_seq_begin", "ra_seq_end", "ra_get_seq_info", "ra_decode_attention",
     "ra_decode_attention_noalloc",
-    "ra_end_step", "ra_graph_mode", "ra_evict_now", "ra_fast_forward", "ra_export_positions",
+    "ra_end_step", "ra_graph_mode", "ra_evict_now", "ra_fast_forward", "ra_seq_fast_forward",
+    "ra_export_positions",
     "ra_write_rows", "ra_read_rows", "ra_read_positions", "ra_status_string",
     "ra_last_hip_error", "ra_attention_plan", "ra_window_select",
     "ra_scored_scratch_bytes", "ra_scored_evict",
@@ -112,6 +113,7 @@ _SIGS = {
     "ra_graph_mode": (_I32, [_P, _I32, _P]),
     "ra_evict_now": (_I32, [_P, _I32, _P]),
     "ra_fast_forward": (_I32, [_P, _I32, _P]),
+    "ra_seq_fast_forward": (_I32, [_P, _I32, _I32, _P]),
     "ra_export_positions": (_I32, [_P, _I32, _P, _I64, _P]),
     "ra_write_rows": (_I32, [_P, _I32, _P, _P, _P]),
     "ra_read_rows": (_I32, [_P, _I32, _I32, _I32, _P, _P, _P]),
@@ -356,6 +358,11 @@ def ra_evict_now(handle, seq, stream=None):
 def ra_fast_forward(handle, n_steps, stream=None):
     _check(_lib().ra_fast_forward(handle, int(n_steps), _stream(stream)),
            "ra_fast_forward")
+
+
+def ra_seq_fast_forward(handle, seq, n_steps, stream=None):
+    _check(_lib().ra_seq_fast_forward(handle, int(seq), int(n_steps), _stream(stream)),
+           "ra_seq_fast_forward")
 
 
 def ra_export_positions(handle, seq, out, stream=None):

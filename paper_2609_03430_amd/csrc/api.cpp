@@ -854,14 +854,20 @@ ra_status ra_evict_now(ra_cache* c, int32_t seq, void* stream) {
   return RA_OK;
 }
 
-ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
-  if (!c || n_steps < 0) return RA_ERR_INVALID_ARG;
-  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
-  if (c->step_open()) return RA_ERR_STATE;
-  const hipStream_t s = static_cast<hipStream_t>(stream);
+namespace {
+
+// Positions-only advance of the active sequences of slots [lo, hi) by
+// n_steps (the whole active range for ra_fast_forward, one slot for
+// ra_seq_fast_forward); the other slots' records and rows are not touched
+// (their deferred moves, if any, stay pending).
+ra_status fast_forward_range(ra_cache* c, int lo, int hi, int32_t n_steps, hipStream_t s) {
   const int every = c->cfg.evict_every;
-  const ra_status fl = flush_pending(c, s);
-  if (fl != RA_OK) return fl;
+  bool pending = false;
+  for (int i = lo; i < hi; ++i) pending = pending || c->mirror[i].due == ra::kDueMovePending;
+  if (pending) {
+    const ra_status fl = flush_pending(c, s);
+    if (fl != RA_OK) return fl;
+  }
   // Runs of steps up to the next trigger of any sequence.  The first pass
   // replays them on a copy of the mirror only, so that a capacity error (rows
   // piling up under the external policy) is reported before any launch; the
@@ -878,15 +884,15 @@ ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
     const bool launch = pass == 1;
     if (launch) restore();
     int remaining = n_steps;
-    while (remaining > 0 && c->slot_hi > c->slot_lo) {
+    while (remaining > 0 && hi > lo) {
       int run = remaining;
-      for (int i = c->slot_lo; i < c->slot_hi; ++i)
+      for (int i = lo; i < hi; ++i)
         if (c->mirror[i].active) run = std::min(run, every - c->mirror[i].step % every);
       if (c->is_paged()) {
         // pages for the run's rows
         int64_t short_groups = 0;
         bool fits = true;
-        for (int i = c->slot_lo; i < c->slot_hi; ++i) {
+        for (int i = lo; i < hi; ++i) {
           if (!c->mirror[i].active) continue;
           fits = fits && c->fits_table(c->mirror[i].len + run);
           short_groups += c->groups_short(i, c->mirror[i].len + run);
@@ -896,12 +902,12 @@ ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
           return RA_ERR_CAPACITY;
         }
         std::vector<ra::TableEntry> te;
-        for (int i = c->slot_lo; i < c->slot_hi; ++i)
+        for (int i = lo; i < hi; ++i)
           if (c->mirror[i].active) c->grow(i, c->mirror[i].len + run, te);
         if (launch && !te.empty())
           RA_LAUNCH(ra::launch_table_set(c->shape(), te.data(), static_cast<int>(te.size()), s));
       } else {
-        for (int i = c->slot_lo; i < c->slot_hi; ++i) {
+        for (int i = lo; i < hi; ++i) {
           const SeqMeta& M = c->mirror[i];
           if (M.active && M.len + run > M.cap) {
             restore();
@@ -910,29 +916,47 @@ ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
         }
       }
       if (launch) {
-        RA_LAUNCH(ra::launch_append_positions(c->shape(), c->meta, c->pos, c->slot_lo,
-                                              c->slot_hi, run, s));
-        RA_LAUNCH(ra::launch_advance(c->meta, c->slot_lo, c->slot_hi, run, c->cfg.recent_r,
+        RA_LAUNCH(ra::launch_append_positions(c->shape(), c->meta, c->pos, lo, hi, run, s));
+        RA_LAUNCH(ra::launch_advance(c->meta, lo, hi, run, c->cfg.recent_r,
                                      trigger_every(c->cfg), s));
       }
-      int due = 0;
-      for (int i = c->slot_lo; i < c->slot_hi; ++i) {
+      int due = 0, candidates = 0;
+      for (int i = lo; i < hi; ++i) {
         SeqMeta& M = c->mirror[i];
         if (!M.active) continue;
         M.step += run;
         M.len += run;
         mirror_plan(M, c->cfg.recent_r, at_trigger(c->cfg, M.step));
         due += M.due;
+        if (M.due) candidates = std::max(candidates, c->span(M));
         if (M.due && c->is_paged()) c->shrink(i, M.len);
       }
       if (due && launch) {
-        RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos,
-                                   c->slot_lo, c->slot_hi, c->max_candidates_due(), true, s));
+        RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos, lo, hi,
+                                   candidates, true, s));
       }
       remaining -= run;
     }
   }
   return RA_OK;
+}
+
+}  // namespace
+
+ra_status ra_fast_forward(ra_cache* c, int32_t n_steps, void* stream) {
+  if (!c || n_steps < 0) return RA_ERR_INVALID_ARG;
+  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
+  if (c->step_open()) return RA_ERR_STATE;
+  return fast_forward_range(c, c->slot_lo, c->slot_hi, n_steps,
+                            static_cast<hipStream_t>(stream));
+}
+
+ra_status ra_seq_fast_forward(ra_cache* c, int32_t seq, int32_t n_steps, void* stream) {
+  if (!c || seq < 0 || seq >= c->cfg.max_seqs || n_steps < 0) return RA_ERR_INVALID_ARG;
+  if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
+  if (c->step_open()) return RA_ERR_STATE;
+  if (!c->mirror[seq].active) return RA_ERR_STATE;
+  return fast_forward_range(c, seq, seq + 1, n_steps, static_cast<hipStream_t>(stream));
 }
 
 ra_status ra_export_positions(ra_cache* c, int32_t seq, int32_t* dev_out,

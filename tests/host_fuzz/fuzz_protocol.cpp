@@ -3,7 +3,8 @@
 // Drives one cache through a random sequence of calls of the C ABI: sequences
 // begin and end, decode steps (every layer, then the end of the step, with
 // the allocation-free entry point now and then), explicit events, fast
-// forwards, row and position reads and writes, entering and leaving graph
+// forwards of every sequence or of one, a request preempted and resumed in a
+// free slot, row and position reads and writes, entering and leaving graph
 // mode, and calls that break the protocol or pass bad arguments.  The device side is the stand-ins of
 // stub_launchers.cpp, so this runs on the CPU, under AddressSanitizer and
 // UndefinedBehaviorSanitizer.  After every call it prints one JSON line: the
@@ -45,6 +46,12 @@ ra_config g_cfg;
 ra_cache* g_c = nullptr;
 int g_external = 0;
 
+struct Request {           // what began each slot
+  int lp;
+  uint64_t seed, rid;
+};
+std::vector<Request> g_req;
+
 void print_state(const char* op, const char* args, int status, int extra) {
   std::printf("{\"op\":\"%s\",\"a\":[%s],\"st\":%d,\"x\":%d,\"s\":[", op, args, status, extra);
   std::vector<int> active(g_cfg.max_seqs), caps(g_cfg.max_seqs);
@@ -71,6 +78,16 @@ int active_slot() {        // a random active slot, or -1
     if (i.active) a.push_back(s);
   }
   return a.empty() ? -1 : a[rnd(static_cast<int>(a.size()))];
+}
+
+int free_slot() {          // a free slot (searched from a random one), or -1
+  const int n = g_cfg.max_seqs, start = rnd(n);
+  for (int k = 0; k < n; ++k) {
+    ra_seq_info i;
+    ra_get_seq_info(g_c, (start + k) % n, &i);
+    if (!i.active) return (start + k) % n;
+  }
+  return -1;
 }
 
 int seq_len(int s) {
@@ -173,13 +190,15 @@ int main(int argc, char** argv) {
   Buf out(static_cast<size_t>(c.max_seqs) * Hq * 128 * esz);
   const size_t ws_bytes = ra_workspace_bytes(&c);
   Buf ws(ws_bytes);
-  char args[128];
+  char args[192];
+  g_req.assign(c.max_seqs, Request{0, 0, 0});
 
   if (lockstep) {
     for (int s = 0; s < c.max_seqs; ++s) {
       const int lp = rnd(max_prompt() + 1);
       const uint64_t seed = next_u64() >> 1, rid = next_u64() >> 1;
       const int st = ra_seq_begin(g_c, s, lp, seed, rid, nullptr, nullptr, nullptr);
+      if (st == RA_OK) g_req[s] = Request{lp, seed, rid};
       std::snprintf(args, sizeof args, "%d,%d,%llu,%llu", s, lp,
                     static_cast<unsigned long long>(seed), static_cast<unsigned long long>(rid));
       print_state("begin", args, st, 0);
@@ -200,6 +219,7 @@ int main(int argc, char** argv) {
       Buf vp(rows ? static_cast<size_t>(L) * Hkv * lp * 128 * esz : 0);
       const int st = ra_seq_begin(g_c, s, lp, seed, rid, rows ? kp.p() : nullptr,
                                   rows ? vp.p() : nullptr, nullptr);
+      if (st == RA_OK) g_req[s] = Request{lp, seed, rid};
       std::snprintf(args, sizeof args, "%d,%d,%llu,%llu", s, lp,
                     static_cast<unsigned long long>(seed), static_cast<unsigned long long>(rid));
       print_state("begin", args, st, 0);
@@ -246,11 +266,47 @@ int main(int argc, char** argv) {
       const int st = ra_evict_now(g_c, s, nullptr);
       std::snprintf(args, sizeof args, "%d", s);
       print_state("evict_now", args, st, 0);
-    } else if (kind < 77) {                            // fast forward
+    } else if (kind < 77) {                            // fast forward: all, or one slot
       const int n = rnd(3 * c.evict_every + 2);
-      const int st = ra_fast_forward(g_c, n, nullptr);
-      std::snprintf(args, sizeof args, "%d", n);
-      print_state("fast_forward", args, st, 0);
+      if (rnd(2)) {
+        const int st = ra_fast_forward(g_c, n, nullptr);
+        std::snprintf(args, sizeof args, "%d", n);
+        print_state("fast_forward", args, st, 0);
+      } else {
+        const int s = rnd(c.max_seqs);
+        const int st = ra_seq_fast_forward(g_c, s, n, nullptr);
+        std::snprintf(args, sizeof args, "%d,%d", s, n);
+        print_state("seq_fast_forward", args, st, 0);
+      }
+    } else if (kind < 80) {                            // preempt a request, resume it
+      const int s = active_slot();
+      if (s < 0) continue;
+      ra_seq_info was;
+      ra_get_seq_info(g_c, s, &was);
+      const Request q = g_req[s];
+      const size_t rows = static_cast<size_t>(L) * Hkv * was.len;
+      Buf ks(rows * 128 * esz), vs(rows * 128 * esz);
+      for (int lg = 0; lg < L * Hkv; ++lg)             // its rows, saved head by head
+        ra_read_rows(g_c, s, lg / Hkv, lg % Hkv,
+                     ks.b.data() + static_cast<size_t>(lg) * was.len * 128 * esz,
+                     vs.b.data() + static_cast<size_t>(lg) * was.len * 128 * esz, nullptr);
+      const int e1 = ra_seq_end(g_c, s, nullptr);
+      const int t = e1 == RA_OK ? free_slot() : s;
+      const int e2 = ra_seq_begin(g_c, t, q.lp, q.seed, q.rid, nullptr, nullptr, nullptr);
+      if (e2 == RA_OK) g_req[t] = q;
+      const int e3 = ra_seq_fast_forward(g_c, t, was.step, nullptr);
+      // the saved rows back (as many as the resumed head holds: explicit
+      // events of its past are not replayed, so it may hold more)
+      const size_t back = static_cast<size_t>(L) * Hkv * (e2 == RA_OK ? seq_len(t) : 0);
+      if (back > rows) {
+        ks.b.resize(back * 128 * esz);
+        vs.b.resize(back * 128 * esz);
+      }
+      const int e4 = ra_write_rows(g_c, t, ks.p(), vs.p(), nullptr);
+      std::snprintf(args, sizeof args, "%d,%d,%d,%llu,%llu,%d,%d,%d,%d,%d", s, t, q.lp,
+                    static_cast<unsigned long long>(q.seed),
+                    static_cast<unsigned long long>(q.rid), was.step, e1, e2, e3, e4);
+      print_state("resume", args, e4, 0);
     } else if (kind < 83) {                            // read rows / positions of one head
       const int s = active_slot();
       if (s < 0) continue;
@@ -283,7 +339,9 @@ int main(int argc, char** argv) {
       ra_seq_info i;
       const int e1 = ra_get_seq_info(g_c, c.max_seqs, &i);
       const int e2 = ra_evict_now(g_c, -1, nullptr);
-      const int e3 = ra_fast_forward(g_c, -1, nullptr);
+      const int e3 = rnd(3) == 0 ? ra_fast_forward(g_c, -1, nullptr)
+                     : rnd(2)    ? ra_seq_fast_forward(g_c, 0, -1, nullptr)
+                                 : ra_seq_fast_forward(g_c, c.max_seqs, 1, nullptr);
       const int e4 = ra_read_rows(g_c, 0, L, 0, nullptr, nullptr, nullptr);
       const int e5 = ra_decode_attention(g_c, L, q.p(), kn.p(), vn.p(), out.p(), ws.p(),
                                          ws_bytes, nullptr);

@@ -126,6 +126,7 @@ def test_null_handle_calls_fail_cleanly():
     assert lib.ra_cache_destroy(None) == B.RA_ERR_INVALID_ARG
     assert lib.ra_end_step(None, None, None) == B.RA_ERR_INVALID_ARG
     assert lib.ra_fast_forward(None, 1, None) == B.RA_ERR_INVALID_ARG
+    assert lib.ra_seq_fast_forward(None, 0, 1, None) == B.RA_ERR_INVALID_ARG
     assert lib.ra_decode_attention(None, 0, None, None, None, None, None, 0, None) \
         == B.RA_ERR_INVALID_ARG
     for code in range(-6, 1):

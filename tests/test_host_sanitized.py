@@ -9,8 +9,11 @@ tables in the caller's metadata buffer, check that every row a launch would
 touch lies in the pool, copy positions for real, and advance the slot
 records as the device does).  The fuzzer (tests/host_fuzz/fuzz_protocol.cpp)
 makes random calls -- begins, ends, decode steps, explicit events, fast
-forwards, row and position reads and writes, entering and leaving graph
-mode, calls inside an open step, bad arguments -- and prints every slot's
+forwards of every sequence or of one, a request preempted (its rows read,
+its slot ended) and resumed in a free slot (begun again, forwarded by its
+steps, its rows written back), row and position reads and writes, entering
+and leaving graph mode, calls inside an open step, bad arguments -- and
+prints every slot's
 mirror after each.  Here the same calls are replayed on the oracle's
 SequenceReplay (the length, step and event count of every sequence after
 every call, Eq. 1 with the periodic trigger), the statuses are checked
@@ -97,6 +100,18 @@ class Replay:
         self.reps[s] = SequenceReplay(lp, keep_count(self.K, lp, self.mode), self.r,
                                       self.every, seed, rid, [(0, 0)], pol, self.block)
 
+    def advance_one(self, s, n):
+        """n positions-only steps of the sequence in slot s."""
+        rep = self.reps[s]
+        if self.policy == EXTERNAL:
+            for _ in range(n):
+                rep.append()
+        elif n == 1:
+            rep.append()
+            rep.end_step()
+        else:
+            rep.advance(n)
+
     def steps(self, n):
         """n decode steps of every sequence; the number of sequences that
         evicted at the last one."""
@@ -160,11 +175,13 @@ def test_protocol_fuzz_matches_oracle(fuzzer, seed):
         was_active = [x[0] for x in prev["s"]]
         between = True
         refused_in_graph = rp.graph and op in ("begin", "end", "evict_now", "fast_forward",
-                                               "read", "write")
+                                               "seq_fast_forward", "read", "write", "resume")
         if refused_in_graph:
             assert st == STATE, line
             if op in ("read", "write"):
                 assert line["x"] == STATE, line
+            if op == "resume":
+                assert a[6:] == [STATE] * 4, line
         elif op == "graph":
             if a[0] == 1:
                 if rp.layout == 2 or rp.policy == EXTERNAL:
@@ -213,6 +230,33 @@ def test_protocol_fuzz_matches_oracle(fuzzer, seed):
             else:
                 assert st == OK
                 rp.steps(a[0])
+        elif op == "seq_fast_forward":
+            s, n = a
+            if not was_active[s]:
+                assert st == STATE, line
+            elif st == CAPACITY:                  # nothing done
+                assert rp.policy == EXTERNAL or rp.layout == 2
+                assert [x[:6] for x in line["s"]] == [x[:6] for x in prev["s"]]
+            else:
+                assert st == OK, line
+                rp.advance_one(s, n)
+        elif op == "resume":
+            # the request of slot s ended and begun again in slot t with the
+            # same prompt length, seed and request id, forwarded by its steps:
+            # the oracle's state of a fresh sequence advanced by those steps
+            # (the steps' periodic events; explicit events are not replayed)
+            s, t, lp, seed, rid, step, e1, e2, e3, e4 = a
+            assert e1 == OK and e2 == OK and e4 == OK and st == OK, line
+            assert t == s or not was_active[t], line
+            del rp.reps[s]
+            rp.begin(t, lp, seed, rid)
+            if e3 == CAPACITY:
+                # rows piling up (external policy), or the forwarded rows need
+                # more pages than the request held (explicit events shortened it)
+                assert rp.policy == EXTERNAL or rp.layout == 2, line
+            else:
+                assert e3 == OK, line
+                rp.advance_one(t, step)
         elif op == "read":
             s, layer, g, cap, n_out = a
             n = line["s"][s][1]
@@ -249,8 +293,14 @@ def test_protocol_fuzz_matches_oracle(fuzzer, seed):
         if op == "step" and any(pend):
             assert line["x"] > 0
             assert all(p == bool(x[0]) for p, x in zip(pend, line["s"])), line
-        elif op in ("read", "write") or (op in ("evict_now", "fast_forward") and st == OK):
+        elif op in ("read", "write", "resume") or (op in ("evict_now", "fast_forward")
+                                                   and st == OK):
             assert not any(pend), line
+        elif op == "seq_fast_forward" and st == OK and prev["s"][a[0]][6]:
+            assert not any(pend), line        # its own pending moves done first
+        elif op == "seq_fast_forward":
+            # another slot's pending moves are carried
+            assert [bool(x[6]) for x in prev["s"]] == pend, line
         else:
             assert all(not p or bool(q[6]) for p, q in zip(pend, prev["s"])), line
         assert all(not p or x[0] for p, x in zip(pend, line["s"]))
