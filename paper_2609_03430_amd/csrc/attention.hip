@@ -216,7 +216,10 @@ __device__ void merge_if_last(const AttnLaunch& a, int G, int Hq, int Hkv) {
   __shared__ int last;
   const int slot = blockIdx.z, g = blockIdx.y, head = slot * Hkv + g;
   const int nsplit = (a.meta[slot].len + 1 + a.split_keys - 1) / a.split_keys;
-  __builtin_amdgcn_s_waitcnt(0);     // this thread's partial stores are written
+  // This thread's partial stores are written before the workgroup counts
+  // itself: the wait is issued as an asm statement that clobbers memory, so
+  // the compiler cannot move the stores (relaxed atomics) past it either.
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
   if (threadIdx.x == 0) {
     const int prev = __hip_atomic_fetch_add(a.arrivals + head, 1, __ATOMIC_RELAXED,
