@@ -157,10 +157,10 @@ struct ra_cache {
     return false;
   }
   int64_t pages_for(int64_t rows) const { return (rows + page_rows - 1) / page_rows; }
-  // paged: page groups slot `s` must add to hold `rows` rows
   // paged: whether `rows` rows fit the block table of one sequence (rows
   // pile up past lp + k_keep + r + R only under the external policy)
   bool fits_table(int64_t rows) const { return pages_for(rows) <= pg.pages_per_seq; }
+  // paged: page groups slot `s` must add to hold `rows` rows
   int64_t groups_short(int s, int64_t rows) const {
     return std::max<int64_t>(0, pages_for(rows) - static_cast<int64_t>(groups[s].size()));
   }
@@ -619,10 +619,15 @@ ra_status ra_seq_begin(ra_cache* c, int32_t seq, int32_t prompt_len, uint64_t se
     std::vector<ra::TableEntry> te;
     c->grow(seq, prompt_len, te);
     M.cap = c->mirror[seq].cap;
-    RA_LAUNCH(ra::launch_table_set(c->shape(), te.data(), static_cast<int>(te.size()), s));
-    RA_LAUNCH(ra::launch_write_rows(c->shape(), M, seq, prompt_len, dev_k_prompt,
-                                    dev_v_prompt, nullptr, c->kpool, c->vpool, c->pos, s));
-    RA_LAUNCH(ra::launch_seq_set(c->meta, seq, M, s));
+    hipError_t e = ra::launch_table_set(c->shape(), te.data(), static_cast<int>(te.size()), s);
+    if (e == hipSuccess)
+      e = ra::launch_write_rows(c->shape(), M, seq, prompt_len, dev_k_prompt, dev_v_prompt,
+                                nullptr, c->kpool, c->vpool, c->pos, s);
+    if (e == hipSuccess) e = ra::launch_seq_set(c->meta, seq, M, s);
+    if (e != hipSuccess) {   // the slot stays inactive: its pages go back
+      c->shrink(seq, 0);
+      return hip_fail(e);
+    }
     c->mirror[seq] = M;
     c->update_range();
     return RA_OK;
