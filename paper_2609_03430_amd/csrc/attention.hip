@@ -380,14 +380,20 @@ __device__ __forceinline__ void compute_block(Softmax& st, const BlockRegs& b,
   bm = fmaxf(bm, __shfl_xor(bm, 16, 64));
   bm = fmaxf(bm, __shfl_xor(bm, 32, 64));
   const float mn = fmaxf(st.m, bm);
-  const float alpha = exp2f(st.m - mn);
+  // With MASKED, every key of a block can be masked while the state is still
+  // empty (a wavefront whose first rows were all dropped): the weights and
+  // the rescale are then taken against 0 instead of mn = -inf, which would
+  // make them NaN; they come out 0 and the state stays empty.  Unmasked
+  // blocks always hold a valid key.
+  const float mr = MASKED && mn == kNegInf ? 0.f : mn;
+  const float alpha = exp2f(st.m - mr);
   // P = hi + lo, both bf16, so the weights keep ~16 significant bits through
   // the bf16 MFMA (the remainder of a bf16 rounding is exact in fp32)
   bf16x8 p_hi, p_lo;
   float psum = 0.f;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    const float pf = exp2f(x[e] - mn);
+    const float pf = exp2f(x[e] - mr);
     const __bf16 hi = static_cast<__bf16>(pf);
     p_hi[e] = hi;
     p_lo[e] = static_cast<__bf16>(pf - static_cast<float>(hi));

@@ -207,3 +207,32 @@ def test_moves_with_no_buffer_or_every_step(r, every):
     assert events >= (6 if every > 1 else 50)     # from step ~31 on
     check_heads(run, oracles)
     run.close()
+
+
+@pytest.mark.parametrize("K,lps,mode,every", [
+    (35, [35, 7, 35], B.RA_BUDGET_TOTAL, 64),      # two of the heads keep no generated row
+    (0, [0, 5, 32], B.RA_BUDGET_EVICTABLE, 64),    # nothing kept; the first has no prompt
+    (2, [0, 33, 64], B.RA_BUDGET_EVICTABLE, 32),
+])
+def test_moves_when_whole_blocks_are_dropped(K, lps, mode, every):
+    """Events that drop whole 32-row blocks, so that a wavefront of the
+    moving attention sees only dropped rows in its first block (or in all of
+    its blocks): its softmax state must stay empty rather than turn NaN, and
+    the outputs, sets and rows stay the oracle's through every event."""
+    log("deferred moves, whole blocks dropped: K=%d lps=%s mode=%d every=%d" % (K, lps, mode,
+                                                                             every))
+    run = Run(L=2, Hq=8, Hkv=2, K=K, lps=lps, r=0, every=every, mode=mode,
+              attn_split=ONE_SPLIT)
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    events = 0
+    after_event = False
+    for t in range(3 * every + 8):
+        ev = _step(run, oracles, t)               # every output within tolerance
+        if after_event:
+            check_heads(run, oracles)
+        if ev:
+            events += 1
+            assert all(_pending(run))
+        after_event = bool(ev)
+    assert events >= 3
+    run.close()
