@@ -400,13 +400,13 @@ ra_status ra_seq_fast_forward(ra_cache* cache, int32_t seq, int32_t n_steps,
 
 /* Copy slot `seq`'s cached positions, [L][Hkv][len] int32 row-major, to
  * device memory (dev_out holds at least L*Hkv*len int32; RA_ERR_CAPACITY,
- * nothing copied, if out_elems is smaller). */
+ * nothing copied, if out_elems is smaller; NULL allowed when len is 0). */
 ra_status ra_export_positions(ra_cache* cache, int32_t seq, int32_t* dev_out,
                               int64_t out_elems, void* stream);
 
 /* Overwrite slot `seq`'s cached rows from row-major device arrays
  * [L][Hkv][len][d] (row j belongs to the j-th cached position, the order of
- * ra_export_positions). */
+ * ra_export_positions; NULL allowed when len is 0). */
 ra_status ra_write_rows(ra_cache* cache, int32_t seq, const void* dev_k,
                         const void* dev_v, void* stream);
 

@@ -966,11 +966,12 @@ ra_status ra_seq_fast_forward(ra_cache* c, int32_t seq, int32_t n_steps, void* s
 
 ra_status ra_export_positions(ra_cache* c, int32_t seq, int32_t* dev_out,
                               int64_t out_elems, void* stream) {
-  if (!c || seq < 0 || seq >= c->cfg.max_seqs || !dev_out) return RA_ERR_INVALID_ARG;
+  if (!c || seq < 0 || seq >= c->cfg.max_seqs) return RA_ERR_INVALID_ARG;
   if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (c->step_open()) return RA_ERR_STATE;
   const SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
+  if (!dev_out && M.len > 0) return RA_ERR_INVALID_ARG;   // nothing to copy: may be NULL
   if (out_elems < static_cast<int64_t>(M.len) * c->cfg.num_layers * c->cfg.num_kv_heads)
     return RA_ERR_CAPACITY;
   RA_LAUNCH(ra::launch_export_positions(c->shape(), M, seq, M.len, c->pos, dev_out,
@@ -980,11 +981,12 @@ ra_status ra_export_positions(ra_cache* c, int32_t seq, int32_t* dev_out,
 
 ra_status ra_write_rows(ra_cache* c, int32_t seq, const void* dev_k, const void* dev_v,
                         void* stream) {
-  if (!c || seq < 0 || seq >= c->cfg.max_seqs || !dev_k || !dev_v) return RA_ERR_INVALID_ARG;
+  if (!c || seq < 0 || seq >= c->cfg.max_seqs) return RA_ERR_INVALID_ARG;
   if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (c->step_open()) return RA_ERR_STATE;
   const SeqMeta& M = c->mirror[seq];
   if (!M.active) return RA_ERR_STATE;
+  if ((!dev_k || !dev_v) && M.len > 0) return RA_ERR_INVALID_ARG;   // NULL only if empty
   const ra_status fl = flush_pending(c, static_cast<hipStream_t>(stream));
   if (fl != RA_OK) return fl;
   // positions are left as they are: pass the region's own positions through
