@@ -100,13 +100,17 @@ class Run:
         v[: self.n] = vv
         return q, k, v
 
-    def step(self):
-        """One decode step of every sequence; returns out [L, max_seqs, Hq, d]."""
+    def step(self, noalloc=False):
+        """One decode step of every sequence (through the allocation-free entry
+        point if `noalloc`); returns out [L, max_seqs, Hq, d]."""
         outs = torch.empty(self.L, self.max_seqs, self.Hq, 128, dtype=self.tdtype,
                            device=DEV)
         for layer in range(self.L):
             q, k, v = self.step_inputs(layer)
-            self.cache.decode(layer, q, k, v, outs[layer])
+            if noalloc:
+                self.cache.decode_noalloc(layer, q, k, v, outs[layer])
+            else:
+                self.cache.decode(layer, q, k, v, outs[layer])
         evicted = B.ra_end_step(self.h)
         self.steps = [s + 1 for s in self.steps]
         return outs, evicted

@@ -3,7 +3,8 @@
 Each case draws a small configuration (layers, heads, group size, budget and
 budget mode, recent buffer, trigger period, dtype, all three layouts, the
 four end-of-step policies, slots, one or several work items per head) and
-then a random sequence of calls: decode steps (most of them), sequences
+then a random sequence of calls: decode steps (most of them; a quarter
+through the allocation-free entry point), sequences
 beginning and ending, explicit events, fast forwards of every sequence or
 of one, a request preempted (rows read, slot ended; the others may decode
 meanwhile) and resumed in a free slot, and graph mode entered (steps then run
@@ -93,7 +94,7 @@ class Fuzz:
     def step(self, oracles, ctx):
         """One decode step; False if the paged pool refused it (nothing done)."""
         try:
-            outs, ev = self.run.step()
+            outs, ev = self.run.step(noalloc=self.rng.integers(0, 4) == 0)
         except B.RandAttnError as e:
             assert e.status == B.RA_ERR_CAPACITY and self.layout == B.RA_LAYOUT_PAGED, e
             return False, 0
