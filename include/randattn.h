@@ -23,16 +23,18 @@
  * - The library never allocates device memory.  The caller owns the pools,
  *   the metadata buffer and the workspace and must keep them alive until
  *   ra_cache_destroy.  (The one fixed device array the library holds, that
- *   of ra_decode_attention_noalloc, comes with its code object.)  One ra_cache must be driven from one stream (calls
- *   are stream-ordered); it is not thread-safe.
+ *   of ra_decode_attention_noalloc, comes with its code object.)  One
+ *   ra_cache must be driven from one stream (calls are stream-ordered); it
+ *   is not thread-safe.
  * - Every call returns an ra_status.  Shapes, capacities, budgets and the
  *   step protocol are validated on the host mirror BEFORE any launch, so an
  *   error leaves device state untouched.  A failed launch returns
  *   RA_ERR_HIP (ra_last_hip_error gives the hipError_t); after RA_ERR_HIP
- *   from a call that launches several kernels (ra_seq_begin, ra_end_step,
- *   ra_evict_now, ra_fast_forward, ra_scored_evict) the host mirror and the
- *   device state may disagree, and the cache should be destroyed.  Nothing
- *   throws across the ABI.
+ *   from a call that launches several kernels (ra_seq_begin, a paged or
+ *   move-carrying ra_decode_attention, ra_end_step, ra_evict_now,
+ *   ra_fast_forward, ra_seq_fast_forward, ra_scored_evict) the host mirror
+ *   and the device state may disagree, and the cache should be destroyed.
+ *   Nothing throws across the ABI.
  * - head_dim must be 128; dtype f32 or bf16 (keys, values, queries and
  *   outputs all in that dtype); positions are int32.
  *
