@@ -33,12 +33,17 @@ T = 32768
 WINDOW = 72          # steps decoded on the GPU (events at 32704 and 32768)
 
 
-@pytest.mark.parametrize("name,layout", [(n, 0) for n in sorted(SHAPES)] +
-                         [("qwen3-14b", 1), ("qwen3-14b", 2)])
-def test_full_size(name, layout):
+@pytest.mark.parametrize("name,layout,graph", [(n, 0, False) for n in sorted(SHAPES)] +
+                         [("qwen3-14b", 1, False), ("qwen3-14b", 2, False),
+                          ("qwen3-14b", 0, True)])
+def test_full_size(name, layout, graph):
+    """`graph`: the window decoded in graph mode (the plan fixed from the
+    regions' capacity, every head's eviction launched at the end of every
+    step and decided on the device), as the per-step HIP graphs of bench.py
+    --graph run it."""
     L, Hq, Hkv, Bsz, lp, K, seed = SHAPES[name]
-    log("full size %s layout %d: L=%d Hq=%d Hkv=%d B=%d lp=%d K=%d"
-        % (name, layout, L, Hq, Hkv, Bsz, lp, K))
+    log("full size %s layout %d graph %d: L=%d Hq=%d Hkv=%d B=%d lp=%d K=%d"
+        % (name, layout, graph, L, Hq, Hkv, Bsz, lp, K))
     run = Run(L=L, Hq=Hq, Hkv=Hkv, K=K, lps=[lp] * Bsz, r=64, every=64,
               seeds=[seed * 1000003 + b for b in range(Bsz)], rids=list(range(Bsz)),
               wl_seed=seed, write_prompt=False, layout=layout, page_rows=64)
@@ -58,6 +63,8 @@ def test_full_size(name, layout):
     log("  oracle replay done")
     check_steps = {0, 8, 31, 32, 33, WINDOW - 1}   # 8: right after the event at step 32704
     worst = 0.0
+    if graph:
+        B.ra_graph_mode(run.h, 1)
     for i in range(WINDOW):
         outs, ev = run.step()
         for o in oracles.values():
@@ -71,6 +78,10 @@ def test_full_size(name, layout):
                 worst = max(worst, err)
         for o in oracles.values():
             o.rep.end_step()
+    if graph:
+        B.ra_graph_mode(run.h, 0)          # the device's records back into the mirror
+        info = B.ra_get_seq_info(run.h, 0)
+        assert (info.step, info.event) == (oracles[0].rep.step, oracles[0].rep.event)
     for b, l, g in sites:
         got = (run.sorted_positions(b, l, g) if layout == B.RA_LAYOUT_HOLE_FILL
                else run.positions(b, l, g))
