@@ -236,3 +236,42 @@ def test_moves_when_whole_blocks_are_dropped(K, lps, mode, every):
         after_event = bool(ev)
     assert events >= 3
     run.close()
+
+
+@pytest.mark.parametrize("layout,every,r,split", [
+    (B.RA_LAYOUT_CHRONOLOGICAL, 1024, 0, ONE_SPLIT),   # up to 1,024 drops per head, deferred
+    (B.RA_LAYOUT_CHRONOLOGICAL, 256, 64, 0),           # split heads: moved on their own first
+    (B.RA_LAYOUT_HOLE_FILL, 1024, 16, 0),
+    (B.RA_LAYOUT_PAGED, 512, 64, 0),
+])
+def test_large_trigger_periods(layout, every, r, split):
+    """Trigger periods up to the largest allowed (1,024 steps), so that an
+    event drops up to ~1,000 rows per head: the drop lists, the moving
+    attention's scan of them across many blocks, the hole-fill moves and the
+    paged rewrite at that size.  Outputs checked every eighth step and at
+    the step after each event, sets and rows after each event."""
+    log("large trigger period layout=%d every=%d r=%d split=%d" % (layout, every, r, split))
+    run = Run(L=1, Hq=8, Hkv=2, K=100, lps=[5, 40], r=r, every=every, layout=layout,
+              attn_split=split, page_rows=64)
+    oracles = [OracleSeq(run, s) for s in range(run.n)]
+    events, after = 0, False
+    for t in range(2 * every + 3):
+        outs, ev = run.step()
+        check = after or t % 8 == 0
+        if check:
+            outs = outs.float().cpu()
+        for o in oracles:
+            o.rep.append()
+            if check:
+                attn_err(outs[0, o.slot], o.attend(0, o.rep.step - 1), B.RA_BF16, (t, o.slot))
+            o.rep.end_step()
+        if after:
+            check_heads(run, oracles)
+        if ev:
+            events += 1
+            if split == ONE_SPLIT:
+                assert all(_pending(run))
+        after = bool(ev)
+    assert events == 2
+    check_heads(run, oracles)
+    run.close()
