@@ -86,7 +86,8 @@ typedef enum {
 typedef struct {
   int32_t num_layers;     /* L >= 1 */
   int32_t num_q_heads;    /* Hq, a multiple of Hkv */
-  int32_t num_kv_heads;   /* Hkv >= 1; group G = Hq / Hkv, G <= 16 */
+  int32_t num_kv_heads;   /* Hkv >= 1; group G = Hq / Hkv, G <= 16;
+                             L * Hkv <= 65536 (RA_ERR_UNSUPPORTED beyond) */
   int32_t head_dim;       /* d; must be 128 */
   int32_t budget_k;       /* K >= 0 (see budget_mode) */
   int32_t recent_r;       /* r >= 0: the buffer of most recent pairs (64) */
@@ -446,8 +447,9 @@ ra_status ra_read_positions(ra_cache* cache, int32_t seq, int32_t layer,
  * [seq_hi-seq_lo][L][Hkv][scores_stride] float, the un-pooled scores of rows
  * [0, len).  dev_drops (optional): [seq_hi-seq_lo][L][Hkv][evict_every]
  * int32, the dropped rows ascending.  The cache is not modified.  bf16 and
- * the chronological layout only (RA_ERR_UNSUPPORTED otherwise); RA_ERR_STATE
- * if a slot has fewer than 64 steps or more than evict_every rows to drop. */
+ * the chronological layout only, and at most 2^20 (slot, layer, KV head)
+ * heads per call (RA_ERR_UNSUPPORTED otherwise); RA_ERR_STATE if a slot has
+ * fewer than 64 steps or more than evict_every rows to drop. */
 ra_status ra_window_select(ra_cache* cache, int32_t seq_lo, int32_t seq_hi,
                            const void* dev_q_window, float* dev_scores,
                            int32_t scores_stride, int32_t* dev_drops, void* stream);
@@ -461,8 +463,9 @@ size_t ra_scored_scratch_bytes(const ra_config* cfg, int32_t max_prompt_len);
  * exceed lp + k_keep; the others are left as they are.  dev_q_window is
  * [max_seqs][L][Hq][64][128] bf16: the queries of each sequence's last 64
  * decode steps, oldest first.  The kept rows stay in chronological order;
- * len becomes lp + k_keep + r.  bf16 and the chronological layout only
- * (RA_ERR_UNSUPPORTED otherwise); RA_ERR_STATE inside an open step, before
+ * len becomes lp + k_keep + r.  bf16 and the chronological layout only, at
+ * most 2^20 (slot, layer, KV head) heads per call (RA_ERR_UNSUPPORTED
+ * otherwise); RA_ERR_STATE inside an open step, before
  * step 64 or when a sequence has more than evict_every rows over its
  * budget; RA_ERR_INVALID_ARG on a bad parameter or a scratch smaller than
  * ra_scored_scratch_bytes.  Asynchronous on `stream`. */

@@ -41,6 +41,23 @@ ra_status hip_fail(hipError_t e) {
 
 int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 
+// The per-(sequence, layer, KV head) kernels (eviction, deferred moves,
+// external rounds' compaction) run one workgroup of up to 1,024 threads per
+// head of the slots given; a range of slots is cut so that one launch holds
+// at most 2^20 workgroups, well inside the dispatch grid's limit.
+constexpr int64_t kMaxHeadsPerLaunch = int64_t(1) << 20;
+
+template <class F>
+hipError_t by_slot_chunks(const ra_config& c, int lo, int hi, F&& launch) {
+  const int64_t per = static_cast<int64_t>(c.num_layers) * c.num_kv_heads;
+  const int chunk = static_cast<int>(std::max<int64_t>(1, kMaxHeadsPerLaunch / per));
+  for (int a = lo; a < hi; a += chunk) {
+    const hipError_t e = launch(a, std::min(hi, a + chunk));
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 // Trigger period of the end-of-step rule; 0 = never (external rounds only).
 int trigger_every(const ra_config& c) {
   return c.policy == RA_POLICY_EXTERNAL ? 0 : c.evict_every;
@@ -312,8 +329,10 @@ ra_status check_decode(const ra_cache* c, int32_t layer, const void* q, const vo
 // or plans another event, runs this first.
 ra_status flush_pending(ra_cache* c, hipStream_t s) {
   if (!c->any_pending()) return RA_OK;
-  RA_LAUNCH(ra::launch_flush_pending(c->shape(), c->meta, c->kpool, c->vpool, c->drops,
-                                     c->cfg.evict_every, c->slot_lo, c->slot_hi, s));
+  RA_LAUNCH(by_slot_chunks(c->cfg, c->slot_lo, c->slot_hi, [&](int lo, int hi) {
+    return ra::launch_flush_pending(c->shape(), c->meta, c->kpool, c->vpool, c->drops,
+                                    c->cfg.evict_every, lo, hi, s);
+  }));
   for (int i = c->slot_lo; i < c->slot_hi; ++i)
     if (c->mirror[i].due == ra::kDueMovePending) c->mirror[i].due = 0;
   return RA_OK;
@@ -416,6 +435,8 @@ ra_status ra_config_check(const ra_config* c) {
       (c->policy == RA_POLICY_BLOCK && c->policy_block < 1) ||
       c->num_kv_heads > 4096)
     return RA_ERR_INVALID_ARG;
+  // kernels with one grid row per (layer, KV head): at most 65,536 of them
+  if (static_cast<int64_t>(c->num_layers) * c->num_kv_heads > 65536) return RA_ERR_UNSUPPORTED;
   if (paged(*c)) {
     if (c->page_rows < 32 || c->page_rows > 1024 || log2_exact(c->page_rows) < 0 ||
         c->max_prompt_len < 0 ||
@@ -746,8 +767,10 @@ ra_status ra_end_step(ra_cache* c, void* stream, int32_t* n_evicted) {
   if (c->graph) {
     // every head's workgroup reads on the device whether its sequence is
     // due; the mirror stays that of the entry into graph mode
-    RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos, c->slot_lo,
-                               c->slot_hi, c->graph_candidates, false, s));
+    RA_LAUNCH(by_slot_chunks(c->cfg, c->slot_lo, c->slot_hi, [&](int lo, int hi) {
+      return ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos, lo, hi,
+                              c->graph_candidates, false, s);
+    }));
     return RA_OK;
   }
   int due = 0;
@@ -773,9 +796,12 @@ ra_status ra_end_step(ra_cache* c, void* stream, int32_t* n_evicted) {
     int n_active = 0;
     for (int i = c->slot_lo; i < c->slot_hi; ++i) n_active += c->mirror[i].active;
     const bool defer = c->drops && due == n_active && attention_plan(c).max_splits == 1;
-    RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos,
-                               c->slot_lo, c->slot_hi, c->max_candidates_due(), defer, s,
-                               defer ? c->drops : nullptr, c->cfg.evict_every));
+    const int candidates = c->max_candidates_due();
+    RA_LAUNCH(by_slot_chunks(c->cfg, c->slot_lo, c->slot_hi, [&](int lo, int hi) {
+      return ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos, lo, hi,
+                              candidates, defer, s, defer ? c->drops : nullptr,
+                              c->cfg.evict_every);
+    }));
     if (defer) {
       RA_LAUNCH(ra::launch_mark_pending(c->meta, c->slot_lo, c->slot_hi, s));
       for (int i = c->slot_lo; i < c->slot_hi; ++i)
@@ -937,8 +963,10 @@ ra_status fast_forward_range(ra_cache* c, int lo, int hi, int32_t n_steps, hipSt
         if (M.due && c->is_paged()) c->shrink(i, M.len);
       }
       if (due && launch) {
-        RA_LAUNCH(ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos, lo, hi,
-                                   candidates, true, s));
+        RA_LAUNCH(by_slot_chunks(c->cfg, lo, hi, [&](int a, int b) {
+          return ra::launch_evict(c->shape(), c->meta, c->kpool, c->vpool, c->pos, a, b,
+                                  candidates, true, s);
+        }));
       }
       remaining -= run;
     }
@@ -1020,6 +1048,9 @@ ra_status ra_window_select(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
   if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (c->cfg.dtype != RA_BF16 || c->cfg.layout != RA_LAYOUT_CHRONOLOGICAL)
     return RA_ERR_UNSUPPORTED;
+  if (static_cast<int64_t>(seq_hi - seq_lo) * c->cfg.num_layers * c->cfg.num_kv_heads >
+      kMaxHeadsPerLaunch)
+    return RA_ERR_UNSUPPORTED;            // one launch per call (measurement only)
   if (c->step_open()) return RA_ERR_STATE;
   int max_len = 0;
   for (int s = seq_lo; s < seq_hi; ++s) {
@@ -1059,6 +1090,9 @@ ra_status ra_scored_evict(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
   if (c->graph) return RA_ERR_STATE;   // needs the host mirror (ra_graph_mode)
   if (prm->scorer < RA_SCORER_SNAPKV || prm->scorer > RA_SCORER_VASE)
     return RA_ERR_INVALID_ARG;
+  if (static_cast<int64_t>(seq_hi - seq_lo) * c->cfg.num_layers * c->cfg.num_kv_heads >
+      kMaxHeadsPerLaunch)
+    return RA_ERR_UNSUPPORTED;            // one launch per call (measurement only)
   if (c->cfg.dtype != RA_BF16 || c->cfg.layout != RA_LAYOUT_CHRONOLOGICAL)
     return RA_ERR_UNSUPPORTED;
   if (prm->scorer == RA_SCORER_RKV &&
@@ -1110,8 +1144,10 @@ ra_status ra_scored_evict(ra_cache* c, int32_t seq_lo, int32_t seq_hi,
   for (int i = c->slot_lo; i < c->slot_hi; ++i) c->mirror[i].due = 0;
   for (int i = seq_lo; i < seq_hi; ++i)
     if (c->mirror[i].active) mirror_plan(c->mirror[i], r, true);
-  RA_LAUNCH(ra::launch_compact_drops(c->shape(), c->meta, c->kpool, c->vpool, c->pos, drops,
-                                     every, seq_lo, seq_hi, s));
+  RA_LAUNCH(by_slot_chunks(c->cfg, seq_lo, seq_hi, [&](int lo, int hi) {
+    return ra::launch_compact_drops(c->shape(), c->meta, c->kpool, c->vpool, c->pos, drops,
+                                    every, lo, hi, s);
+  }));
   return RA_OK;
 }
 

@@ -48,7 +48,8 @@ def test_config_validation():
             setattr(c, k, v)
         assert B.ra_config_check(c) == B.RA_ERR_INVALID_ARG, kw
     unsupported = [dict(head_dim=64), dict(num_q_heads=136, num_kv_heads=8),
-                   dict(evict_every=2048), dict(budget_k=40000)]
+                   dict(evict_every=2048), dict(budget_k=40000),
+                   dict(num_layers=4096, num_q_heads=32, num_kv_heads=32)]   # L * Hkv > 65536
     for kw in unsupported:
         c = B.make_config(40, 40, 8, 8192, max_seqs=32)
         for k, v in kw.items():
