@@ -387,6 +387,11 @@ ra_status launch_decode(ra_cache* c, int32_t layer, const void* q, const void* k
   a.arrivals = c->arrivals;
   a.waves = plan.waves;
   a.wide_regs = plan.wide_regs;
+  // fp32 heads of several splits: merged by their last split, which spares
+  // a launch and its gap; in graph mode the launches follow each other with
+  // no gap and the merge kernel (256 threads per head, against the 64 of a
+  // split) is the faster of the two
+  a.merge_kernel = c->graph ? 1 : 0;
   if (move) {
     a.move = 1;
     a.waves = 8;

@@ -200,7 +200,7 @@ __device__ __forceinline__ float load_shared_level(const float* p) {
 }
 
 // The split partials of one head merged by the last of its splits to finish
-// (bf16 attention).  Every split stores its partials with store_shared_level
+// (outputs of element type E: bf16 bits or float).  Every split stores its partials with store_shared_level
 // and waits until they are written; then one thread counts the split on the
 // head's arrival counter.  The split that brings the count to nsplit reads
 // every split's partials with load_shared_level, merges them as
@@ -209,6 +209,7 @@ __device__ __forceinline__ float load_shared_level(const float* p) {
 // thread of the workgroup after its partials are stored; the head and its
 // split count are taken afresh from the grid position and the slot record
 // (kept from before the key loop, they would take registers the loop needs).
+template <typename E>
 __device__ void merge_if_last(const AttnLaunch& a, int G, int Hq, int Hkv) {
   __shared__ float sm[kMaxSplits * kMaxGroup];   // split maxima, then weights
   __shared__ float sl[kMaxSplits * kMaxGroup];   // split sums
@@ -266,8 +267,11 @@ __device__ void merge_if_last(const AttnLaunch& a, int G, int Hq, int Hkv) {
     inv_l[t] = 1.f / lsum;
   }
   __syncthreads();
-  uint16_t* out = static_cast<uint16_t*>(a.out) +
-                  (static_cast<int64_t>(slot) * Hq + g * G) * kHeadDim;
+  E* out = static_cast<E*>(a.out) + (static_cast<int64_t>(slot) * Hq + g * G) * kHeadDim;
+  const auto put = [&](int idx, float o) {
+    if constexpr (sizeof(E) == 2) out[idx] = f32_to_bf16(o);
+    else out[idx] = o;
+  };
   if (fast) {
 #pragma unroll
     for (int j = 0; j < kFastItems; ++j) {
@@ -278,7 +282,7 @@ __device__ void merge_if_last(const AttnLaunch& a, int G, int Hq, int Hkv) {
 #pragma unroll
       for (int s = 0; s < kFastSplits; ++s)
         if (s < nsplit) o += pv[j][s] * sm[s * G + q];
-      out[idx] = f32_to_bf16(o * inv_l[q]);
+      put(idx, o * inv_l[q]);
     }
     return;
   }
@@ -287,7 +291,7 @@ __device__ void merge_if_last(const AttnLaunch& a, int G, int Hq, int Hkv) {
     float o = 0.f;
     for (int s = 0; s < nsplit; ++s)
       o += load_shared_level(po + (s * G) * kHeadDim + idx) * sm[s * G + q];
-    out[idx] = f32_to_bf16(o * inv_l[q]);
+    put(idx, o * inv_l[q]);
   }
 }
 
@@ -627,7 +631,7 @@ __global__ __launch_bounds__(64 * W, MINW) void attn_bf16_kernel(
     }
   }
   if constexpr (kFusedMerge) {
-    if (w.nsplit > 1) merge_if_last(a, G, Hq, Hkv);
+    if (w.nsplit > 1) merge_if_last<uint16_t>(a, G, Hq, Hkv);
   }
 }
 
@@ -1031,20 +1035,52 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnLaunch a, Paging pg, i
                       static_cast<float*>(a.kpool),
                       static_cast<float*>(a.vpool), a.pos);
 
+  // one split: the normalised output; several: the partials, merged by the
+  // split that finishes last (merge_if_last) or, with merge_kernel, by the
+  // merge kernel launched next
   const int head = w.slot * Hkv + w.g;
+  if (w.nsplit == 1) {
+    float* out = static_cast<float*>(a.out) +
+                 (static_cast<int64_t>(w.slot) * Hq + w.g * G) * kHeadDim;
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      if (GT > 0 || q < G) {
+        const float inv = 1.f / l[q];
+        out[q * kHeadDim + lane] = acc[q][0] * inv;
+        out[q * kHeadDim + lane + 64] = acc[q][1] * inv;
+      }
+    }
+    return;
+  }
   const int64_t item = static_cast<int64_t>(head) * a.split_stride + w.split;
+  if (a.merge_kernel) {
+#pragma unroll
+    for (int q = 0; q < kQ; ++q) {
+      if (GT > 0 || q < G) {
+        float* po = a.ws_o + (item * G + q) * kHeadDim;
+        po[lane] = acc[q][0];
+        po[lane + 64] = acc[q][1];
+        if (lane == 0) {
+          a.ws_ml[(item * G + q) * 2] = m[q];
+          a.ws_ml[(item * G + q) * 2 + 1] = l[q];
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int q = 0; q < kQ; ++q) {
     if (GT > 0 || q < G) {
       float* po = a.ws_o + (item * G + q) * kHeadDim;
-      po[lane] = acc[q][0];
-      po[lane + 64] = acc[q][1];
+      store_shared_level(po + lane, acc[q][0]);
+      store_shared_level(po + lane + 64, acc[q][1]);
       if (lane == 0) {
-        a.ws_ml[(item * G + q) * 2] = m[q];
-        a.ws_ml[(item * G + q) * 2 + 1] = l[q];
+        store_shared_level(a.ws_ml + (item * G + q) * 2, m[q]);
+        store_shared_level(a.ws_ml + (item * G + q) * 2 + 1, l[q]);
       }
     }
   }
+  merge_if_last<float>(a, G, Hq, Hkv);
 }
 
 template <int GT, bool PAGED>
@@ -1098,8 +1134,9 @@ hipError_t launch_attention_t(const Shape& sh, const AttnLaunch& a, hipStream_t 
       case 8: launch_f32<8, PAGED>(grid, s, a, sh, scale_log2); break;
       default: launch_f32<0, PAGED>(grid, s, a, sh, scale_log2); break;
     }
-    hipLaunchKernelGGL(combine_kernel<float>, cgrid, dim3(256), 0, s, a, sh.G, sh.Hq, sh.Hkv,
-                       false);
+    if (a.merge_kernel && a.max_splits > 1)
+      hipLaunchKernelGGL(combine_kernel<float>, cgrid, dim3(256), 0, s, a, sh.G, sh.Hq,
+                         sh.Hkv, true);
   }
   return hipGetLastError();
 }

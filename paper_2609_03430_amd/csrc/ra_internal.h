@@ -166,6 +166,9 @@ struct AttnLaunch {
   // some sequence has a deferred row move (bf16, one split per head): the
   // launch runs the kernel that moves rows while it attends
   int move;
+  // fp32: heads of several splits are merged by a merge kernel launched after
+  // the attention (1) instead of by their last split (0)
+  int merge_kernel;
   const int32_t* drops;  // the deferred drop lists (see launch_evict)
   int drop_stride;
   // bf16: per (slot, KV head) count of the splits done this launch, zero
