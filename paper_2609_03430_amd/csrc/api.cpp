@@ -45,7 +45,10 @@ int64_t round_up(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 // external rounds' compaction) run one workgroup of up to 1,024 threads per
 // head of the slots given; a range of slots is cut so that one launch holds
 // at most 2^20 workgroups, well inside the dispatch grid's limit.
-constexpr int64_t kMaxHeadsPerLaunch = int64_t(1) << 20;
+#ifndef RA_MAX_HEADS_PER_LAUNCH
+#define RA_MAX_HEADS_PER_LAUNCH (1 << 20)   // smaller in the host-only test build
+#endif
+constexpr int64_t kMaxHeadsPerLaunch = RA_MAX_HEADS_PER_LAUNCH;
 
 template <class F>
 hipError_t by_slot_chunks(const ra_config& c, int lo, int hi, F&& launch) {

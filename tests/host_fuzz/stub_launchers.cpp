@@ -173,10 +173,18 @@ hipError_t launch_append_positions(const Shape&, const SeqMeta* meta, int32_t*, 
   return hipSuccess;
 }
 
-hipError_t launch_evict(const Shape&, const SeqMeta* meta, void*, void*, int32_t*, int slot_lo,
+// The test build cuts per-head launches into chunks of at most 3 heads, or
+// one slot where a slot has more (RA_MAX_HEADS_PER_LAUNCH=3).
+void check_chunk(const Shape& sh, int slot_lo, int slot_hi, const char* what) {
+  if (slot_hi - slot_lo > 1 && (slot_hi - slot_lo) * sh.L * sh.Hkv > 3)
+    fail(what, slot_lo, slot_hi);
+}
+
+hipError_t launch_evict(const Shape& sh, const SeqMeta* meta, void*, void*, int32_t*, int slot_lo,
                         int slot_hi, int max_candidates, bool, hipStream_t, int32_t* drops_out,
                         int drop_stride) {
   if (slot_lo < 0 || slot_hi > g_max_seqs || slot_lo >= slot_hi) fail("evict range", slot_lo, slot_hi);
+  check_chunk(sh, slot_lo, slot_hi, "evict launch over the per-launch bound");
   if (max_candidates < 0 || max_candidates > kMaxCandidates) fail("candidates", max_candidates, 0);
   if (drops_out && (drop_stride < 1 || drop_stride > kMaxEvery)) fail("drop stride", drop_stride, 0);
   touch_read(meta + slot_lo, sizeof(SeqMeta) * (slot_hi - slot_lo));
@@ -197,10 +205,11 @@ hipError_t launch_clear_pending(SeqMeta* meta, int slot_lo, int slot_hi, hipStre
   return hipSuccess;
 }
 
-hipError_t launch_flush_pending(const Shape&, SeqMeta* meta, void*, void*, const int32_t* drops,
+hipError_t launch_flush_pending(const Shape& sh, SeqMeta* meta, void*, void*, const int32_t* drops,
                                 int drop_stride, int slot_lo, int slot_hi, hipStream_t) {
   if (slot_lo < 0 || slot_hi > g_max_seqs || !drops || drop_stride < 1)
     fail("flush", slot_lo, drop_stride);
+  check_chunk(sh, slot_lo, slot_hi, "flush launch over the per-launch bound");
   return launch_clear_pending(meta, slot_lo, slot_hi, nullptr);   // as the device's does
 }
 
@@ -274,8 +283,9 @@ hipError_t scratch_address(void** out) {
   return hipSuccess;
 }
 
-hipError_t launch_compact_drops(const Shape&, const SeqMeta*, void*, void*, int32_t*,
-                                const int32_t*, int, int, int, hipStream_t) {
+hipError_t launch_compact_drops(const Shape& sh, const SeqMeta*, void*, void*, int32_t*,
+                                const int32_t*, int, int slot_lo, int slot_hi, hipStream_t) {
+  check_chunk(sh, slot_lo, slot_hi, "compaction launch over the per-launch bound");
   return hipSuccess;
 }
 

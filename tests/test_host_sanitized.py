@@ -56,7 +56,10 @@ def fuzzer(tmp_path_factory):
     common = ["-O1", "-g", "-std=c++17", "-I" + os.path.join(ROOT, "include")]
     san = ["-fsanitize=address,undefined", "-fno-sanitize-recover=all"]
     # HIP sources for the host pass only; each sanitizer flag for the host
-    hip = [HIPCC, "-x", "hip", "--cuda-host-only", "-I" + CSRC] + common + [
+    # launches of per-head kernels cut into chunks of one slot (3 heads at
+    # most), so that the chunked launch loops run under the sanitizers too
+    hip = [HIPCC, "-x", "hip", "--cuda-host-only", "-I" + CSRC,
+           "-DRA_MAX_HEADS_PER_LAUNCH=3"] + common + [
         "-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
         "-fno-sanitize-recover=all"]
     objs = []
