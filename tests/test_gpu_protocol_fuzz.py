@@ -11,8 +11,9 @@ meanwhile) and resumed in a free slot, and graph mode entered (steps then run
 in it) and left.  Every output of every step is checked against the fp64
 oracle; the kept sets after every step with an event, and the rows after
 explicit events, fast forwards, resumes, leaving graph mode, at a quarter of
-the events and at the end.  The paged layout's refusals for lack of pages
-are met by ending a sequence, as a serving loop would.
+the events and at the end.  Half of the paged cases get a pool of about 60%
+of what their slots could hold; the refusals of steps for lack of pages are
+met by ending a sequence, as a serving loop would.
 """
 
 import numpy as np
@@ -46,13 +47,24 @@ class Fuzz:
                         r=int(rng.choice([0, 4, 8])), every=int(rng.choice([1, 4, 8, 16])),
                         split=int(rng.choice([0, 4096])), page_rows=int(rng.choice([32, 64])))
         c = self.cfg
+        pool = None
+        if self.layout == B.RA_LAYOUT_PAGED and seed % 2:
+            # the pool at ~60% of what every slot could hold: steps are refused
+            # for lack of pages and a sequence is preempted, as a serving loop would
+            probe = B.make_config(self.L, self.Hkv * G, self.Hkv, K, c["r"], c["every"], mode,
+                                  self.dtype, self.max_seqs, layout=self.layout,
+                                  page_rows=c["page_rows"], max_prompt_len=self.maxlp)
+            group = self.L * self.Hkv * c["page_rows"]
+            full = self.max_seqs * B.ra_seq_rows(probe, self.maxlp)
+            pool = max(2 * group, int(full * 0.6) // group * group)
+            c["pool"] = pool
         self.run = Run(L=self.L, Hq=self.Hkv * G, Hkv=self.Hkv, K=K, lps=[self.maxlp] * self.max_seqs,
                        r=c["r"], every=c["every"], dtype=self.dtype, mode=mode,
                        layout=self.layout, policy=policy,
                        block=int(rng.integers(1, 6)) if policy == B.RA_POLICY_BLOCK else 1,
                        begin=False, max_seqs=self.max_seqs, attn_split=c["split"],
                        page_rows=c["page_rows"], max_prompt_len=self.maxlp,
-                       wl_seed=300 + seed)
+                       wl_seed=300 + seed, pool_rows=pool)
         self.run.active = set()
         self.oracles, self.explicit = {}, {}
         self.n_req = 0
