@@ -334,9 +334,9 @@ __global__ __launch_bounds__(NT) void evict_kernel(
       int p;
       if constexpr (PAGED) p = pos[prow(lp + c)];
       else p = P[lp + c];
-      if (p < thr) {
+      tie[i] = static_cast<uint32_t>(p);     // kept for every slot: the
+      if (p < thr) {                         // positions-only compaction below
         score[i] = policy_key(policy, block, p, lp, event, layer, g, seed, rid);
-        tie[i] = static_cast<uint32_t>(p);
         valid |= 1u << i;
       }
     }
@@ -344,7 +344,7 @@ __global__ __launch_bounds__(NT) void evict_kernel(
 
   // 2. radix select of the m smallest (score, position); 3. drop list
   const uint32_t drop = select_smallest<NT, KPT, 64>(score, tie, valid, m, sel_sh);
-  drop_list<NT, KPT>(drop, lp, f, sel_sh);
+  const int drops_below = drop_list<NT, KPT>(drop, lp, f, sel_sh);
   const int d0 = f[0];
   // deferred row moves: this head's drop slots, ascending, for the next
   // step's attention (rows are left in place by a positions-only event)
@@ -392,6 +392,36 @@ __global__ __launch_bounds__(NT) void evict_kernel(
 
   // 4. order-preserving in-place compaction of positions, keys and values
   __shared__ int src_of[chunk_rows<NT, E>()];
+  if constexpr (POS_ONLY) {
+    // Positions only: every slot below old_len - r was read into tie[] before
+    // the selection's barriers, so each survivor among them goes straight to
+    // its compacted slot (its slot less the drops below it), with no read of
+    // the region after those barriers.  Only the r most recent rows, above
+    // every candidate, take the chunked move: their sources lie above every
+    // destination written here.
+    int k = drops_below;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int c = t * KPT + i;
+      if (c < span) {
+        if ((drop >> i) & 1) {
+          ++k;
+        } else if (k) {
+          if constexpr (PAGED) pos[prow(lp + c - k)] = static_cast<int32_t>(tie[i]);
+          else P[lp + c - k] = static_cast<int32_t>(tie[i]);
+        }
+      }
+    }
+    if (r > 0) {
+      if constexpr (PAGED)
+        compact_rows<NT, E, true>(f, m, src_of, new_len - r, new_len, old_len, prow, kpool,
+                                  vpool, pos);
+      else
+        compact_rows<NT, E, true>(f, m, src_of, new_len - r, new_len, old_len,
+                                  RegionRows{region}, kpool, vpool, P);
+    }
+    return;
+  }
   if constexpr (PAGED)
     compact_rows<NT, E, POS_ONLY>(f, m, src_of, d0, new_len, old_len, prow, kpool, vpool, pos);
   else

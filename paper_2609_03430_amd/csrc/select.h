@@ -99,9 +99,10 @@ __device__ __forceinline__ uint32_t select_smallest(const uint64_t (&key)[KPT],
 }
 
 // Writes the dropped candidates' slots, ascending, as f[k] = slot_k - k
-// (slot = slot0 + candidate index).  Ends with a barrier.
+// (slot = slot0 + candidate index).  Ends with a barrier.  Returns the
+// number of dropped candidates held by lower threads.
 template <int NT, int KPT>
-__device__ __forceinline__ void drop_list(uint32_t drop, int slot0, int* f, SelectShared& sh) {
+__device__ __forceinline__ int drop_list(uint32_t drop, int slot0, int* f, SelectShared& sh) {
   const int t = threadIdx.x;
   const int mine = __popc(drop);
   const int incl = wave_inclusive_scan(mine);
@@ -109,6 +110,7 @@ __device__ __forceinline__ void drop_list(uint32_t drop, int slot0, int* f, Sele
   __syncthreads();
   int k = incl - mine;
   for (int w = 0; w < (t >> 6); ++w) k += sh.wave_tot[w];
+  const int before = k;
 #pragma unroll
   for (int i = 0; i < KPT; ++i) {
     if ((drop >> i) & 1) {
@@ -117,6 +119,7 @@ __device__ __forceinline__ void drop_list(uint32_t drop, int slot0, int* f, Sele
     }
   }
   __syncthreads();
+  return before;
 }
 
 }  // namespace ra
