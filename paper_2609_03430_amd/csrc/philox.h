@@ -17,6 +17,20 @@
 
 namespace ra {
 
+// Full 128-bit product of two 64-bit words from four 32 x 32 -> 64-bit
+// multiply-adds (schoolbook, 32-bit limbs; no partial sum exceeds 64 bits:
+// each is at most (2^32 - 1)^2 + 2 (2^32 - 1) = 2^64 - 1).
+__device__ __forceinline__ void mul_64x64(uint64_t a, uint64_t b, uint64_t& hi,
+                                          uint64_t& lo) {
+  const uint64_t a0 = static_cast<uint32_t>(a), a1 = a >> 32;
+  const uint64_t b0 = static_cast<uint32_t>(b), b1 = b >> 32;
+  const uint64_t t = a0 * b0;
+  const uint64_t u = a1 * b0 + (t >> 32);
+  const uint64_t v = a0 * b1 + (u & 0xffffffffull);
+  hi = a1 * b1 + (u >> 32) + (v >> 32);
+  lo = (v << 32) | (t & 0xffffffffull);
+}
+
 __device__ __forceinline__ uint64_t philox_score(uint64_t p, uint64_t e,
                                                  uint64_t l, uint64_t g,
                                                  uint64_t seed, uint64_t rid) {
@@ -32,8 +46,9 @@ __device__ __forceinline__ uint64_t philox_score(uint64_t p, uint64_t e,
       k0 += kW0;
       k1 += kW1;
     }
-    const uint64_t hi0 = __umul64hi(kM0, c0), lo0 = kM0 * c0;
-    const uint64_t hi1 = __umul64hi(kM1, c2), lo1 = kM1 * c2;
+    uint64_t hi0, lo0, hi1, lo1;
+    mul_64x64(kM0, c0, hi0, lo0);
+    mul_64x64(kM1, c2, hi1, lo1);
     const uint64_t n0 = hi1 ^ c1 ^ k0;
     const uint64_t n2 = hi0 ^ c3 ^ k1;
     c0 = n0;
