@@ -1,5 +1,5 @@
 """Shared test setup: the ``gpu`` marker, the import path, and a record of
-each GPU test's worst errors (gpurun_out/parity_records.jsonl)."""
+each GPU test's worst errors (parity_records.jsonl, one JSON line per test)."""
 
 import os
 import sys

@@ -219,8 +219,8 @@ def _f64(x):
     return np.asarray(x, dtype=np.float64)
 
 
-# Worst figures of the running test, written to a record at its end (see
-# conftest.py): the GPU machine's gpurun_out/ comes back with the run.
+# Worst figures of the running test, appended to a JSON-lines record at its
+# end (see conftest.py), in the repository's output folder for remote runs.
 _WORST = {}
 RECORD = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
                       "gpurun_out", "parity_records.jsonl")
