@@ -334,8 +334,10 @@ __global__ __launch_bounds__(NT) void evict_kernel(
       int p;
       if constexpr (PAGED) p = pos[prow(lp + c)];
       else p = P[lp + c];
-      tie[i] = static_cast<uint32_t>(p);     // kept for every slot: the
-      if (p < thr) {                         // positions-only compaction below
+      // every slot's position is kept (not only the candidates'): the
+      // positions-only compaction below writes the survivors from here
+      tie[i] = static_cast<uint32_t>(p);
+      if (p < thr) {
         score[i] = policy_key(policy, block, p, lp, event, layer, g, seed, rid);
         valid |= 1u << i;
       }
