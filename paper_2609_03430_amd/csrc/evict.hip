@@ -73,6 +73,12 @@ __device__ __forceinline__ uint64_t policy_key(int policy, int block, int p, int
   }
 }
 
+// The position whose draw scores position p under `policy`: the block-wise
+// policy draws once per block of `block` positions from the prompt's end.
+__device__ __forceinline__ int draw_position(int policy, int block, int p, int lp) {
+  return policy == 2 ? lp + (p - lp) / block * block : p;
+}
+
 // Number of drops d_k (= f[k] + k, ascending) with d_k <= x.
 __device__ __forceinline__ int count_le_slot(const int* f, int m, int x) {
   int lo = 0, hi = m;
@@ -338,8 +344,53 @@ __global__ __launch_bounds__(NT) void evict_kernel(
       // positions-only compaction below writes the survivors from here
       tie[i] = static_cast<uint32_t>(p);
       if (p < thr) {
-        score[i] = policy_key(policy, block, p, lp, event, layer, g, seed, rid);
+        // the largest builds draw per candidate as it is read
+        if (KPT > 9) score[i] = policy_key(policy, block, p, lp, event, layer, g, seed, rid);
         valid |= 1u << i;
+      }
+    }
+  }
+  if (KPT <= 9) {
+    // The keys of every slot (a slot that is no candidate keeps a zero key,
+    // which the selection ignores), three Philox blocks in lockstep: their
+    // independent rounds interleave, where one conditional draw per candidate
+    // runs each 10-round chain of dependent multiplies on its own.  The
+    // policy is the same for the whole workgroup.
+    if (policy == 3) {
+#pragma unroll
+      for (int i = 0; i < KPT; ++i)
+        score[i] = (valid >> i) & 1 ? policy_key(3, block, static_cast<int>(tie[i]), lp, event,
+                                                 layer, g, seed, rid)
+                                    : 0;
+    } else {
+      int q[KPT];
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) q[i] = static_cast<int>(tie[i]);
+      if (policy == 2) {
+#pragma unroll
+        for (int i = 0; i < KPT; ++i) q[i] = draw_position(2, block, q[i], lp);
+      }
+      const uint64_t dl = policy == 1 ? 0 : static_cast<uint64_t>(layer);
+      const uint64_t dg = policy == 1 ? 0 : static_cast<uint64_t>(g);
+      constexpr int kWays = 3;
+#pragma unroll
+      for (int i0 = 0; i0 < KPT; i0 += kWays) {
+        uint64_t b[kWays], w[kWays][4];
+#pragma unroll
+        for (int j = 0; j < kWays; ++j)
+          b[j] = i0 + j < KPT ? static_cast<uint64_t>(q[i0 + j] >> 2) : 0;
+        philox_blocks<kWays>(b, static_cast<uint64_t>(event), dl, dg, seed, rid, w);
+#pragma unroll
+        for (int j = 0; j < kWays; ++j) {
+          if (i0 + j < KPT) {
+            // word k of the block, by masks (a select chain becomes branches)
+            const int i = i0 + j, k = q[i] & 3;
+            uint64_t x = 0;
+#pragma unroll
+            for (int n = 0; n < 4; ++n) x |= w[j][n] & (0ull - static_cast<uint64_t>(k == n));
+            score[i] = x & (0ull - static_cast<uint64_t>((valid >> i) & 1));
+          }
+        }
       }
     }
   }

@@ -60,4 +60,44 @@ __device__ __forceinline__ uint64_t philox_score(uint64_t p, uint64_t e,
   return w == 0 ? c0 : (w == 1 ? c1 : (w == 2 ? c2 : c3));
 }
 
+// N blocks at counters (b[j], e, l, g), key (seed, rid), evaluated in
+// lockstep so that their independent rounds interleave; w[j][i] is word i of
+// block j (the scores of positions 4 b[j] .. 4 b[j] + 3).
+template <int N>
+__device__ __forceinline__ void philox_blocks(const uint64_t (&b)[N], uint64_t e, uint64_t l,
+                                              uint64_t g, uint64_t seed, uint64_t rid,
+                                              uint64_t (&w)[N][4]) {
+  constexpr uint64_t kM0 = 0xD2E7470EE14C6C93ull;
+  constexpr uint64_t kM1 = 0xCA5A826395121157ull;
+  constexpr uint64_t kW0 = 0x9E3779B97F4A7C15ull;
+  constexpr uint64_t kW1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    w[j][0] = b[j];
+    w[j][1] = e;
+    w[j][2] = l;
+    w[j][3] = g;
+  }
+  uint64_t k0 = seed, k1 = rid;
+#pragma unroll
+  for (int round = 0; round < 10; ++round) {
+    if (round) {
+      k0 += kW0;
+      k1 += kW1;
+    }
+#pragma unroll
+    for (int j = 0; j < N; ++j) {
+      uint64_t hi0, lo0, hi1, lo1;
+      mul_64x64(kM0, w[j][0], hi0, lo0);
+      mul_64x64(kM1, w[j][2], hi1, lo1);
+      const uint64_t n0 = hi1 ^ w[j][1] ^ k0;
+      const uint64_t n2 = hi0 ^ w[j][3] ^ k1;
+      w[j][0] = n0;
+      w[j][1] = lo1;
+      w[j][2] = n2;
+      w[j][3] = lo0;
+    }
+  }
+}
+
 }  // namespace ra
